@@ -1,0 +1,416 @@
+"""CPU oracle for one compressed-MoE decode layer (test infrastructure only).
+
+This module is TEST INFRASTRUCTURE. Only the test suite, the smoke check in
+``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``bench.py`` may
+import it. The product path (the HIP library and its Python binding) never
+imports, calls or links anything here, and this module imports nothing from
+the product package.
+
+It is a plain, slow, obviously-correct float64 numpy implementation of what
+the hot path computes, written from the paper:
+
+* MoE block semantics (Sec. 2.1): a router picks ``k`` of ``E`` experts for an
+  input ``h`` and assigns each an affinity ``a_e``; each selected expert runs
+  gate and up projections, combines them with the activation ``phi`` into
+  ``p_e``, maps ``p_e`` back to the hidden size with its down projection, and
+  the block returns the affinity-weighted sum of the expert outputs.
+* Hybrid representation (Sec. 3.1, Eq. (1)): an expert matrix is a blockwise
+  VQ part ``Q_B(J_e)`` (Sec. 2.3: each column is cut into length-``d`` blocks
+  running along the input dimension, each block replaced by a code word of the
+  shared code book ``B``) plus a low-rank part ``D C_e`` on a basis ``D`` shared
+  by all experts.
+* Storage rate (Sec. 5.5 display and Appendix A.2, Eq. (7)).
+
+Readings where the paper is silent (recorded with the rest in the design doc):
+
+* The down projection is compressed as ``Q_e + A_e B`` with ``B`` [r, H]
+  shared on the output side (the workload definition; the paper itself keeps
+  down in BF16, Sec. 3.1).
+* ``phi`` is SiLU gating: ``p = silu(g) * u``.
+* Top-k order is descending logit with exact ties going to the lower expert
+  index; the bias is part of the logit; gating is a softmax over the k
+  selected logits.
+* Inside a code block, code-word element ``i`` maps to input row ``b*d + i``.
+
+Functions:
+
+* ``moe_layer``            -- O1: dense reconstruction of every selected
+                              expert's matrices, then plain matmuls.
+* ``moe_layer_factored``   -- O3: Eq. (1) evaluated in factored form,
+                              ``Q^T x + V^T (U^T x)`` (gate/up) and
+                              ``Q^T p + B^T (A^T p)`` (down).
+* ``moe_layer_scalar``     -- O2: pure-Python scalar loops for tiny shapes.
+
+All bf16 inputs arrive as raw uint16 bit patterns and are widened exactly.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+LAYER_KEYS = (
+    "router_w", "router_bias",
+    "cb_gate", "cb_up", "cb_down",
+    "codes_gate", "codes_up", "codes_down",
+    "U_gate", "U_up", "V_gate", "V_up",
+    "A_down", "B_down",
+)
+
+
+# --------------------------------------------------------------------------
+# exact widening of stored inputs
+# --------------------------------------------------------------------------
+def bf16_to_f64(bits) -> np.ndarray:
+    """Widen raw bf16 bit patterns (uint16) to float64 exactly.
+
+    A bf16 value is the upper half of an IEEE binary32 word, so shifting the
+    16 stored bits into the high half of a uint32 gives the binary32 value,
+    which float64 represents exactly.
+    """
+    b = np.ascontiguousarray(np.asarray(bits, dtype=np.uint16))
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def _f(a) -> np.ndarray:
+    """Float64 view of an input: bf16 bit patterns are widened, floats cast."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return bf16_to_f64(a)
+    return a.astype(np.float64)
+
+
+# --------------------------------------------------------------------------
+# router (Sec. 2.1)
+# --------------------------------------------------------------------------
+def router_logits(x, router_w, router_bias=None) -> np.ndarray:
+    """Router scores ``l[t, e] = sum_h x[t, h] * Wr[h, e] + bias[e]`` (Sec. 2.1)."""
+    xf = _f(x)
+    wr = _f(router_w)
+    logits = xf @ wr
+    if router_bias is not None:
+        logits = logits + _f(router_bias)[None, :]
+    return logits
+
+
+def select_topk(logits, k: int):
+    """Pick the ``k`` largest logits per token (Sec. 2.1).
+
+    Experts are ordered by the key ``(-logit, expert)``, i.e. by descending
+    logit with exact ties resolved toward the lower expert index, using a plain
+    Python sort. Returns ``(idx [B, k] int64, margin [B])`` where ``margin`` is
+    the gap between the k-th and (k+1)-th logit (``inf`` when k == E).
+    """
+    logits = np.asarray(logits, dtype=np.float64)
+    B, E = logits.shape
+    idx = np.zeros((B, k), dtype=np.int64)
+    margin = np.full(B, np.inf)
+    for t in range(B):
+        order = sorted(range(E), key=lambda e: (-logits[t, e], e))
+        idx[t] = order[:k]
+        if k < E:
+            margin[t] = logits[t, order[k - 1]] - logits[t, order[k]]
+    return idx, margin
+
+
+def gating(logits, idx) -> np.ndarray:
+    """Affinities ``a``: a softmax over the k selected logits of each token."""
+    logits = np.asarray(logits, dtype=np.float64)
+    sel = np.take_along_axis(logits, np.asarray(idx), axis=1)
+    w = np.exp(sel - sel.max(axis=1, keepdims=True))
+    return w / w.sum(axis=1, keepdims=True)
+
+
+def route(x, router_w, router_bias, k: int):
+    """Router + top-k + gating: returns ``(idx, a, margin, logits)``."""
+    logits = router_logits(x, router_w, router_bias)
+    idx, margin = select_topk(logits, k)
+    return idx, gating(logits, idx), margin, logits
+
+
+# --------------------------------------------------------------------------
+# hybrid representation (Sec. 2.3 and Sec. 3.1, Eq. (1))
+# --------------------------------------------------------------------------
+def decode_vq(codes, codebook, d: int) -> np.ndarray:
+    """Blockwise VQ matrix ``Q_B(J)`` (Sec. 2.3).
+
+    ``codes`` is the index map ``J`` of shape ``[n_in / d, n_out]``; every
+    column of the reconstructed ``[n_in, n_out]`` matrix is cut into
+    length-``d`` blocks along the input dimension and block ``b`` of column
+    ``j`` is the code word ``codebook[J[b, j]]``, so that
+    ``Q[b*d + i, j] = codebook[J[b, j], i]``.
+    """
+    J = np.asarray(codes).astype(np.int64)
+    cb = _f(codebook)
+    nb, n_out = J.shape
+    assert cb.shape[1] == d
+    blocks = cb[J]                      # [nb, n_out, d]: code word of block (b, j)
+    return blocks.transpose(0, 2, 1).reshape(nb * d, n_out)
+
+
+def expert_matrices(layer: dict, e: int, d: int):
+    """Dense reconstructions of expert ``e``'s gate, up and down matrices.
+
+    Gate/up follow Eq. (1): ``W = Q_B(J_e) + D C_e`` with ``D = U`` [H, r]
+    and ``C_e = V_e`` [r, I], giving [H, I]. Down is ``Q_B(J^d_e) + A_e B``
+    with ``A_e`` [I, r] private and ``B`` [r, H] shared, giving [I, H].
+    """
+    Wg = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d)
+    Wu = decode_vq(layer["codes_up"][e], layer["cb_up"], d)
+    Wd = decode_vq(layer["codes_down"][e], layer["cb_down"], d)
+    r = 0 if layer.get("U_gate") is None else _f(layer["U_gate"]).shape[1]
+    if r > 0:
+        Wg = Wg + _f(layer["U_gate"]) @ _f(layer["V_gate"][e])
+        Wu = Wu + _f(layer["U_up"]) @ _f(layer["V_up"][e])
+        Wd = Wd + _f(layer["A_down"][e]) @ _f(layer["B_down"])
+    return Wg, Wu, Wd
+
+
+def silu(g):
+    """SiLU ``g * sigmoid(g)``, the gating activation phi of the workload."""
+    g = np.asarray(g, dtype=np.float64)
+    return g / (1.0 + np.exp(-g))
+
+
+def shared_proj(x, U) -> np.ndarray:
+    """Shared rank-r projection ``z = D^T h`` for every token (Sec. 4.2)."""
+    return _f(x) @ _f(U)
+
+
+# --------------------------------------------------------------------------
+# O1: the layer from dense reconstructions
+# --------------------------------------------------------------------------
+def expert_ffn(x, idx, a, layer: dict, d: int) -> np.ndarray:
+    """Expert computation plus the affinity-weighted sum for fixed routing.
+
+    For token ``t`` and its j-th selected expert ``e``: ``g = Wg^T x_t``,
+    ``u = Wu^T x_t``, ``p = silu(g) * u``, ``y_e = Wd^T p``; the output is
+    ``sum_j a[t, j] * y_e`` summed in selection order (Sec. 2.1).
+    """
+    xf = _f(x)
+    idx = np.asarray(idx)
+    a = np.asarray(a, dtype=np.float64)
+    B = xf.shape[0]
+    H = xf.shape[1]
+    y = np.zeros((B, H))
+    cache = {}
+    for t in range(B):
+        for j in range(idx.shape[1]):
+            e = int(idx[t, j])
+            if e not in cache:
+                cache[e] = expert_matrices(layer, e, d)
+            Wg, Wu, Wd = cache[e]
+            g = Wg.T @ xf[t]
+            u = Wu.T @ xf[t]
+            p = silu(g) * u
+            y[t] += a[t, j] * (Wd.T @ p)
+    return y
+
+
+def moe_layer(x, layer: dict, k: int, d: int):
+    """O1: route, then run the selected experts from dense reconstructions.
+
+    Returns ``(y [B, H] f64, idx [B, k], a [B, k], margin [B])``.
+    """
+    idx, a, margin, _ = route(x, layer["router_w"], layer.get("router_bias"), k)
+    y = expert_ffn(x, idx, a, layer, d)
+    return y, idx, a, margin
+
+
+# --------------------------------------------------------------------------
+# O3: Eq. (1) in factored form
+# --------------------------------------------------------------------------
+def expert_ffn_factored(x, idx, a, layer: dict, d: int, z=None) -> np.ndarray:
+    """Same result as ``expert_ffn`` evaluated as in Eq. (1).
+
+    Gate/up: ``o = Q_B(J_e)^T x + V_e^T (U^T x)`` with the shared projection
+    ``U^T x`` computed once per token (Sec. 4.2); down:
+    ``y_e = Q_B(J^d_e)^T p + B^T (A_e^T p)``. ``z`` optionally supplies the
+    shared projections as ``[2, B, r]`` (gate, up).
+    """
+    xf = _f(x)
+    idx = np.asarray(idx)
+    a = np.asarray(a, dtype=np.float64)
+    B, H = xf.shape
+    has_lr = layer.get("U_gate") is not None and _f(layer["U_gate"]).shape[1] > 0
+    if has_lr and z is None:
+        z = np.stack([shared_proj(xf, layer["U_gate"]), shared_proj(xf, layer["U_up"])])
+    y = np.zeros((B, H))
+    for t in range(B):
+        for j in range(idx.shape[1]):
+            e = int(idx[t, j])
+            g = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d).T @ xf[t]
+            u = decode_vq(layer["codes_up"][e], layer["cb_up"], d).T @ xf[t]
+            if has_lr:
+                g = g + _f(layer["V_gate"][e]).T @ np.asarray(z[0][t], dtype=np.float64)
+                u = u + _f(layer["V_up"][e]).T @ np.asarray(z[1][t], dtype=np.float64)
+            p = silu(g) * u
+            ye = decode_vq(layer["codes_down"][e], layer["cb_down"], d).T @ p
+            if has_lr:
+                ye = ye + _f(layer["B_down"]).T @ (_f(layer["A_down"][e]).T @ p)
+            y[t] += a[t, j] * ye
+    return y
+
+
+def moe_layer_factored(x, layer: dict, k: int, d: int):
+    """O3: route, then Eq. (1) in factored form. Same return as ``moe_layer``."""
+    idx, a, margin, _ = route(x, layer["router_w"], layer.get("router_bias"), k)
+    return expert_ffn_factored(x, idx, a, layer, d), idx, a, margin
+
+
+def expert_outputs_sampled(x, idx, a, layer: dict, d: int, cols) -> np.ndarray:
+    """Output columns ``cols`` of ``expert_ffn_factored`` for every token.
+
+    The down projection is evaluated only for the requested output columns,
+    which lets full-size parity checks compare a sample of outputs.
+    """
+    xf = _f(x)
+    idx = np.asarray(idx)
+    a = np.asarray(a, dtype=np.float64)
+    cols = np.asarray(cols)
+    B = xf.shape[0]
+    has_lr = layer.get("U_gate") is not None and _f(layer["U_gate"]).shape[1] > 0
+    if has_lr:
+        zg = shared_proj(xf, layer["U_gate"])
+        zu = shared_proj(xf, layer["U_up"])
+        Bd = _f(layer["B_down"])[:, cols]
+    out = np.zeros((B, len(cols)))
+    for t in range(B):
+        for j in range(idx.shape[1]):
+            e = int(idx[t, j])
+            g = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d).T @ xf[t]
+            u = decode_vq(layer["codes_up"][e], layer["cb_up"], d).T @ xf[t]
+            if has_lr:
+                g = g + _f(layer["V_gate"][e]).T @ zg[t]
+                u = u + _f(layer["V_up"][e]).T @ zu[t]
+            p = silu(g) * u
+            Qd = decode_vq(layer["codes_down"][e][:, cols], layer["cb_down"], d)
+            ye = Qd.T @ p
+            if has_lr:
+                ye = ye + Bd.T @ (_f(layer["A_down"][e]).T @ p)
+            out[t] += a[t, j] * ye
+    return out
+
+
+# --------------------------------------------------------------------------
+# O2: scalar brute force (tiny shapes only)
+# --------------------------------------------------------------------------
+def moe_layer_scalar(x, layer: dict, k: int, d: int):
+    """O2: the whole layer with Python floats and explicit loops.
+
+    Every weight is formed element by element from its definition,
+    ``W[i][j] = cb[J[i // d][j]][i % d] + sum_q U[i][q] * V[q][j]``, and every
+    product is an explicit loop; no numpy arithmetic is used. Intended for
+    shapes with H, I <= 32.
+    """
+    X = _f(x).tolist()
+    Wr = _f(layer["router_w"]).tolist()
+    bias = None if layer.get("router_bias") is None else _f(layer["router_bias"]).tolist()
+    cbg = _f(layer["cb_gate"]).tolist()
+    cbu = _f(layer["cb_up"]).tolist()
+    cbd = _f(layer["cb_down"]).tolist()
+    Jg = np.asarray(layer["codes_gate"]).tolist()
+    Ju = np.asarray(layer["codes_up"]).tolist()
+    Jd = np.asarray(layer["codes_down"]).tolist()
+    has_lr = layer.get("U_gate") is not None and _f(layer["U_gate"]).shape[1] > 0
+    if has_lr:
+        Ug = _f(layer["U_gate"]).tolist()
+        Uu = _f(layer["U_up"]).tolist()
+        Vg = _f(layer["V_gate"]).tolist()
+        Vu = _f(layer["V_up"]).tolist()
+        Ad = _f(layer["A_down"]).tolist()
+        Bd = _f(layer["B_down"]).tolist()
+        r = len(Ug[0])
+    else:
+        r = 0
+    B = len(X)
+    H = len(X[0])
+    E = len(Wr[0])
+    I = len(Jg[0][0])
+
+    def w_in_out(cb, J, U, V, e, i, j):
+        val = cb[J[e][i // d][j]][i % d]
+        for q in range(r):
+            val += U[i][q] * V[e][q][j]
+        return val
+
+    def w_down(e, i, h):
+        val = cbd[Jd[e][i // d][h]][i % d]
+        for q in range(r):
+            val += Ad[e][i][q] * Bd[q][h]
+        return val
+
+    Y, IDX, A, MARGIN = [], [], [], []
+    for t in range(B):
+        logit = []
+        for e in range(E):
+            s = 0.0
+            for h in range(H):
+                s += X[t][h] * Wr[h][e]
+            if bias is not None:
+                s += bias[e]
+            logit.append(s)
+        # selection sort, descending, lower index wins ties
+        remaining = list(range(E))
+        chosen = []
+        for _ in range(k):
+            best = remaining[0]
+            for e in remaining[1:]:
+                if logit[e] > logit[best]:
+                    best = e
+            chosen.append(best)
+            remaining.remove(best)
+        MARGIN.append(logit[chosen[-1]] - max(logit[e] for e in remaining) if remaining else math.inf)
+        m = max(logit[e] for e in chosen)
+        ex = [math.exp(logit[e] - m) for e in chosen]
+        tot = sum(ex)
+        aff = [v / tot for v in ex]
+        yt = [0.0] * H
+        for j, e in enumerate(chosen):
+            g = [0.0] * I
+            u = [0.0] * I
+            for c in range(I):
+                for i in range(H):
+                    g[c] += X[t][i] * w_in_out(cbg, Jg, Ug if r else None, Vg if r else None, e, i, c)
+                    u[c] += X[t][i] * w_in_out(cbu, Ju, Uu if r else None, Vu if r else None, e, i, c)
+            p = [g[c] / (1.0 + math.exp(-g[c])) * u[c] for c in range(I)]
+            for h in range(H):
+                s = 0.0
+                for i in range(I):
+                    s += p[i] * w_down(e, i, h)
+                yt[h] += aff[j] * s
+        Y.append(yt)
+        IDX.append(chosen)
+        A.append(aff)
+    return (np.array(Y), np.array(IDX, dtype=np.int64), np.array(A), np.array(MARGIN))
+
+
+# --------------------------------------------------------------------------
+# RMS normalisation between stacked layers (48-layer decode step)
+# --------------------------------------------------------------------------
+def rmsnorm(y, eps: float = 1e-6) -> np.ndarray:
+    """``y / sqrt(mean(y^2) + eps)`` per row, no learned scale (float64)."""
+    y = np.asarray(y, dtype=np.float64)
+    return y / np.sqrt(np.mean(y * y, axis=1, keepdims=True) + eps)
+
+
+# --------------------------------------------------------------------------
+# storage accounting (Sec. 5.5 display; Appendix A.2, Eq. (7))
+# --------------------------------------------------------------------------
+def storage_bits_per_weight(d: int, K: int, r: int, H: int, I: int, E: int,
+                            b_index: int | None = None, b_coef: int = 16,
+                            b_codebook: int = 16, b_basis: int = 16) -> float:
+    """Bits per original weight of one compressed projection, Eq. (7).
+
+    ``log2(K)/d`` for the private index map (stored with ``b_index`` bits per
+    index, 8 for K <= 256), ``b_C r / H`` for the private coefficients, and the
+    shared code book and basis amortised over the ``E`` experts' ``H I``
+    weights. With BF16 factors and one-byte indices this is
+    ``8/d + 16 r/H + 16 r/(E I) + 16 K d/(E H I)``.
+    """
+    if b_index is None:
+        b_index = max(1, math.ceil(math.log2(K)))
+        b_index = 8 if b_index <= 8 else 16
+    return (b_index / d + b_coef * r / H
+            + (b_codebook * K * d + b_basis * H * r) / (E * H * I))

@@ -1,0 +1,52 @@
+"""Workload shapes of the compressed-MoE decode layer.
+
+Each workload is one MoE layer (or a stack of them) with the expert matrices
+stored as blockwise VQ codes plus a shared-basis low-rank term. Shapes follow
+the Qwen3-30B-A3B MoE layer of the paper's model table (Table 2: H=2048,
+I=768, E=128, top-8) with the rank and code-book sizes fixed per workload.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    H: int          # hidden size
+    I: int          # expert intermediate size
+    E: int          # experts per layer
+    top_k: int      # experts selected per token
+    d: int          # VQ block length (along the input dimension)
+    K: int          # code words per code book
+    r: int          # rank of the shared low-rank basis
+    B: int          # decode batch (tokens per step)
+    seed: int
+    layers: int = 1
+    hot_experts: tuple = ()      # experts whose router logit gets +hot_bias
+    hot_bias: float = 0.0
+    description: str = field(default="", compare=False)
+
+    @property
+    def shape(self):
+        return (self.H, self.I, self.E, self.top_k, self.d, self.K, self.r)
+
+
+TINY = Workload("tiny_h256_i128_e8_top2_b1", H=256, I=128, E=8, top_k=2, d=4, K=16, r=8,
+                B=1, seed=0, description="tiny layer, d=4, K=16, r=8, batch 1")
+QWEN3_B1 = Workload("qwen3_30b_a3b_moe_layer_b1", H=2048, I=768, E=128, top_k=8, d=8, K=256,
+                    r=128, B=1, seed=1,
+                    description="Qwen3-30B-A3B-shaped MoE layer, d=8, K=256, r=128, batch 1")
+QWEN3_B16 = Workload("qwen3_30b_a3b_moe_layer_b16", H=2048, I=768, E=128, top_k=8, d=8, K=256,
+                     r=128, B=16, seed=1,
+                     description="Qwen3-30B-A3B-shaped MoE layer, batch 16")
+WIDE_SKEW_B4 = Workload("wide_h4096_i1536_e64_top6_b4_skewed", H=4096, I=1536, E=64, top_k=6,
+                        d=8, K=256, r=256, B=4, seed=2, hot_experts=tuple(range(8)),
+                        hot_bias=2.0,
+                        description="wider layer, r=256, batch 4, 8 hot experts (+2.0 logit)")
+QWEN3_48L_B16 = Workload("qwen3_48_layer_decode_step_b16", H=2048, I=768, E=128, top_k=8, d=8,
+                         K=256, r=128, B=16, seed=1, layers=48,
+                         description="48 stacked Qwen3-shaped layers, RMS-normalised between")
+
+WORKLOADS = {w.name: w for w in (TINY, QWEN3_B1, QWEN3_B16, WIDE_SKEW_B4, QWEN3_48L_B16)}
