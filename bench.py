@@ -1,0 +1,274 @@
+#!/usr/bin/env python3
+"""Benchmark of the compressed-MoE decode layer on one MI355X.
+
+A step is one full layer call (route + top-k + gating, shared projections,
+grouped gate/up, down and combine) on one batch of synthetic input; steps
+rotate over several independently seeded layers so that the weights are read
+from HBM, not from the 256 MB last-level cache. Prints one JSON line.
+
+value  = compressed-weight bytes touched per step (active experts' codes and
+         low-rank coefficients, plus the shared bases and code books) summed
+         over the timed steps, divided by the timed wall time (GB/s).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer decode µs at batch 1/16; achieved HBM GB/s (% of peak)"
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="qwen3_30b_a3b_moe_layer_b1")
+    ap.add_argument("--also", default="qwen3_30b_a3b_moe_layer_b16,wide_h4096_i1536_e64_top6_b4_skewed",
+                    help="comma-separated extra workloads timed the same way (reported under 'also')")
+    ap.add_argument("--layers", type=int, default=8, help="independently seeded layers rotated")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_21137_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def compressed_bytes(w, n_active: int, z_sep: bool = False) -> dict:
+    """Algorithmic bytes of one step: what the method must read at least once.
+
+    Per active expert: gate and up codes (H*I/d bytes each) and coefficients
+    V (r*I bf16 each); down codes (I*H/d) and A (I*r bf16). Shared: the basis
+    U (one per projection when separate), the output basis B and three code
+    books. The router weights are counted separately.
+    """
+    per_gateup = 2 * (w.H * w.I // w.d) + 2 * (w.r * w.I * 2)
+    per_down = (w.I * w.H // w.d) + (w.I * w.r * 2)
+    basis_u = (2 if z_sep else 1) * w.H * w.r * 2
+    basis_b = w.r * w.H * 2
+    codebooks = 3 * w.K * w.d * 2
+    router = w.H * w.E * 2 + w.E * 4
+    return {"compressed": n_active * (per_gateup + per_down) + basis_u + basis_b + codebooks,
+            "expert_kernel": n_active * (per_gateup + per_down) + basis_b + codebooks,
+            "route_kernel": router + basis_u,
+            "per_expert_gateup": per_gateup, "per_expert_down": per_down}
+
+
+def load_traffic(kernel: str, workload: str, src_hash: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_pmc.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_hash") != src_hash:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def time_workload(C, torch, w, steps, warmup, n_layers, layers_cache):
+    from paper_2609_21137_amd import synth
+    shape = C.shape_of(w)
+    key = (w.H, w.I, w.E, w.d, w.K, w.r, w.seed, w.hot_experts, w.hot_bias)
+    if key not in layers_cache:
+        layers_cache.clear()
+        torch.cuda.empty_cache()
+        dls = []
+        for li in range(n_layers):
+            dls.append(C.DeviceLayer.from_numpy(synth.workload_layer(w, li)))
+        layers_cache[key] = dls
+    dls = layers_cache[key]
+    xs = [C.bf16_tensor(synth.workload_input(w, li)) for li in range(n_layers)]
+    ws = C.new_workspace(shape, w.B)
+    y = torch.empty((w.B, w.H), dtype=torch.float32, device="cuda")
+    idx = torch.empty((w.B, w.top_k), dtype=torch.int32, device="cuda")
+    wt = torch.empty((w.B, w.top_k), dtype=torch.float32, device="cuda")
+    structs = [dl.struct() for dl in dls]
+
+    # routing (hence the active-expert count) is fixed per (layer, input)
+    n_act = []
+    for li in range(n_layers):
+        C.moe_layer(shape, xs[li], dls[li], ws=ws, out=y, idx=idx, w=wt)
+        torch.cuda.synchronize()
+        n_act.append(len(np.unique(idx.cpu().numpy())))
+
+    import ctypes
+    lib = C.lib()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    ptrs = [(ctypes.c_void_p(xs[li].data_ptr()), structs[li]) for li in range(n_layers)]
+    args_tail = (ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(idx.data_ptr()),
+                 ctypes.c_void_p(wt.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(), stream)
+    fn = lib.cardan_moe_layer
+    B = w.B
+
+    def step(i):
+        xp, st = ptrs[i % n_layers]
+        rc = fn(ctypes.byref(shape), B, xp, ctypes.byref(st), *args_tail)
+        if rc != 0:
+            raise RuntimeError(lib.cardan_last_error().decode())
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` layer calls, bracketed by device syncs;
+    # HIP events around every kernel on the call's stream give kernel times
+    C.profile_begin(steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    prof = C.profile_end()
+
+    # same loop without kernel events, for the event overhead
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for i in range(steps):
+        step(i)
+    torch.cuda.synchronize()
+    wall_clean = time.perf_counter() - t1
+
+    acts = [n_act[i % n_layers] for i in range(steps)]
+    tot = {"compressed": 0, "expert_kernel": 0, "route_kernel": 0}
+    for a in acts:
+        b = compressed_bytes(w, a)
+        for k in tot:
+            tot[k] += b[k]
+    return {"wall_s": wall, "wall_clean_s": wall_clean, "prof": prof, "bytes": tot,
+            "mean_active": float(np.mean(acts)), "layers": n_layers}
+
+
+def cpu_baseline(w, budget_s):
+    """The float64 oracle timed on this host's cores on a bounded sample."""
+    import threadpoolctl
+
+    import oracle.cardan_oracle as O
+    from paper_2609_21137_amd import synth
+    cores = len(os.sched_getaffinity(0))
+    L = synth.workload_layer(w, 0)
+    x = synth.workload_input(w, 0)
+    n, t_tot, nbytes = 0, 0.0, 0
+    with threadpoolctl.threadpool_limits(cores):
+        while t_tot < budget_s or n == 0:
+            t0 = time.perf_counter()
+            _, idx, _, _ = O.moe_layer_factored(x, L, w.top_k, w.d)
+            t_tot += time.perf_counter() - t0
+            nbytes += compressed_bytes(w, len(np.unique(idx)))["compressed"]
+            n += 1
+    return {"value": round(nbytes / t_tot / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{n} steps of {w.name} (layer 0), float64 numpy factored form, "
+                      f"{t_tot:.1f} s total, {1e3 * t_tot / n:.1f} ms/step"}
+
+
+def summarize(w, r, src_hash):
+    prof = r["prof"]
+    steps = prof["expert"][1]
+    ex_ms = prof["expert"][0] / max(1, steps)
+    ex_bytes = r["bytes"]["expert_kernel"] / max(1, steps)
+    achieved = ex_bytes / (ex_ms * 1e-3) / 1e9
+    traffic = load_traffic("k_expert", w.name, src_hash)
+    return {
+        "workload": w.name,
+        "B": w.B,
+        "us_per_layer": round(1e6 * r["wall_s"] / steps, 3),
+        "us_per_layer_no_kernel_events": round(1e6 * r["wall_clean_s"] / steps, 3),
+        "GBps": round(r["bytes"]["compressed"] / r["wall_s"] / 1e9, 2),
+        "GBps_no_kernel_events": round(r["bytes"]["compressed"] / r["wall_clean_s"] / 1e9, 2),
+        "mean_active_experts": r["mean_active"],
+        "kernel_us": {k: round(1e3 * v[0] / max(1, v[1]), 3) for k, v in prof.items() if v[1]},
+        "roofline": {"kernel": "k_expert", "bound": "hbm", "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "bytes_per_launch": round(ex_bytes)},
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2609_21137_amd import cardan as C
+    from paper_2609_21137_amd.configs import WORKLOADS
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    src_hash = kernel_source_hash()
+    w = WORKLOADS[args.workload]
+    cache = {}
+    print(f"[bench] {w.name}: synthesizing {args.layers} layers", file=sys.stderr, flush=True)
+    r = time_workload(C, torch, w, args.steps, args.warmup, args.layers, cache)
+    main_sum = summarize(w, r, src_hash)
+    print(f"[bench] {w.name}: {main_sum['us_per_layer']} us/layer", file=sys.stderr, flush=True)
+    also = []
+    for name in [s for s in args.also.split(",") if s]:
+        ww = WORKLOADS[name]
+        print(f"[bench] {ww.name}", file=sys.stderr, flush=True)
+        rr = time_workload(C, torch, ww, args.steps, args.warmup, args.layers, cache)
+        also.append(summarize(ww, rr, src_hash))
+        print(f"[bench] {ww.name}: {also[-1]['us_per_layer']} us/layer", file=sys.stderr,
+              flush=True)
+    cache.clear()
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, args.cpu_seconds)
+    steps = args.steps
+    line = {
+        "metric": METRIC,
+        "value": main_sum["GBps"],
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * r["wall_s"] / steps, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "H": w.H, "I": w.I, "E": w.E, "top_k": w.top_k, "d": w.d,
+                   "K": w.K, "r": w.r, "B": w.B, "layers_rotated": args.layers,
+                   "parallelism": "none"},
+        "us_per_layer": main_sum["us_per_layer"],
+        "hbm_frac_of_peak": round(main_sum["GBps"] / HBM_PEAK_GBPS, 4),
+        "kernel_us": main_sum["kernel_us"],
+        "mean_active_experts": main_sum["mean_active_experts"],
+        "no_kernel_events": {"us_per_layer": main_sum["us_per_layer_no_kernel_events"],
+                             "GBps": main_sum["GBps_no_kernel_events"]},
+        "roofline": main_sum["roofline"],
+        "cpu_baseline": cpu,
+        "also": also,
+        "kernel_source_hash": src_hash,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

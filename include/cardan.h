@@ -1,0 +1,177 @@
+/*
+ * cardan.h -- C ABI of libcardan.so, an MI355X (gfx950) implementation of one
+ * batch-1-to-64 Mixture-of-Experts decode layer whose expert matrices are
+ * stored compressed.
+ *
+ * The layer (paper Sec. 2.1): a router scores the E experts for every token,
+ * keeps the top-k and weights them with a softmax over the k kept logits;
+ * every kept expert runs gate and up projections, the SiLU-gated product
+ * p = silu(g) * u, and a down projection; the layer output is the
+ * affinity-weighted sum of the expert outputs.
+ *
+ * Expert representation (paper Sec. 2.3 and Sec. 3.1, Eq. (1)): a gate or up
+ * matrix W_e [H, I] is Q_B(J_e) + U V_e, where Q_B(J_e) is rebuilt from a
+ * shared code book B [K, d] and a private uint8 index map J_e [H/d, I] (block
+ * b of column j is code word J_e[b, j], whose element i sits at input row
+ * b*d + i), U [H, r] is a basis shared by all experts and V_e [r, I] holds
+ * private coefficients. The down matrix [I, H] is Q_B(J^d_e) + A_e B with
+ * private A_e [I, r] and a shared output-side basis B [r, H].
+ *
+ * Conventions for every entry point:
+ *   - bf16 values are raw bit patterns (uint16_t); all arrays are dense and
+ *     row-major in the shapes given; every pointer is a DEVICE pointer,
+ *     16-byte aligned, owned by the caller and only read during the call
+ *     (outputs are written). The library never allocates, frees or
+ *     synchronises inside these calls and keeps no pointer after returning.
+ *   - All work is enqueued on `stream` and the call returns without waiting.
+ *     Buffers must stay valid until the stream has passed the work.
+ *   - Arguments are validated before anything is enqueued; on any error
+ *     nothing is launched, a negative code is returned and
+ *     cardan_last_error() describes it.
+ *   - `ws` is a caller-owned device workspace of at least
+ *     cardan_workspace_bytes() bytes. It must be zero-filled once before its
+ *     first use; every completed call leaves it ready for the next. Calls
+ *     that overlap in time must not share a workspace.
+ *   - Supported shapes: d in {4, 8}; 1 <= K <= 256; H % 64 == 0;
+ *     I % 32 == 0; 1 <= E <= 1024; 1 <= top_k <= min(E, 32); 0 <= r <= 512;
+ *     1 <= B <= 64. Other shapes return CARDAN_ERR_UNSUPPORTED or
+ *     CARDAN_ERR_BAD_SHAPE.
+ *   - Code values >= K read zero code words (memory-safe); expert indices
+ *     outside [0, E) passed to cardan_vq_lr_expert_ffn contribute nothing.
+ *   - The first int32 of the workspace (CARDAN_WS_STATUS_OFFSET) counts
+ *     internal waits that gave up after their bound (seconds); nonzero means
+ *     the results of the calls since it was last zero are invalid. The
+ *     library never clears it; the caller may.
+ */
+#ifndef CARDAN_H
+#define CARDAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same declaration as HIP's own; lets this header stand alone. */
+typedef struct ihipStream_t* hipStream_t;
+typedef struct ihipEvent_t* hipEvent_t;
+
+#define CARDAN_ABI_VERSION 1
+#define CARDAN_WS_STATUS_OFFSET 0
+
+enum {
+  CARDAN_OK = 0,
+  CARDAN_ERR_NULL_PTR = -1,   /* a required pointer is NULL               */
+  CARDAN_ERR_BAD_SHAPE = -2,  /* shape or batch outside the valid domain  */
+  CARDAN_ERR_UNSUPPORTED = -3,/* valid but not compiled (e.g. d == 2)     */
+  CARDAN_ERR_WORKSPACE = -4,  /* ws_bytes below cardan_workspace_bytes()  */
+  CARDAN_ERR_HIP = -5,        /* a HIP launch or event call failed        */
+  CARDAN_ERR_ALIGN = -6       /* a pointer is not 16-byte aligned         */
+};
+
+typedef uint16_t cardan_bf16;
+
+/* Layer shape: hidden size H, expert intermediate size I, E experts, top_k
+ * selected per token, VQ block length d, K code words, rank r (Table 1). */
+typedef struct {
+  int32_t H, I, E, top_k, d, K, r;
+} cardan_shape;
+
+/* One layer's weights (device pointers). With r == 0 the six low-rank
+ * pointers may be NULL. U_up may equal U_gate (one basis for both). */
+typedef struct {
+  const cardan_bf16* router_w;    /* [H][E]                                  */
+  const float*       router_bias; /* [E] added to the logits, or NULL        */
+  const cardan_bf16* cb_gate;     /* [K][d] shared gate code book            */
+  const cardan_bf16* cb_up;       /* [K][d] shared up code book              */
+  const cardan_bf16* cb_down;     /* [K][d] shared down code book            */
+  const uint8_t*     codes_gate;  /* [E][H/d][I] private index maps          */
+  const uint8_t*     codes_up;    /* [E][H/d][I]                             */
+  const uint8_t*     codes_down;  /* [E][I/d][H]                             */
+  const cardan_bf16* U_gate;      /* [H][r] shared basis (gate)              */
+  const cardan_bf16* U_up;        /* [H][r] shared basis (up)                */
+  const cardan_bf16* V_gate;      /* [E][r][I] private coefficients          */
+  const cardan_bf16* V_up;        /* [E][r][I]                               */
+  const cardan_bf16* A_down;      /* [E][I][r] private down factor           */
+  const cardan_bf16* B_down;      /* [r][H] shared output-side down basis    */
+} cardan_layer;
+
+/* ABI version of the loaded library (CARDAN_ABI_VERSION). */
+int cardan_abi_version(void);
+
+/* Text of the last error on the calling thread ("" if none). Valid until the
+ * next cardan_* call on the same thread. */
+const char* cardan_last_error(void);
+
+/* Workspace size in bytes needed by every ws-taking entry point for this
+ * shape and batch B. Host-only; no device is touched. */
+int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out);
+
+/* Router and gating (paper Sec. 2.1): logits l[t][e] = sum_h x[t][h] *
+ * router_w[h][e] + router_bias[e], accumulated in float64 from the exact bf16
+ * products; the top_k experts by descending logit (exact ties to the lower
+ * index) go to topk_idx[B][top_k] (int32, in that order) and their softmax
+ * over the top_k logits to topk_w[B][top_k] (float32).
+ * x: [B][H] bf16. */
+int cardan_route_topk(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                      const cardan_bf16* router_w, const float* router_bias,
+                      int32_t* topk_idx, float* topk_w,
+                      void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Shared projections of Eq. (1) (paper Sec. 4.2, computed once per token):
+ * z[0][t][q] = sum_h U_gate[h][q] x[t][h] and z[1][t][q] likewise with U_up,
+ * as float32 z[2][B][r]. Both halves are always written; U_up may equal
+ * U_gate. Requires r > 0. */
+int cardan_shared_proj(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                       const cardan_bf16* U_gate, const cardan_bf16* U_up, float* z,
+                       void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Expert computation and weighted combine for a given routing (Sec. 2.1,
+ * Eq. (1)): tokens are grouped by expert so each selected expert's codes are
+ * read once; for every (token, selected expert) g and u are the VQ gather sum
+ * plus V^T z (one float32 accumulation), p = silu(g) * u, the down output is
+ * Q^T p + B^T (A^T p), and y[t] = sum_j topk_w[t][j] * y_{topk_idx[t][j]}.
+ * topk_idx/topk_w: [B][top_k] as produced by cardan_route_topk; z: [2][B][r]
+ * as produced by cardan_shared_proj (may be NULL iff r == 0);
+ * y: [B][H] float32 output. */
+int cardan_vq_lr_expert_ffn(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                            const int32_t* topk_idx, const float* topk_w, const float* z,
+                            const cardan_layer* layer, float* y,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The whole layer: route + top-k + gating, shared projections, grouped
+ * expert computation and combine. Writes y [B][H] float32 and the routing
+ * topk_idx [B][top_k] int32, topk_w [B][top_k] float32. */
+int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                     const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* RMS normalisation between stacked layers: x_next[t][h] =
+ * bf16_rne(y[t][h] / sqrt(mean_h y[t][h]^2 + eps)), no learned scale.
+ * y: [B][H] float32, x_next: [B][H] bf16. Needs no workspace. */
+int cardan_rmsnorm_bf16(int32_t B, int32_t H, const float* y, float eps,
+                        cardan_bf16* x_next, hipStream_t stream);
+
+/* Kernel timing for measurement. cardan_profile_begin(n) makes the next n
+ * calls record a HIP event pair around each kernel they launch, on the
+ * call's stream; cardan_profile_end() waits for those events and writes, per
+ * kernel kind, the summed milliseconds and the launch count (arrays of
+ * length CARDAN_PROFILE_KINDS, ordered as the enum below). A layer call runs
+ * the routing kernel (routing, shared projections, grouping) and then the
+ * expert kernel (gate/up, down, combine). Host-global state: not
+ * thread-safe, not for use under graph capture. */
+enum {
+  CARDAN_KERNEL_ROUTE = 0,    /* router, top-k, gating, grouping, z = U^T x */
+  CARDAN_KERNEL_EXPERT = 1,   /* gate/up, down, weighted combine            */
+  CARDAN_KERNEL_RMSNORM = 2,
+  CARDAN_PROFILE_KINDS = 3
+};
+int cardan_profile_begin(int32_t max_calls);
+int cardan_profile_end(float* ms_per_kind, int32_t* launches_per_kind);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CARDAN_H */

@@ -227,29 +227,37 @@ def expert_ffn_factored(x, idx, a, layer: dict, d: int, z=None) -> np.ndarray:
     Gate/up: ``o = Q_B(J_e)^T x + V_e^T (U^T x)`` with the shared projection
     ``U^T x`` computed once per token (Sec. 4.2); down:
     ``y_e = Q_B(J^d_e)^T p + B^T (A_e^T p)``. ``z`` optionally supplies the
-    shared projections as ``[2, B, r]`` (gate, up).
+    shared projections as ``[2, B, r]`` (gate, up). Each selected expert's
+    VQ matrices are rebuilt once and applied to all of its tokens; the
+    per-token expert outputs are then summed in selection order.
     """
     xf = _f(x)
     idx = np.asarray(idx)
     a = np.asarray(a, dtype=np.float64)
     B, H = xf.shape
+    k = idx.shape[1]
     has_lr = layer.get("U_gate") is not None and _f(layer["U_gate"]).shape[1] > 0
     if has_lr and z is None:
         z = np.stack([shared_proj(xf, layer["U_gate"]), shared_proj(xf, layer["U_up"])])
-    y = np.zeros((B, H))
-    for t in range(B):
-        for j in range(idx.shape[1]):
-            e = int(idx[t, j])
-            g = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d).T @ xf[t]
-            u = decode_vq(layer["codes_up"][e], layer["cb_up"], d).T @ xf[t]
+    contrib = np.zeros((B, k, H))
+    for e in sorted(set(int(v) for v in idx.ravel())):
+        Qg = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d)
+        Qu = decode_vq(layer["codes_up"][e], layer["cb_up"], d)
+        Qd = decode_vq(layer["codes_down"][e], layer["cb_down"], d)
+        for t, j in zip(*np.nonzero(idx == e)):
+            g = Qg.T @ xf[t]
+            u = Qu.T @ xf[t]
             if has_lr:
                 g = g + _f(layer["V_gate"][e]).T @ np.asarray(z[0][t], dtype=np.float64)
                 u = u + _f(layer["V_up"][e]).T @ np.asarray(z[1][t], dtype=np.float64)
             p = silu(g) * u
-            ye = decode_vq(layer["codes_down"][e], layer["cb_down"], d).T @ p
+            ye = Qd.T @ p
             if has_lr:
                 ye = ye + _f(layer["B_down"]).T @ (_f(layer["A_down"][e]).T @ p)
-            y[t] += a[t, j] * ye
+            contrib[t, j] = a[t, j] * ye
+    y = np.zeros((B, H))
+    for j in range(k):
+        y += contrib[:, j]
     return y
 
 

@@ -1,0 +1,471 @@
+// C ABI of libcardan.so: argument validation, launch planning, workspace
+// layout and the kernel sequence of every entry point.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "../../include/cardan.h"
+#include "cardan_plan.h"
+
+namespace cardan {
+const void* route_kernel();
+const void* expert_kernel(int d);
+hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t);
+hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t);
+hipError_t launch_rmsnorm(hipStream_t, int, int, const float*, float, uint16_t*);
+}  // namespace cardan
+
+using namespace cardan;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+int pow2_floor(double v) {
+  int p = 1;
+  while (p * 2 <= v) p *= 2;
+  return p;
+}
+
+// Shape and batch validation shared by every entry point.
+int check_shape(const cardan_shape* s, int32_t B) {
+  if (!s) return fail(CARDAN_ERR_NULL_PTR, "shape is NULL");
+  if (s->H <= 0 || s->I <= 0 || s->E <= 0 || s->top_k <= 0 || s->d <= 0 || s->K <= 0 || s->r < 0)
+    return fail(CARDAN_ERR_BAD_SHAPE, "shape fields must be positive (r >= 0)");
+  if (s->top_k > s->E) return fail(CARDAN_ERR_BAD_SHAPE, "top_k=%d exceeds E=%d", s->top_k, s->E);
+  if (s->H % s->d || s->I % s->d)
+    return fail(CARDAN_ERR_BAD_SHAPE, "H=%d and I=%d must be multiples of d=%d", s->H, s->I, s->d);
+  if (B < 1 || B > kMaxB) return fail(CARDAN_ERR_BAD_SHAPE, "B=%d outside [1, %d]", B, kMaxB);
+  if (s->K > 256) return fail(CARDAN_ERR_BAD_SHAPE, "K=%d exceeds 256 (uint8 codes)", s->K);
+  if (s->d != 4 && s->d != 8) return fail(CARDAN_ERR_UNSUPPORTED, "d=%d not compiled (4, 8)", s->d);
+  if (s->H % 64) return fail(CARDAN_ERR_UNSUPPORTED, "H=%d must be a multiple of 64", s->H);
+  if (s->I % 32) return fail(CARDAN_ERR_UNSUPPORTED, "I=%d must be a multiple of 32", s->I);
+  if (s->E > kMaxE) return fail(CARDAN_ERR_UNSUPPORTED, "E=%d exceeds %d", s->E, kMaxE);
+  if (s->top_k > kMaxK) return fail(CARDAN_ERR_UNSUPPORTED, "top_k=%d exceeds %d", s->top_k, kMaxK);
+  if (s->r > kMaxR || (s->r % 8))
+    return fail(CARDAN_ERR_UNSUPPORTED, "r=%d must be a multiple of 8 and <= %d", s->r, kMaxR);
+  return CARDAN_OK;
+}
+
+constexpr size_t kLdsBudget = 32 * 1024;  // dynamic LDS limit of either kernel
+
+int ks_max(int total, int splits) { return ceil_div(total, splits); }
+
+// Largest x/z staging of a gate/up split (uint4 per token row).
+int gateup_ld(int KSX, int KSZ, int ns) {
+  int best = 0;
+  const int KS = KSX + KSZ;
+  for (int s = 0; s < ns; ++s) {
+    const int k0 = s * KS / ns, k1 = (s + 1) * KS / ns;
+    const int x = std::min(k1, KSX) - std::min(k0, KSX);
+    const int z = std::max(k1, KSX) - std::max(k0, KSX);
+    best = std::max(best, (x * 4 + 1) + (z * 8 + 1));
+  }
+  return best;
+}
+
+size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// Dynamic LDS of k_route for a plan.
+size_t lds_route(const Plan& P) {
+  const int KSX = P.H / 32;
+  size_t need = (size_t)kTokPass * kRowsRouter * 4;                    // router chunk
+  need = std::max(need, (size_t)kMaxE * 8 + kMaxK * 4);                 // select
+  need = std::max(need, (size_t)(kMaxB * kMaxK + 2 * kMaxE + 4) * 4);   // grouping
+  if (P.flags & F_Z)
+    need = std::max(need, (size_t)4 * kTokPass * (ks_max(KSX, P.nch_z) * 4 + 1) * 16);
+  return round256(need);
+}
+
+// Dynamic LDS of k_expert for a plan.
+size_t lds_expert(const Plan& P) {
+  const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KSD = P.I / 32;
+  size_t need = (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns) * 16;
+  need = std::max(need, (size_t)P.nt_max * (ks_max(KSD, P.nsd) * 8 + 1) * 16);
+  need = std::max(need, (size_t)P.tpc * (KSZ * 8 + 1) * 16);
+  return round256(need);
+}
+
+// Launch plan, item counts and workspace layout; depends only on
+// (shape, B, z_sep, flags).
+Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
+  Plan P;
+  memset(&P, 0, sizeof P);
+  P.H = s->H; P.I = s->I; P.E = s->E; P.k = s->top_k; P.d = s->d; P.K = s->K; P.r = s->r;
+  P.B = B;
+  P.flags = flags;
+  P.S = B * P.k;
+  P.max_act = P.E < P.S ? P.E : P.S;
+  P.nch_r = P.H / kRowsRouter;
+  P.n_eg = ceil_div(P.E, 64);
+  P.z_sep = z_sep;
+  P.nt_max = std::min(B, kTokPass);
+  P.tpc = std::min(kTokPass, ceil_div(B, 4));
+  const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KS = KSX + KSZ, KSD = P.I / 32;
+  P.nch_z = std::max(1, KSX / 2);                  // two K-steps of U per z unit
+  // expected active experts under uniform routing, to size the splits
+  const double exp_act = fmax(1.0, P.E * (1.0 - pow(1.0 - (double)P.k / P.E, (double)B)));
+  P.ncg = ceil_div(P.I, kColsPerGroup);
+  P.ns = std::min(KS, pow2_floor(1024.0 / (exp_act * 2 * P.ncg)));
+  while (P.ns < KS && (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns) * 16 > kLdsBudget) ++P.ns;
+  P.ncgh = ceil_div(P.H, kColsPerGroup);
+  P.ncgr = ceil_div(P.r, kColsPerGroup);
+  P.nsd = std::min(KSD, pow2_floor(512.0 / (exp_act * (P.ncgh + P.ncgr))));
+  while (P.nsd < KSD && (size_t)P.nt_max * (ks_max(KSD, P.nsd) * 8 + 1) * 16 > kLdsBudget) ++P.nsd;
+  P.n_cb = P.ncgh * ceil_div(B, P.tpc);
+
+  const int z_units = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nch_z;
+  P.n_rc = (flags & F_ROUTE) ? P.nch_r * P.n_eg : 0;
+  P.n_zc = (flags & F_Z) ? ceil_div(z_units, 4) : 0;
+  P.n_sel = (flags & F_ROUTE) ? B : ((flags & F_GROUP) ? 1 : 0);
+  P.n_zr = (flags & F_Z) ? ceil_div(2 * B * P.r, kWG) : 0;
+  P.n_pre = P.n_rc + P.n_zc + P.n_sel + P.n_zr;
+
+  // counters first, at offsets that depend only on (E, I)
+  size_t o = 0;
+  P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);
+  P.o_gu_tick = o; o = align256(o + (size_t)kMaxE * ceil_div(P.I, kColsPerGroup) * 4);
+  P.o_gu_done = o; o = align256(o + (size_t)kMaxE * 4);
+  P.o_rl = o; o = align256(o + (size_t)P.nch_r * B * P.E * 8);
+  P.o_zp = o; o = align256(o + (size_t)2 * P.nch_z * B * P.r * 4);
+  P.o_z = o; o = align256(o + (size_t)2 * B * P.r * 4);
+  P.o_off = o; o = align256(o + (size_t)(P.E + 1) * 4);
+  P.o_act = o; o = align256(o + (size_t)P.E * 4);
+  P.o_nact = o; o = align256(o + 4);
+  P.o_slot_tok = o; o = align256(o + (size_t)P.S * 4);
+  P.o_slot_w = o; o = align256(o + (size_t)P.S * 4);
+  P.o_tok_slot = o; o = align256(o + (size_t)P.S * 4);
+  P.o_gu = o; o = align256(o + (size_t)P.S * 2 * P.ns * P.I * 4);
+  P.o_p = o; o = align256(o + (size_t)P.S * P.I * 4);
+  P.o_dn = o; o = align256(o + (size_t)P.nsd * P.S * P.H * 4);
+  P.o_uap = o; o = align256(o + (size_t)P.nsd * P.S * P.r * 4);
+  P.total = o;
+  P.lds_route = lds_route(P);
+  P.lds_expert = lds_expert(P);
+  return P;
+}
+
+// Co-resident workgroups of a kernel on the current device for a given
+// dynamic LDS size (cached per device, kernel and LDS size).
+int resident_grid(const void* fn, size_t lds, hipError_t* err) {
+  struct Entry {
+    int dev;
+    const void* fn;
+    size_t lds;
+    int grid;
+  };
+  static Entry cache[64];
+  static int n_cache = 0;
+  int dev = 0;
+  *err = hipGetDevice(&dev);
+  if (*err != hipSuccess) return 0;
+  for (int i = 0; i < n_cache; ++i)
+    if (cache[i].dev == dev && cache[i].fn == fn && cache[i].lds == lds) return cache[i].grid;
+  int cus = 0, per_cu = 0;
+  *err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (*err != hipSuccess) return 0;
+  *err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kWG, lds);
+  if (*err != hipSuccess) return 0;
+  const int g = std::max(1, cus * per_cu);
+  if (n_cache < 64) cache[n_cache++] = {dev, fn, lds, g};
+  return g;
+}
+
+int check_ws(const Plan& P, const void* ws, size_t ws_bytes) {
+  if (!ws) return fail(CARDAN_ERR_NULL_PTR, "workspace is NULL");
+  if (misaligned(ws)) return fail(CARDAN_ERR_ALIGN, "workspace is not 16-byte aligned");
+  if (ws_bytes < P.total)
+    return fail(CARDAN_ERR_WORKSPACE, "workspace of %zu bytes < required %zu", ws_bytes, P.total);
+  return CARDAN_OK;
+}
+
+#define REQ(p, name)                                                                  \
+  do {                                                                                \
+    if (!(p)) return fail(CARDAN_ERR_NULL_PTR, "%s is NULL", name);                   \
+    if (misaligned(p)) return fail(CARDAN_ERR_ALIGN, "%s is not 16-byte aligned", name); \
+  } while (0)
+
+int check_layer(const cardan_shape* s, const cardan_layer* L, bool need_router) {
+  if (!L) return fail(CARDAN_ERR_NULL_PTR, "layer is NULL");
+  if (need_router) REQ(L->router_w, "router_w");
+  if (L->router_bias && (reinterpret_cast<uintptr_t>(L->router_bias) & 3u))
+    return fail(CARDAN_ERR_ALIGN, "router_bias is not 4-byte aligned");
+  REQ(L->cb_gate, "cb_gate");
+  REQ(L->cb_up, "cb_up");
+  REQ(L->cb_down, "cb_down");
+  REQ(L->codes_gate, "codes_gate");
+  REQ(L->codes_up, "codes_up");
+  REQ(L->codes_down, "codes_down");
+  if (s->r > 0) {
+    REQ(L->U_gate, "U_gate");
+    REQ(L->U_up, "U_up");
+    REQ(L->V_gate, "V_gate");
+    REQ(L->V_up, "V_up");
+    REQ(L->A_down, "A_down");
+    REQ(L->B_down, "B_down");
+  }
+  return CARDAN_OK;
+}
+
+// ---- kernel timing ---------------------------------------------------------
+struct Profiler {
+  bool on = false;
+  int cap = 0;
+  int calls = 0;
+  std::vector<hipEvent_t> ev;       // per call: 2 events per kind
+  std::vector<unsigned char> used;  // per call and kind
+};
+Profiler g_prof;
+
+struct Timed {
+  hipStream_t st;
+  int kind;
+  bool rec;
+  Timed(hipStream_t s, int k) : st(s), kind(k), rec(false) {
+    if (g_prof.on && g_prof.calls < g_prof.cap) {
+      const size_t i = (size_t)g_prof.calls * CARDAN_PROFILE_KINDS + kind;
+      if (!g_prof.used[i] && hipEventRecord(g_prof.ev[2 * i], st) == hipSuccess) rec = true;
+    }
+  }
+  void done() {
+    if (rec) {
+      const size_t i = (size_t)g_prof.calls * CARDAN_PROFILE_KINDS + kind;
+      if (hipEventRecord(g_prof.ev[2 * i + 1], st) == hipSuccess) g_prof.used[i] = 1;
+    }
+  }
+};
+
+void prof_next_call() {
+  if (g_prof.on && g_prof.calls < g_prof.cap) ++g_prof.calls;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(CARDAN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Sizes the grids and launches k_route (if the call has routing items) and
+// k_expert (if it has expert work) for one call.
+int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
+  if (P.lds_route > kLdsBudget || P.lds_expert > kLdsBudget)
+    return fail(CARDAN_ERR_UNSUPPORTED, "shape needs %zu/%zu bytes of LDS (> %zu)", P.lds_route,
+                P.lds_expert, kLdsBudget);
+  hipError_t err;
+  if (P.n_pre > 0) {
+    const int cap = resident_grid(route_kernel(), P.lds_route, &err);
+    if (cap <= 0) return hip_fail(err, "occupancy query");
+    Timed tm(stream, CARDAN_KERNEL_ROUTE);
+    err = launch_route(P, A, std::min(cap, P.n_pre), P.lds_route, stream);
+    if (err != hipSuccess) return hip_fail(err, "k_route launch");
+    tm.done();
+  }
+  if (P.flags & F_EXPERTS) {
+    const int cap = resident_grid(expert_kernel(P.d), P.lds_expert, &err);
+    if (cap <= 0) return hip_fail(err, "occupancy query");
+    Timed tm(stream, CARDAN_KERNEL_EXPERT);
+    err = launch_expert(P, A, cap, P.lds_expert, stream);
+    if (err != hipSuccess) return hip_fail(err, "k_expert launch");
+    tm.done();
+  }
+  prof_next_call();
+  return CARDAN_OK;
+}
+
+Args args_for(const cardan_layer* L, uint8_t* ws) {
+  Args A;
+  memset(&A, 0, sizeof A);
+  if (L) A.L = *L;
+  A.ws = ws;
+  return A;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cardan_abi_version(void) { return CARDAN_ABI_VERSION; }
+
+const char* cardan_last_error(void) { return g_err; }
+
+int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out) {
+  g_err[0] = 0;
+  int rc = check_shape(shape, B);
+  if (rc) return rc;
+  if (!out) return fail(CARDAN_ERR_NULL_PTR, "out is NULL");
+  *out = make_plan(shape, B, 1, F_ROUTE | F_Z | F_GROUP | F_EXPERTS).total;
+  return CARDAN_OK;
+}
+
+int cardan_route_topk(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                      const cardan_bf16* router_w, const float* router_bias, int32_t* topk_idx,
+                      float* topk_w, void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  int rc = check_shape(shape, B);
+  if (rc) return rc;
+  REQ(x, "x");
+  REQ(router_w, "router_w");
+  REQ(topk_idx, "topk_idx");
+  REQ(topk_w, "topk_w");
+  if (router_bias && (reinterpret_cast<uintptr_t>(router_bias) & 3u))
+    return fail(CARDAN_ERR_ALIGN, "router_bias is not 4-byte aligned");
+  const Plan P = make_plan(shape, B, 1, F_ROUTE);
+  if ((rc = check_ws(P, ws, ws_bytes))) return rc;
+  cardan_layer L;
+  memset(&L, 0, sizeof L);
+  L.router_w = router_w;
+  L.router_bias = router_bias;
+  Args A = args_for(&L, static_cast<uint8_t*>(ws));
+  A.x = x;
+  A.topk_idx = topk_idx;
+  A.topk_w = topk_w;
+  return run_layer(P, A, stream);
+}
+
+int cardan_shared_proj(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                       const cardan_bf16* U_gate, const cardan_bf16* U_up, float* z, void* ws,
+                       size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  int rc = check_shape(shape, B);
+  if (rc) return rc;
+  if (shape->r == 0) return fail(CARDAN_ERR_BAD_SHAPE, "shared projection needs r > 0");
+  REQ(x, "x");
+  REQ(U_gate, "U_gate");
+  REQ(U_up, "U_up");
+  REQ(z, "z");
+  const Plan P = make_plan(shape, B, U_up != U_gate, F_Z);
+  if ((rc = check_ws(P, ws, ws_bytes))) return rc;
+  cardan_layer L;
+  memset(&L, 0, sizeof L);
+  L.U_gate = U_gate;
+  L.U_up = U_up;
+  Args A = args_for(&L, static_cast<uint8_t*>(ws));
+  A.x = x;
+  A.z_out = z;
+  return run_layer(P, A, stream);
+}
+
+int cardan_vq_lr_expert_ffn(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                            const int32_t* topk_idx, const float* topk_w, const float* z,
+                            const cardan_layer* layer, float* y, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  g_err[0] = 0;
+  int rc = check_shape(shape, B);
+  if (rc) return rc;
+  REQ(x, "x");
+  REQ(topk_idx, "topk_idx");
+  REQ(topk_w, "topk_w");
+  REQ(y, "y");
+  if (shape->r > 0) REQ(z, "z");
+  if ((rc = check_layer(shape, layer, false))) return rc;
+  const Plan P = make_plan(shape, B, 1, F_GROUP | F_EXPERTS);
+  if ((rc = check_ws(P, ws, ws_bytes))) return rc;
+  Args A = args_for(layer, static_cast<uint8_t*>(ws));
+  A.x = x;
+  A.idx_in = topk_idx;
+  A.w_in = topk_w;
+  A.z_in = z;
+  A.y = y;
+  return run_layer(P, A, stream);
+}
+
+int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                     const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
+                     void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  int rc = check_shape(shape, B);
+  if (rc) return rc;
+  REQ(x, "x");
+  REQ(y, "y");
+  REQ(topk_idx, "topk_idx");
+  REQ(topk_w, "topk_w");
+  if ((rc = check_layer(shape, layer, true))) return rc;
+  const int z_sep = shape->r > 0 && layer->U_up != layer->U_gate;
+  const int flags = F_ROUTE | F_GROUP | F_EXPERTS | (shape->r > 0 ? F_Z : 0);
+  const Plan P = make_plan(shape, B, z_sep, flags);
+  if ((rc = check_ws(P, ws, ws_bytes))) return rc;
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  Args A = args_for(layer, w);
+  A.x = x;
+  A.topk_idx = topk_idx;
+  A.topk_w = topk_w;
+  A.z_out = reinterpret_cast<float*>(w + P.o_z);
+  A.y = y;
+  return run_layer(P, A, stream);
+}
+
+int cardan_rmsnorm_bf16(int32_t B, int32_t H, const float* y, float eps, cardan_bf16* x_next,
+                        hipStream_t stream) {
+  g_err[0] = 0;
+  if (B < 1 || H < 1) return fail(CARDAN_ERR_BAD_SHAPE, "B=%d, H=%d must be positive", B, H);
+  REQ(y, "y");
+  REQ(x_next, "x_next");
+  Timed tm(stream, CARDAN_KERNEL_RMSNORM);
+  hipError_t e = launch_rmsnorm(stream, B, H, y, eps, x_next);
+  if (e != hipSuccess) return hip_fail(e, "rmsnorm launch");
+  tm.done();
+  prof_next_call();
+  return CARDAN_OK;
+}
+
+int cardan_profile_begin(int32_t max_calls) {
+  g_err[0] = 0;
+  if (max_calls < 1) return fail(CARDAN_ERR_BAD_SHAPE, "max_calls must be positive");
+  const size_t need = (size_t)max_calls * CARDAN_PROFILE_KINDS * 2;
+  while (g_prof.ev.size() < need) {
+    hipEvent_t e;
+    hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) return hip_fail(err, "hipEventCreate");
+    g_prof.ev.push_back(e);
+  }
+  g_prof.used.assign((size_t)max_calls * CARDAN_PROFILE_KINDS, 0);
+  g_prof.cap = max_calls;
+  g_prof.calls = 0;
+  g_prof.on = true;
+  return CARDAN_OK;
+}
+
+int cardan_profile_end(float* ms_per_kind, int32_t* launches_per_kind) {
+  g_err[0] = 0;
+  if (!ms_per_kind || !launches_per_kind) return fail(CARDAN_ERR_NULL_PTR, "output is NULL");
+  for (int k = 0; k < CARDAN_PROFILE_KINDS; ++k) {
+    ms_per_kind[k] = 0.0f;
+    launches_per_kind[k] = 0;
+  }
+  g_prof.on = false;
+  for (int c = 0; c < g_prof.calls; ++c) {
+    for (int k = 0; k < CARDAN_PROFILE_KINDS; ++k) {
+      const size_t i = (size_t)c * CARDAN_PROFILE_KINDS + k;
+      if (!g_prof.used[i]) continue;
+      hipError_t err = hipEventSynchronize(g_prof.ev[2 * i + 1]);
+      if (err != hipSuccess) return hip_fail(err, "hipEventSynchronize");
+      float ms = 0.0f;
+      err = hipEventElapsedTime(&ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]);
+      if (err != hipSuccess) return hip_fail(err, "hipEventElapsedTime");
+      ms_per_kind[k] += ms;
+      launches_per_kind[k] += 1;
+    }
+  }
+  g_prof.calls = 0;
+  return CARDAN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,982 @@
+// HIP kernels for gfx950 (MI355X) of the compressed-MoE decode layer.
+//
+// k_layer is a persistent kernel that runs a whole layer call (paper Sec. 2.1
+// and Sec. 4) as an ordered list of work items (see cardan_plan.h):
+//   routing-independent work first -- router partial logits in float64 and
+//   the shared projections z = U^T x (Sec. 4.2: computed once per token);
+//   then per-token top-k and gating, the grouping of (token, expert) slots by
+//   expert, and the expert tiles, which stream each active expert's codes
+//   and coefficients from HBM exactly once per step.
+// Down-projection tiles issue their HBM loads before they wait for the gate/up
+// result of their expert, so weight traffic keeps flowing across the
+// gate/up -> down dependency (the GPU form of the paper's overlap windows,
+// Sec. 4.1).
+//
+// Every contraction runs on the matrix cores (v_mfma_f32_16x16x32_bf16) with
+// the token slots of an expert as the M dimension: for the VQ part each lane
+// decodes one uint8 code into its code word (d bf16 values from the LDS copy
+// of the code book) and that code word IS the lane's slice of the weight
+// operand, so decoded weights never leave registers; the low-rank factors
+// enter the same accumulators as dense bf16 operands, which makes the VQ sum
+// and V^T z one float32 accumulation before the activation (Sec. 4.2, joint
+// accumulation).
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include "cardan_plan.h"
+
+namespace cardan {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr unsigned kSpinLimit = 1u << 24;  // polls before a wait gives up (seconds)
+
+__device__ __forceinline__ float bf(uint32_t b) { return __uint_as_float(b << 16); }
+
+__device__ __forceinline__ uint32_t rne_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ f32x4 mfma_bf16(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ int* ctr(const Args& A, int i) {
+  return reinterpret_cast<int*>(A.ws) + i * kCtrStride;
+}
+
+template <typename T>
+__device__ __forceinline__ T* wsp(const Args& A, size_t off) {
+  return reinterpret_cast<T*>(A.ws + off);
+}
+
+// Makes this workgroup's global writes visible device-wide, then adds 1 to
+// `c`. Every wave releases its own stores before the barrier.
+__device__ __forceinline__ void arrive(int* c) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) atomicAdd(c, 1);
+}
+
+// Waits until *c >= target (thread 0 polls), then acquires. Bounded: on
+// timeout the error counter is raised and the caller proceeds, so the grid
+// always drains.
+__device__ __forceinline__ void wait_geq(const Args& A, int* c, int target) {
+  if (threadIdx.x == 0) {
+    unsigned it = 0;
+    while (__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++it > kSpinLimit) {
+        atomicAdd(ctr(A, C_ERR), 1);
+        break;
+      }
+    }
+  }
+  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+// Ticket: after every wave released its writes, returns true in the one
+// workgroup that arrives last of `total` (which then acquires and resets).
+__device__ __forceinline__ bool last_of(int* tick, int total, int* s_flag) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) *s_flag = (atomicAdd(tick, 1) == total - 1);
+  __syncthreads();
+  const bool last = *s_flag;
+  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  return last;
+}
+
+// Exclusive prefix sum of arr[0..n) (n <= 4 * kWG) in place; returns the total.
+__device__ int block_exclusive_scan(int* arr, int n, int* tmp4) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int base = tid * 4;
+  int v[4], s = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[j] = (base + j < n) ? arr[base + j] : 0;
+    s += v[j];
+  }
+  int incl = s;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  if (lane == 63) tmp4[w] = incl;
+  __syncthreads();
+  int pre = 0;
+  for (int i = 0; i < w; ++i) pre += tmp4[i];
+  const int total = tmp4[0] + tmp4[1] + tmp4[2] + tmp4[3];
+  int ex = pre + incl - s;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (base + j < n) arr[base + j] = ex;
+    ex += v[j];
+  }
+  __syncthreads();
+  return total;
+}
+
+// Router chunk (c, g): partial logits over hidden rows [64c, 64c + 64) for
+// experts [64g, 64g + 64). Wave w owns experts 64g + 16w + (lane & 15); the
+// four lane groups (lane >> 4) own rows h = 4i + (lane >> 4). float64
+// accumulation of exact bf16 products; the four row groups are combined with
+// a fixed shuffle tree.
+__device__ void item_router_chunk(const Plan& P, const Args& A, int c, int g, uint8_t* smem) {
+  float* xs = reinterpret_cast<float*>(smem);  // [16][64] (bf16 values are exact in f32)
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int E = P.E, H = P.H, B = P.B, h0 = c * kRowsRouter;
+  const int e = g * 64 + w * 16 + (lane & 15), rq = lane >> 4;
+  const bool ev = e < E;
+  const uint16_t* Wr = A.L.router_w;
+  uint32_t wv[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) wv[i] = ev ? Wr[(size_t)(h0 + rq + 4 * i) * E + e] : 0u;
+  double* rl = wsp<double>(A, P.o_rl);
+  for (int tg = 0; tg < B; tg += kTokPass) {
+    const int nt = min(kTokPass, B - tg);
+    for (int i = tid; i < kTokPass * kRowsRouter; i += kWG) {
+      const int t = i / kRowsRouter, h = i % kRowsRouter;
+      xs[i] = t < nt ? bf(A.x[(size_t)(tg + t) * H + h0 + h]) : 0.0f;
+    }
+    __syncthreads();
+    double acc[kTokPass];
+#pragma unroll
+    for (int t = 0; t < kTokPass; ++t) acc[t] = 0.0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const double wd = (double)bf(wv[i]);
+      const int h = rq + 4 * i;
+#pragma unroll
+      for (int t = 0; t < kTokPass; ++t) acc[t] = fma(wd, (double)xs[t * kRowsRouter + h], acc[t]);
+    }
+#pragma unroll
+    for (int t = 0; t < kTokPass; ++t) {
+      acc[t] += __shfl_xor(acc[t], 16);
+      acc[t] += __shfl_xor(acc[t], 32);
+    }
+    if (rq == 0 && ev) {
+#pragma unroll
+      for (int t = 0; t < kTokPass; ++t)
+        if (t < nt) rl[((size_t)c * B + tg + t) * E + e] = acc[t];
+    }
+    __syncthreads();
+  }
+  arrive(ctr(A, C_ROUTE_ARR));
+}
+
+// Groups the B*k routing slots by expert (single workgroup): per-expert
+// offsets, the ascending list of active experts, slot -> token and weight,
+// and (token, j) -> slot. Slots of one expert keep (token, j) order.
+__device__ void group_slots(const Plan& P, const Args& A, const int32_t* __restrict__ idx,
+                            const float* __restrict__ wts, uint8_t* smem) {
+  int* s_idx = reinterpret_cast<int*>(smem);  // [S]
+  int* s_cnt = s_idx + kMaxB * kMaxK;         // [E]
+  int* s_flag = s_cnt + kMaxE;                // [E]
+  int* s_tmp = s_flag + kMaxE;                // [4]
+  const int tid = threadIdx.x, E = P.E, S = P.S, k = P.k;
+  int* g_off = wsp<int>(A, P.o_off);
+  int* g_act = wsp<int>(A, P.o_act);
+  int* g_slot_tok = wsp<int>(A, P.o_slot_tok);
+  float* g_slot_w = wsp<float>(A, P.o_slot_w);
+  int* g_tok_slot = wsp<int>(A, P.o_tok_slot);
+  for (int e = tid; e < E; e += kWG) s_cnt[e] = 0;
+  for (int i = tid; i < S; i += kWG) {
+    const int e = idx[i];
+    s_idx[i] = (e >= 0 && e < E) ? e : -1;
+  }
+  __syncthreads();
+  for (int i = tid; i < S; i += kWG)
+    if (s_idx[i] >= 0) atomicAdd(&s_cnt[s_idx[i]], 1);
+  __syncthreads();
+  for (int e = tid; e < E; e += kWG) s_flag[e] = s_cnt[e] > 0;
+  __syncthreads();
+  const int total = block_exclusive_scan(s_cnt, E, s_tmp);
+  const int nact = block_exclusive_scan(s_flag, E, s_tmp);
+  for (int e = tid; e < E; e += kWG) {
+    const int o = s_cnt[e];
+    const int o1 = (e + 1 < E) ? s_cnt[e + 1] : total;
+    g_off[e] = o;
+    if (o1 > o) g_act[s_flag[e]] = e;
+  }
+  if (tid == 0) {
+    g_off[E] = total;
+    *wsp<int>(A, P.o_nact) = nact;
+  }
+  for (int i = tid; i < S; i += kWG) {
+    const int e = s_idx[i];
+    if (e < 0) {
+      g_tok_slot[i] = -1;
+      continue;
+    }
+    int rank = 0;
+    for (int j = 0; j < i; ++j) rank += (s_idx[j] == e);
+    const int pos = s_cnt[e] + rank;
+    g_slot_tok[pos] = i / k;
+    g_slot_w[pos] = wts[i];
+    g_tok_slot[i] = pos;
+  }
+}
+
+// Select item for token t: logits (fixed-order sum of the chunk partials plus
+// bias), top-k by descending logit with ties to the lower index, softmax over
+// the k selected logits. The last select item groups the slots and publishes
+// the routing. With routing given by the caller there is one select item that
+// only groups.
+__device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) {
+  __shared__ int s_last;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int E = P.E, k = P.k, B = P.B;
+  if (P.flags & F_ROUTE) {
+    double* lg = reinterpret_cast<double*>(smem);          // [E]
+    int* sel = reinterpret_cast<int*>(lg + kMaxE);          // [k]
+    wait_geq(A, ctr(A, C_ROUTE_ARR), P.n_rc);
+    const double* rl = wsp<const double>(A, P.o_rl);
+    for (int e = tid; e < E; e += kWG) {
+      double s = 0.0;
+      for (int c0 = 0; c0 < P.nch_r; c0 += 8) {
+        double v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          v[i] = (c0 + i < P.nch_r) ? rl[((size_t)(c0 + i) * B + t) * E + e] : 0.0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s += v[i];
+      }
+      if (A.L.router_bias) s += (double)A.L.router_bias[e];
+      lg[e] = s;
+    }
+    __syncthreads();
+    if (w == 0) {
+      for (int j = 0; j < k; ++j) {
+        double bv = -INFINITY;
+        int be = 0x7fffffff;
+        for (int e = lane; e < E; e += 64) {
+          bool taken = false;
+          for (int jj = 0; jj < j; ++jj) taken |= (sel[jj] == e);
+          if (!taken) {
+            const double v = lg[e];
+            if (v > bv || (v == bv && e < be)) {
+              bv = v;
+              be = e;
+            }
+          }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+          const double ov = __shfl_xor(bv, o);
+          const int oe = __shfl_xor(be, o);
+          if (ov > bv || (ov == bv && oe < be)) {
+            bv = ov;
+            be = oe;
+          }
+        }
+        sel[j] = be;  // the same value in every lane
+      }
+      const double mx = lg[sel[0]];
+      const double ex = lane < k ? exp(lg[sel[lane]] - mx) : 0.0;
+      double sum = ex;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+      if (lane < k) {
+        A.topk_idx[t * k + lane] = sel[lane];
+        A.topk_w[t * k + lane] = (float)(ex / sum);
+      }
+    }
+    if (!(P.flags & F_GROUP)) return;
+    if (!last_of(ctr(A, C_SEL_ARR), P.n_sel, &s_last)) return;
+    group_slots(P, A, A.topk_idx, A.topk_w, smem);
+  } else {
+    group_slots(P, A, A.idx_in, A.w_in, smem);
+  }
+}
+
+// z reduce item i: outputs [256 i, 256 i + 256) of z[2][B][r], each the
+// fixed-order sum of its chunk partials (both halves from one basis when
+// U_up is U_gate).
+__device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
+  wait_geq(A, ctr(A, C_Z_ARR), P.n_zc);
+  const int o = i * kWG + threadIdx.x;
+  const int B = P.B, r = P.r;
+  if (o < 2 * B * r) {
+    const int pj = o / (B * r), rem = o % (B * r);
+    const int src = P.z_sep ? pj : 0;
+    const float* zp = wsp<const float>(A, P.o_zp) + ((size_t)src * P.nch_z * B) * r + rem;
+    float s = 0.0f;
+    for (int c0 = 0; c0 < P.nch_z; c0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = (c0 + j < P.nch_z) ? zp[(size_t)(c0 + j) * B * r] : 0.0f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s += v[j];
+    }
+    A.z_out[o] = s;
+  }
+}
+
+// ===========================================================================
+// MFMA streams
+// ===========================================================================
+// Every product here is D[token][column] += A[token][K] * W[K][column] on
+// v_mfma_f32_16x16x32_bf16, one wave per 64 output columns:
+//   A (activations): lane l = 16 g + n holds token row n, inputs
+//     32 ks + 8 g .. + 8 of K-step ks, read from LDS (`ops`, [token][uint4]
+//     with NOPS interleaved sets: 1 for bf16 x, 2 for the bf16 hi/lo parts of
+//     a float32 operand, whose two products are summed).
+//   W (weights): lane l holds rows 32 ks + 8 g .. + 8 of output column
+//     c0 + 4 n + q for MFMA q = 0..3. For VQ weights this slice is one code
+//     word (d = 8) or two (d = 4) read from the LDS code book; for dense bf16
+//     factors it is gathered from 8 rows of 4 columns with v_perm.
+//   D: accumulator q, element i of lane l = token 4 g + i, column c0 + 4 n + q.
+// Weight loads run a fixed-depth register pipeline (PD K-steps in flight);
+// prime() issues the first PD steps so callers can start the HBM traffic
+// before they wait for their activations.
+
+__device__ __forceinline__ uint4 a_operand(const uint4* __restrict__ ops, int idx, bool valid) {
+  return valid ? ops[idx] : make_uint4(0, 0, 0, 0);
+}
+
+template <int D, int NOPS, int PD>
+struct VqPipe {
+  static constexpr int W = D == 8 ? 1 : 2;
+  uint32_t buf[PD][W];
+  const uint8_t* codes;
+  int row_len, col, ks0, nks;
+  bool cv;
+
+  __device__ __forceinline__ void load(int ks, uint32_t (&b)[W]) {
+    const int g = (threadIdx.x & 63) >> 4;
+    if (D == 8) {
+      b[0] = cv ? *reinterpret_cast<const uint32_t*>(codes + (size_t)(ks * 4 + g) * row_len + col) : 0u;
+    } else {
+      const size_t row = (size_t)(ks * 8 + 2 * g);
+      b[0] = cv ? *reinterpret_cast<const uint32_t*>(codes + row * row_len + col) : 0u;
+      b[1] = cv ? *reinterpret_cast<const uint32_t*>(codes + (row + 1) * row_len + col) : 0u;
+    }
+  }
+  // codes [n_in/d][row_len] of one expert; columns [c0, c0 + 64) of n_out
+  __device__ __forceinline__ void prime(const uint8_t* c, int rl, int c0, int n_out, int k0, int k1) {
+    codes = c;
+    row_len = rl;
+    col = c0 + 4 * (threadIdx.x & 15);
+    cv = col < n_out;
+    ks0 = k0;
+    nks = k1 - k0;
+#pragma unroll
+    for (int u = 0; u < PD; ++u)
+      if (u < nks) load(ks0 + u, buf[u]);
+  }
+  __device__ __forceinline__ void step(int ks, const uint32_t (&b)[W], const uint4* __restrict__ cb_s,
+                                       const uint4* __restrict__ ops, int ops_ld, int ops_ks0, int nt,
+                                       f32x4 acc[4]) {
+    const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
+    const int oi = n * ops_ld + ((ks - ops_ks0) * 4 + g) * NOPS;
+    const uint4 a0 = a_operand(ops, oi, n < nt);
+    uint4 a1 = a0;
+    if (NOPS == 2) a1 = a_operand(ops, oi + 1, n < nt);
+    const uint2* cb2 = reinterpret_cast<const uint2*>(cb_s);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint4 w;
+      if (D == 8) {
+        w = cb_s[(b[0] >> (8 * q)) & 255u];
+      } else {
+        const uint2 lo = cb2[(b[0] >> (8 * q)) & 255u];
+        const uint2 hi = cb2[(b[1] >> (8 * q)) & 255u];
+        w = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
+      acc[q] = mfma_bf16(a0, w, acc[q]);
+      if (NOPS == 2) acc[q] = mfma_bf16(a1, w, acc[q]);
+    }
+  }
+  __device__ __forceinline__ void run(const uint4* cb_s, const uint4* ops, int ops_ld, int ops_ks0,
+                                      int nt, f32x4 acc[4]) {
+    for (int i0 = 0; i0 < nks; i0 += PD) {
+#pragma unroll
+      for (int u = 0; u < PD; ++u) {
+        const int i = i0 + u;
+        if (i < nks) {
+          step(ks0 + i, buf[u], cb_s, ops, ops_ld, ops_ks0, nt, acc);
+          if (i + PD < nks) load(ks0 + i + PD, buf[u]);
+          // keep each step's LDS operand reads inside the step: hoisting them
+          // across the unrolled pipeline costs registers, not time
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  }
+};
+
+template <int Q>
+__device__ __forceinline__ uint4 dense_w(const uint2 (&b)[8]) {
+  constexpr uint32_t sel = (Q & 1) ? 0x07060302u : 0x05040100u;
+  if (Q < 2)
+    return make_uint4(__builtin_amdgcn_perm(b[1].x, b[0].x, sel), __builtin_amdgcn_perm(b[3].x, b[2].x, sel),
+                      __builtin_amdgcn_perm(b[5].x, b[4].x, sel), __builtin_amdgcn_perm(b[7].x, b[6].x, sel));
+  return make_uint4(__builtin_amdgcn_perm(b[1].y, b[0].y, sel), __builtin_amdgcn_perm(b[3].y, b[2].y, sel),
+                    __builtin_amdgcn_perm(b[5].y, b[4].y, sel), __builtin_amdgcn_perm(b[7].y, b[6].y, sel));
+}
+
+template <int NOPS, int PD>
+struct DensePipe {
+  uint2 buf[PD][8];
+  const uint16_t* W;
+  int ld, col, k_rows, ks0, nks;
+  bool cv;
+
+  __device__ __forceinline__ void load(int ks, uint2 (&b)[8]) {
+    const int g = (threadIdx.x & 63) >> 4;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int row = ks * 32 + 8 * g + e;
+      b[e] = (cv && row < k_rows) ? *reinterpret_cast<const uint2*>(W + (size_t)row * ld + col)
+                                  : make_uint2(0, 0);
+    }
+  }
+  // W [k_rows][ld] row-major bf16; columns [c0, c0 + 64) of n_out
+  __device__ __forceinline__ void prime(const uint16_t* w, int ldw, int c0, int n_out, int kr, int k0,
+                                        int k1) {
+    W = w;
+    ld = ldw;
+    col = c0 + 4 * (threadIdx.x & 15);
+    cv = col < n_out;
+    k_rows = kr;
+    ks0 = k0;
+    nks = k1 - k0;
+#pragma unroll
+    for (int u = 0; u < PD; ++u)
+      if (u < nks) load(ks0 + u, buf[u]);
+  }
+  __device__ __forceinline__ void step(int ks, const uint2 (&b)[8], const uint4* __restrict__ ops, int ops_ld,
+                                       int ops_ks0, int nt, f32x4 acc[4]) {
+    const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
+    const int oi = n * ops_ld + ((ks - ops_ks0) * 4 + g) * NOPS;
+    const uint4 a0 = a_operand(ops, oi, n < nt);
+    uint4 a1 = a0;
+    if (NOPS == 2) a1 = a_operand(ops, oi + 1, n < nt);
+    const uint4 w0 = dense_w<0>(b), w1 = dense_w<1>(b), w2 = dense_w<2>(b), w3 = dense_w<3>(b);
+    acc[0] = mfma_bf16(a0, w0, acc[0]);
+    acc[1] = mfma_bf16(a0, w1, acc[1]);
+    acc[2] = mfma_bf16(a0, w2, acc[2]);
+    acc[3] = mfma_bf16(a0, w3, acc[3]);
+    if (NOPS == 2) {
+      acc[0] = mfma_bf16(a1, w0, acc[0]);
+      acc[1] = mfma_bf16(a1, w1, acc[1]);
+      acc[2] = mfma_bf16(a1, w2, acc[2]);
+      acc[3] = mfma_bf16(a1, w3, acc[3]);
+    }
+  }
+  __device__ __forceinline__ void run(const uint4* ops, int ops_ld, int ops_ks0, int nt, f32x4 acc[4]) {
+    for (int i0 = 0; i0 < nks; i0 += PD) {
+#pragma unroll
+      for (int u = 0; u < PD; ++u) {
+        const int i = i0 + u;
+        if (i < nks) {
+          step(ks0 + i, buf[u], ops, ops_ld, ops_ks0, nt, acc);
+          if (i + PD < nks) load(ks0 + i + PD, buf[u]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  }
+};
+
+constexpr int kPdVq = 16;    // code K-steps in flight per wave (256 B each)
+constexpr int kPdDense = 1;  // dense K-steps in flight per wave (4 KB each)
+
+__device__ __forceinline__ void zero_acc(f32x4 acc[4]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// Stores token rows 4g + i < nt of the wave's accumulators: row t goes to
+// dst(t) + c0 + 4n as one float4 (the 4 MFMAs' columns).
+template <typename F>
+__device__ __forceinline__ void store_acc(const f32x4 acc[4], int nt, int c0, int n_out, F dst) {
+  const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
+  const int col = c0 + 4 * n;
+  if (col >= n_out) return;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = 4 * g + i;
+    if (t < nt) *reinterpret_cast<float4*>(dst(t) + col) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+  }
+}
+
+// Stages bf16 activation rows (8 inputs per uint4) for token slots [0, nt):
+// ops[t * ld + j] = inputs 8 j .. 8 j + 7 of row src(t). Threads first,
+// first + stride, ... share the work (the whole workgroup by default).
+template <typename F>
+__device__ __forceinline__ void stage_bf16(uint4* ops, int ld, int nt, int n8, F src,
+                                           int first = threadIdx.x, int stride = kWG) {
+  for (int i = first; i < nt * n8; i += stride) {
+    const int t = i / n8, j = i % n8;
+    ops[t * ld + j] = *reinterpret_cast<const uint4*>(src(t) + 8 * j);
+  }
+}
+
+// Stages float32 activation rows as bf16 hi/lo pairs: ops[t * ld + 2 j] (hi)
+// and [.. + 1] (lo) hold inputs 8 j .. 8 j + 7 of row src(t), value = hi + lo.
+template <typename F>
+__device__ __forceinline__ void stage_split(uint4* ops, int ld, int nt, int n8, F src) {
+  for (int i = threadIdx.x; i < nt * n8; i += kWG) {
+    const int t = i / n8, j = i % n8;
+    const float4* p = reinterpret_cast<const float4*>(src(t) + 8 * j);
+    const float4 v0 = p[0], v1 = p[1];
+    const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    uint32_t h[8], lw[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      h[u] = rne_bf16(f[u]);
+      lw[u] = rne_bf16(f[u] - bf(h[u]));
+    }
+    ops[t * ld + 2 * j] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                                     h[6] | (h[7] << 16));
+    ops[t * ld + 2 * j + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
+                                         lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
+  }
+}
+
+// ===========================================================================
+// shared projections on MFMA
+// ===========================================================================
+// z unit u (one wave): basis pj, 64 columns, K-split s of H; item j runs the
+// four units 4 j .. 4 j + 3 side by side. Partial z goes to zp[pj][s][t][q].
+__device__ void item_z(const Plan& P, const Args& A, int j, uint8_t* smem) {
+  const int w = threadIdx.x >> 6;
+  const int ncol = (P.r + 63) / 64;
+  const int units = (P.z_sep ? 2 : 1) * ncol * P.nch_z;
+  const int u = j * 4 + w;
+  const bool active = u < units;
+  const int uu = active ? u : 0;
+  const int pj = uu / (ncol * P.nch_z), rem = uu % (ncol * P.nch_z);
+  const int c64 = rem % ncol, s = rem / ncol;
+  const int KS = P.H / 32;
+  const int ks0 = s * KS / P.nch_z, ks1 = (s + 1) * KS / P.nch_z;
+  const int c0 = c64 * 64;
+  const uint16_t* U = pj ? A.L.U_up : A.L.U_gate;
+  // each wave stages its own activations: [16 tokens][(ks1 - ks0) * 4 + 1] uint4
+  const int ld = (KS + P.nch_z - 1) / P.nch_z * 4 + 1;
+  uint4* ops = reinterpret_cast<uint4*>(smem) + w * kTokPass * ld;
+  float* zp = wsp<float>(A, P.o_zp);
+  const int B = P.B, H = P.H, r = P.r;
+  DensePipe<1, kPdDense> pipe;
+  for (int tg = 0; tg < B; tg += kTokPass) {
+    const int nt = min(kTokPass, B - tg);
+    if (active) pipe.prime(U, r, c0, r, H, ks0, ks1);
+    __syncthreads();
+    if (active)  // this wave's own region: lanes stride by 64
+      stage_bf16(ops, ld, nt, (ks1 - ks0) * 4,
+                 [&](int t) { return A.x + (size_t)(tg + t) * H + ks0 * 32; }, threadIdx.x & 63, 64);
+    __syncthreads();
+    if (active) {
+      f32x4 acc[4];
+      zero_acc(acc);
+      pipe.run(ops, ld, ks0, nt, acc);
+      store_acc(acc, nt, c0, r, [&](int t) { return zp + (((size_t)pj * P.nch_z + s) * B + tg + t) * r; });
+    }
+  }
+  arrive(ctr(A, C_Z_ARR));
+}
+
+// ===========================================================================
+// expert tiles
+// ===========================================================================
+struct Routing {
+  int e, s0, ne;
+};
+
+__device__ __forceinline__ Routing expert_of(const Plan& P, const Args& A, int a) {
+  const int e = wsp<const int>(A, P.o_act)[a];
+  const int* off = wsp<const int>(A, P.o_off);
+  const int s0 = off[e];
+  return {e, s0, off[e + 1] - s0};
+}
+
+// Gate/up tile (a, pj, cg, s): 256 output columns of projection pj over
+// split s of the joint reduction axis [x (H inputs) | z (r ranks)], i.e. the
+// VQ gather sum and V^T z accumulate in the same MFMA accumulators. The last
+// of the 2 ns tiles of (a, cg) applies p = silu(g) * u.
+template <int D>
+__device__ void item_gateup(const Plan& P, const Args& A, int jt, const uint4* cbs, uint8_t* smem) {
+  __shared__ int s_last;
+  const int s = jt % P.ns;
+  jt /= P.ns;
+  const int cg = jt % P.ncg;
+  jt /= P.ncg;
+  const int pj = jt & 1, a = jt >> 1;
+  const Routing R = expert_of(P, A, a);
+  const int H = P.H, I = P.I, r = P.r, B = P.B;
+  const int KSX = H / 32, KSZ = (r + 31) / 32, KS = KSX + KSZ;
+  const int ks0 = s * KS / P.ns, ks1 = (s + 1) * KS / P.ns;
+  const int x0 = min(ks0, KSX), x1 = min(ks1, KSX);
+  const int z0 = max(ks0, KSX) - KSX, z1 = max(ks1, KSX) - KSX;
+  const int w = threadIdx.x >> 6;
+  const int c0 = cg * kColsPerGroup + w * 64;
+  const uint8_t* codes = (pj ? A.L.codes_up : A.L.codes_gate) + (size_t)R.e * (H / D) * I;
+  const uint16_t* V = r > 0 ? (pj ? A.L.V_up : A.L.V_gate) + (size_t)R.e * r * I : nullptr;
+
+  const int ldx = (x1 - x0) * 4 + 1, ldz = (z1 - z0) * 8 + 1;
+  uint4* xs = reinterpret_cast<uint4*>(smem);
+  uint4* zs = xs + P.nt_max * ldx;
+  float* gu = wsp<float>(A, P.o_gu);
+  const int* slot_tok = wsp<const int>(A, P.o_slot_tok);
+  const float* zsrc = (P.flags & F_Z) ? A.z_out : A.z_in;
+  const uint4* cb = cbs + pj * 256;
+
+  VqPipe<D, 1, kPdVq> vq;
+  DensePipe<2, kPdDense> lr;
+  for (int tg = 0; tg < R.ne; tg += kTokPass) {
+    const int nt = min(kTokPass, R.ne - tg);
+    vq.prime(codes, I, c0, I, x0, x1);
+    lr.prime(V, I, c0, I, r, z0, z1);
+    __syncthreads();
+    stage_bf16(xs, ldx, nt, (x1 - x0) * 4,
+               [&](int t) { return A.x + (size_t)slot_tok[R.s0 + tg + t] * H + x0 * 32; });
+    if (z1 > z0) {
+      // rank rows past r are zero-padded on both operands
+      const int nz = (z1 - z0) * 32;
+      for (int i = threadIdx.x; i < nt * (nz / 8); i += kWG) {
+        const int t = i / (nz / 8), jj = i % (nz / 8);
+        const float* zr = zsrc + ((size_t)pj * B + slot_tok[R.s0 + tg + t]) * r;
+        uint32_t h[8], lw[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int q = z0 * 32 + 8 * jj + u;
+          const float f = q < r ? zr[q] : 0.0f;
+          h[u] = rne_bf16(f);
+          lw[u] = rne_bf16(f - bf(h[u]));
+        }
+        zs[t * ldz + 2 * jj] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                                          h[6] | (h[7] << 16));
+        zs[t * ldz + 2 * jj + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
+                                              lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
+      }
+    }
+    __syncthreads();
+    f32x4 acc[4];
+    zero_acc(acc);
+    vq.run(cb, xs, ldx, x0, nt, acc);
+    lr.run(zs, ldz, z0, nt, acc);
+    store_acc(acc, nt, c0, I, [&](int t) { return gu + (((size_t)(R.s0 + tg + t) * 2 + pj) * P.ns + s) * I; });
+  }
+
+  int* tick = wsp<int>(A, P.o_gu_tick) + a * P.ncg + cg;
+  if (!last_of(tick, 2 * P.ns, &s_last)) return;
+  // the last tile of (a, cg): p = silu(sum of gate splits) * (sum of up splits)
+  const int cc = cg * kColsPerGroup + threadIdx.x;
+  float* pbuf = wsp<float>(A, P.o_p);
+  if (cc < I) {
+    for (int t = 0; t < R.ne; ++t) {
+      const float* src = gu + (size_t)(R.s0 + t) * 2 * P.ns * I + cc;
+      float gs = 0.0f, us = 0.0f;
+      for (int j0 = 0; j0 < P.ns; j0 += 8) {
+        float vg[8], vu[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          vg[j] = (j0 + j < P.ns) ? src[(size_t)(j0 + j) * I] : 0.0f;
+          vu[j] = (j0 + j < P.ns) ? src[(size_t)(P.ns + j0 + j) * I] : 0.0f;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          gs += vg[j];
+          us += vu[j];
+        }
+      }
+      pbuf[(size_t)(R.s0 + t) * I + cc] = gs / (1.0f + expf(-gs)) * us;
+    }
+  }
+  if (threadIdx.x == 0) *tick = 0;
+  arrive(wsp<int>(A, P.o_gu_done) + a);
+}
+
+// Down tile (a, cgx, s) over split s of I, 256 output columns: for cgx <
+// ncgh the VQ columns of H (Q^T p -> dn[s]), else the low-rank columns of r
+// (A_e^T p -> uap[s]). Weight loads are issued before waiting for the
+// expert's p.
+template <typename Pipe, typename Prime, typename Run, typename Dst>
+__device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Routing& R, int a, int s,
+                                          int ks0, int ks1, int c0, int n_out, Pipe& pipe, Prime prime,
+                                          Run run, Dst dst, uint8_t* smem) {
+  prime();
+  wait_geq(A, wsp<int>(A, P.o_gu_done) + a, P.ncg);
+  const int I = P.I;
+  const int ld = (ks1 - ks0) * 8 + 1;
+  uint4* ps = reinterpret_cast<uint4*>(smem);
+  const float* pbuf = wsp<const float>(A, P.o_p);
+  for (int tg = 0; tg < R.ne; tg += kTokPass) {
+    const int nt = min(kTokPass, R.ne - tg);
+    if (tg > 0) prime();
+    __syncthreads();
+    stage_split(ps, ld, nt, (ks1 - ks0) * 4,
+                [&](int t) { return pbuf + (size_t)(R.s0 + tg + t) * I + ks0 * 32; });
+    __syncthreads();
+    f32x4 acc[4];
+    zero_acc(acc);
+    run(ps, ld, nt, acc);
+    store_acc(acc, nt, c0, n_out, [&](int t) { return dst(R.s0 + tg + t); });
+  }
+  arrive(ctr(A, C_DOWN_DONE));
+  (void)pipe;
+  (void)s;
+}
+
+template <int D>
+__device__ void item_down_vq(const Plan& P, const Args& A, int a, int cgx, int s,
+                                          const uint4* cbs, uint8_t* smem) {
+  const Routing R = expert_of(P, A, a);
+  const int H = P.H, I = P.I, S = P.S, KS = I / 32;
+  const int ks0 = s * KS / P.nsd, ks1 = (s + 1) * KS / P.nsd;
+  const int c0 = cgx * kColsPerGroup + (threadIdx.x >> 6) * 64;
+  const uint8_t* codes = A.L.codes_down + (size_t)R.e * (I / D) * H;
+  float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
+  VqPipe<D, 2, kPdVq> pipe;
+  down_body(P, A, R, a, s, ks0, ks1, c0, H, pipe, [&]() { pipe.prime(codes, H, c0, H, ks0, ks1); },
+            [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs + 2 * 256, ps, ld, ks0, nt, acc); },
+            [&](int slot) { return dn + (size_t)slot * H; }, smem);
+}
+
+__device__ void item_down_lr(const Plan& P, const Args& A, int a, int cgr, int s,
+                                          uint8_t* smem) {
+  const Routing R = expert_of(P, A, a);
+  const int I = P.I, r = P.r, S = P.S, KS = I / 32;
+  const int ks0 = s * KS / P.nsd, ks1 = (s + 1) * KS / P.nsd;
+  const int c0 = cgr * kColsPerGroup + (threadIdx.x >> 6) * 64;
+  const uint16_t* Ae = A.L.A_down + (size_t)R.e * I * r;
+  float* uap = wsp<float>(A, P.o_uap) + (size_t)s * S * r;
+  DensePipe<2, kPdDense> pipe;
+  down_body(P, A, R, a, s, ks0, ks1, c0, r, pipe, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); },
+            [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(ps, ld, ks0, nt, acc); },
+            [&](int slot) { return uap + (size_t)slot * r; }, smem);
+}
+
+// Combine tile (cgy, tq): output columns [256 cgy, +256) of tokens
+// [tpc tq, tpc tq + tpc): y[t] = sum_j a_j sum_s dn[s][slot_j] + B^T u[t]
+// with u[t] = sum_j a_j sum_s uap[s][slot_j]. B rows are loaded before the
+// wait; B^T u runs on MFMA with u as bf16 hi/lo.
+__device__ void item_combine(const Plan& P, const Args& A, int jc, int nact, uint8_t* smem) {
+  const int cgy = jc % P.ncgh, tq = jc / P.ncgh;
+  const int H = P.H, r = P.r, k = P.k, S = P.S;
+  const int t0 = tq * P.tpc, nt = min(P.tpc, P.B - t0);
+  const int w = threadIdx.x >> 6;
+  const int c0 = cgy * kColsPerGroup + w * 64;
+  const int KSR = (r + 31) / 32;
+  DensePipe<2, kPdDense> bp;
+  if (r > 0) bp.prime(A.L.B_down, H, c0, H, r, 0, KSR);
+
+  wait_geq(A, ctr(A, C_DOWN_DONE), nact * down_tiles_per_expert(P));
+
+  const float* slot_w = wsp<const float>(A, P.o_slot_w);
+  const int* tok_slot = wsp<const int>(A, P.o_tok_slot);
+  const float* dn = wsp<const float>(A, P.o_dn);
+  const float* uap = wsp<const float>(A, P.o_uap);
+  f32x4 acc[4];
+  zero_acc(acc);
+  if (r > 0) {
+    const int ld = KSR * 8 + 1;
+    uint4* us = reinterpret_cast<uint4*>(smem);
+    for (int i = threadIdx.x; i < nt * KSR * 4; i += kWG) {
+      const int t = i / (KSR * 4), jj = i % (KSR * 4);
+      uint32_t h[8], lw[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int q = 8 * jj + u;
+        float v = 0.0f;
+        if (q < r) {
+          for (int j = 0; j < k; ++j) {
+            const int sl = tok_slot[(t0 + t) * k + j];
+            if (sl < 0) continue;
+            float sv = 0.0f;
+            for (int ss = 0; ss < P.nsd; ++ss) sv += uap[((size_t)ss * S + sl) * r + q];
+            v = fmaf(slot_w[sl], sv, v);
+          }
+        }
+        h[u] = rne_bf16(v);
+        lw[u] = rne_bf16(v - bf(h[u]));
+      }
+      us[t * ld + 2 * jj] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                                       h[6] | (h[7] << 16));
+      us[t * ld + 2 * jj + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
+                                           lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
+    }
+    __syncthreads();
+    bp.run(us, ld, 0, nt, acc);
+  }
+  // VQ part and output: token rows 4g + i of this wave's 64 columns
+  const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
+  const int col = c0 + 4 * n;
+  if (col < H) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = 4 * g + i;
+      if (t >= nt) continue;
+      float4 vq = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int j = 0; j < k; ++j) {
+        const int sl = tok_slot[(t0 + t) * k + j];
+        if (sl < 0) continue;
+        float4 sv = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int ss = 0; ss < P.nsd; ++ss) {
+          const float4 d = *reinterpret_cast<const float4*>(dn + ((size_t)ss * S + sl) * H + col);
+          sv.x += d.x;
+          sv.y += d.y;
+          sv.z += d.z;
+          sv.w += d.w;
+        }
+        const float wj = slot_w[sl];
+        vq.x = fmaf(wj, sv.x, vq.x);
+        vq.y = fmaf(wj, sv.y, vq.y);
+        vq.z = fmaf(wj, sv.z, vq.z);
+        vq.w = fmaf(wj, sv.w, vq.w);
+      }
+      *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) =
+          make_float4(vq.x + acc[0][i], vq.y + acc[1][i], vq.z + acc[2][i], vq.w + acc[3][i]);
+    }
+  }
+}
+
+// ===========================================================================
+// the two persistent kernels of a layer call
+// ===========================================================================
+// The last workgroup to leave a kernel clears that kernel's counters, so the
+// workspace is ready for the next call.
+__device__ __forceinline__ void exit_and_reset(const Args& A, int exit_ctr, const int* clear,
+                                               int n_clear, int* arr, int n_arr) {
+  __shared__ int s_last;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = (atomicAdd(ctr(A, exit_ctr), 1) == (int)gridDim.x - 1);
+  __syncthreads();
+  if (!s_last) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  if (threadIdx.x < n_clear) *ctr(A, clear[threadIdx.x]) = 0;
+  for (int e = threadIdx.x; e < n_arr; e += kWG) arr[e] = 0;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+}
+
+// Routing-independent work and the routing itself: router chunks, z units,
+// per-token select (the last one groups the slots), z reduce.
+__global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  for (int j = blockIdx.x; j < P.n_pre; j += gridDim.x) {
+    __syncthreads();
+    int jj = j;
+    if (jj < P.n_rc) {
+      item_router_chunk(P, A, jj % P.nch_r, jj / P.nch_r, smem);
+      continue;
+    }
+    jj -= P.n_rc;
+    if (jj < P.n_zc) {
+      item_z(P, A, jj, smem);
+      continue;
+    }
+    jj -= P.n_zc;
+    if (jj < P.n_sel) {
+      item_select(P, A, jj, smem);
+      continue;
+    }
+    jj -= P.n_sel;
+    item_z_reduce(P, A, jj);
+  }
+  const int clear[4] = {C_ROUTE_ARR, C_Z_ARR, C_SEL_ARR, C_EXIT_R};
+  exit_and_reset(A, C_EXIT_R, clear, 4, nullptr, 0);
+}
+
+// Expert work of the active experts (count published by k_route): gate/up
+// tiles, down tiles (waiting per expert for p), combine tiles (waiting for
+// every down tile).
+template <int D>
+__global__ __launch_bounds__(kWG) void k_expert(Plan P, Args A) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  __shared__ uint4 cbs[3 * 256];  // gate, up, down code books (zero-padded to 256 words)
+  const int tid = threadIdx.x;
+  {
+    // code word c of book b at cbs[b * 256 + c] (d = 8) or at the 8-byte
+    // slot b * 512 + c of the uint2 view (d = 4)
+    uint16_t* c16 = reinterpret_cast<uint16_t*>(cbs);
+    const uint16_t* src[3] = {A.L.cb_gate, A.L.cb_up, A.L.cb_down};
+    for (int b = 0; b < 3; ++b)
+      for (int i = tid; i < 256 * D; i += kWG) {
+        const int word = i / D;
+        c16[b * 256 * 8 + i] = word < P.K ? src[b][i] : (uint16_t)0;
+      }
+  }
+  const int nact = *wsp<const int>(A, P.o_nact);
+  const int tgu = gateup_tiles_per_expert(P), tdn = down_tiles_per_expert(P);
+  const int n_items = nact * (tgu + tdn) + P.n_cb;
+  for (int jp = blockIdx.x; jp < n_items; jp += gridDim.x) {
+    __syncthreads();
+    int j = jp;
+    if (j < nact * tgu) {
+      item_gateup<D>(P, A, j, cbs, smem);
+      continue;
+    }
+    j -= nact * tgu;
+    if (j < nact * tdn) {
+      const int a = j / tdn, rem = j % tdn, cgx = rem / P.nsd, s = rem % P.nsd;
+      if (cgx < P.ncgh)
+        item_down_vq<D>(P, A, a, cgx, s, cbs, smem);
+      else
+        item_down_lr(P, A, a, cgx - P.ncgh, s, smem);
+      continue;
+    }
+    j -= nact * tdn;
+    item_combine(P, A, j, nact, smem);
+  }
+  const int clear[2] = {C_DOWN_DONE, C_EXIT_E};
+  exit_and_reset(A, C_EXIT_E, clear, 2, wsp<int>(A, P.o_gu_done), P.E);
+}
+
+// x_next = bf16_rne(y / sqrt(mean(y^2) + eps)) per token.
+__global__ __launch_bounds__(kWG) void k_rmsnorm(int H, const float* __restrict__ y, float eps,
+                                                 uint16_t* __restrict__ xn) {
+  __shared__ float part[4];
+  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const float* yr = y + (size_t)t * H;
+  float ss = 0.0f;
+  for (int h = tid; h < H; h += kWG) ss = fmaf(yr[h], yr[h], ss);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  if (lane == 0) part[w] = ss;
+  __syncthreads();
+  const float tot = part[0] + part[1] + part[2] + part[3];
+  const float inv = 1.0f / sqrtf(tot / (float)H + eps);
+  for (int h = tid; h < H; h += kWG) xn[(size_t)t * H + h] = (uint16_t)rne_bf16(yr[h] * inv);
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+const void* route_kernel() { return reinterpret_cast<const void*>(&k_route); }
+
+const void* expert_kernel(int d) {
+  return d == 8 ? reinterpret_cast<const void*>(&k_expert<8>)
+                : reinterpret_cast<const void*>(&k_expert<4>);
+}
+
+hipError_t launch_route(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st) {
+  hipLaunchKernelGGL(k_route, dim3(grid), dim3(kWG), lds, st, P, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_expert(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st) {
+  if (P.d == 8)
+    hipLaunchKernelGGL(k_expert<8>, dim3(grid), dim3(kWG), lds, st, P, A);
+  else
+    hipLaunchKernelGGL(k_expert<4>, dim3(grid), dim3(kWG), lds, st, P, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(hipStream_t st, int B, int H, const float* y, float eps, uint16_t* xn) {
+  hipLaunchKernelGGL(k_rmsnorm, dim3(B), dim3(kWG), 0, st, H, y, eps, xn);
+  return hipGetLastError();
+}
+
+}  // namespace cardan

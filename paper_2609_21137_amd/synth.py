@@ -41,13 +41,13 @@ def _rng(seed: int, layer: int, tensor_id: int, extra: int = 0) -> np.random.Gen
 def f32_to_bf16_bits(a) -> np.ndarray:
     """Round float32 values to bf16 (nearest, ties to even); return uint16 bits."""
     f = np.ascontiguousarray(np.asarray(a, dtype=np.float32))
-    u = f.view(np.uint32).astype(np.uint64)
-    rounded = (u + np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)
-    out = rounded.astype(np.uint16)
+    u = f.view(np.uint32)
     nan = np.isnan(f)
     if nan.any():
-        out[nan] = np.uint16(0x7FC0)
-    return out
+        u = np.where(nan, np.uint32(0x7FC00000), u)
+    # finite inputs cannot overflow: the largest is 0xFF7FFFFF + 0x8000
+    rounded = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return rounded.astype(np.uint16)
 
 
 def to_bf16_bits(a) -> np.ndarray:
