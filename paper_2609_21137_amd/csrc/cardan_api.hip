@@ -18,6 +18,7 @@ const void* route_kernel();
 const void* expert_kernel(int d);
 hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t);
 hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t);
+hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t);
 hipError_t launch_rmsnorm(hipStream_t, int, int, const float*, float, uint16_t*);
 }  // namespace cardan
 
@@ -141,19 +142,25 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.n_zr = (flags & F_Z) ? ceil_div(2 * B * P.r, kWG) : 0;
   P.n_pre = P.n_rc + P.n_zc + P.n_sel + P.n_zr;
 
-  // counters first, at offsets that depend only on (E, I)
+  // counters first, at offsets that depend only on the shape
+  P.n_rc_flags = P.nch_r * P.n_eg;
+  P.n_zc_flags = ceil_div(2 * ceil_div(P.r, 64) * P.nch_z, 4);
   size_t o = 0;
   P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);
-  P.o_gu_tick = o; o = align256(o + (size_t)kMaxE * ceil_div(P.I, kColsPerGroup) * 4);
-  P.o_gu_done = o; o = align256(o + (size_t)kMaxE * 4);
+  P.o_rc_flag = o; o = align256(o + (size_t)P.n_rc_flags * 4);
+  P.o_zc_flag = o; o = align256(o + (size_t)P.n_zc_flags * 4);
+  P.o_gu_tick = o; o = align256(o + (size_t)P.E * P.ncg * 4);
+  P.o_gu_done = o; o = align256(o + (size_t)P.E * 4);
+  P.o_dn_done = o; o = align256(o + (size_t)P.E * (P.ncgh + P.ncgr) * 4);
   P.o_rl = o; o = align256(o + (size_t)P.nch_r * B * P.E * 8);
   P.o_zp = o; o = align256(o + (size_t)2 * P.nch_z * B * P.r * 4);
   P.o_z = o; o = align256(o + (size_t)2 * B * P.r * 4);
   P.o_off = o; o = align256(o + (size_t)(P.E + 1) * 4);
-  P.o_act = o; o = align256(o + (size_t)P.E * 4);
+  P.o_act = o; o = align256(o + (size_t)P.E * 16);  // int4 (expert, first slot, count, 0)
   P.o_nact = o; o = align256(o + 4);
   P.o_slot_tok = o; o = align256(o + (size_t)P.S * 4);
   P.o_slot_w = o; o = align256(o + (size_t)P.S * 4);
+  P.o_slot_e = o; o = align256(o + (size_t)P.S * 4);
   P.o_tok_slot = o; o = align256(o + (size_t)P.S * 4);
   P.o_gu = o; o = align256(o + (size_t)P.S * 2 * P.ns * P.I * 4);
   P.o_p = o; o = align256(o + (size_t)P.S * P.I * 4);
@@ -277,6 +284,10 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
     err = launch_route(P, A, std::min(cap, P.n_pre), P.lds_route, stream);
     if (err != hipSuccess) return hip_fail(err, "k_route launch");
     tm.done();
+    if (!(P.flags & F_EXPERTS)) {  // k_expert would clear these counters
+      err = launch_route_reset(P, A, stream);
+      if (err != hipSuccess) return hip_fail(err, "k_route_reset launch");
+    }
   }
   if (P.flags & F_EXPERTS) {
     const int cap = resident_grid(expert_kernel(P.d), P.lds_expert, &err);

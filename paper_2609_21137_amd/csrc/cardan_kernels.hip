@@ -57,42 +57,139 @@ __device__ __forceinline__ T* wsp(const Args& A, size_t off) {
   return reinterpret_cast<T*>(A.ws + off);
 }
 
-// Makes this workgroup's global writes visible device-wide, then adds 1 to
-// `c`. Every wave releases its own stores before the barrier.
-__device__ __forceinline__ void arrive(int* c) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  if (threadIdx.x == 0) atomicAdd(c, 1);
+// ---- optional item timeline (debug builds with CARDAN_TRACE) --------------
+// Records per work item the device real-time clock (100 MHz, shared by all
+// CUs) at start, after its dependency wait and at end, into workspace bytes
+// past the normal layout. Compiled out of the library by default.
+#ifdef CARDAN_TRACE
+__shared__ unsigned long long s_trace[5];  // wait end, then up to 4 phase marks
+__device__ __forceinline__ unsigned long long rt_clock() { return __builtin_amdgcn_s_memrealtime(); }
+__device__ __forceinline__ void trace_wait_done() {
+  if (threadIdx.x == 0) s_trace[0] = rt_clock();
+}
+__device__ __forceinline__ void trace_mark(int i) {
+  if (threadIdx.x == 0) s_trace[1 + i] = rt_clock();
+}
+struct ItemTrace {
+  unsigned long long t0;
+  __device__ __forceinline__ ItemTrace() : t0(rt_clock()) {
+    if (threadIdx.x < 5) s_trace[threadIdx.x] = 0;
+  }
+  __device__ __forceinline__ void done(const Args& A, const Plan& P, int slot, int kind) {
+    if (threadIdx.x != 0) return;
+    unsigned long long* rec = reinterpret_cast<unsigned long long*>(A.ws + P.total) + 8 * (size_t)slot;
+    rec[0] = ((unsigned long long)kind << 48) | ((unsigned long long)blockIdx.x << 24) | (unsigned)slot;
+    rec[1] = t0;
+    rec[2] = s_trace[0];
+    rec[3] = rt_clock();
+    for (int i = 0; i < 4; ++i) rec[4 + i] = s_trace[1 + i];
+  }
+};
+#else
+__device__ __forceinline__ void trace_wait_done() {}
+__device__ __forceinline__ void trace_mark(int) {}
+struct ItemTrace {
+  __device__ __forceinline__ void done(const Args&, const Plan&, int, int) {}
+};
+#endif
+
+// ---- cross-workgroup communication ------------------------------------------
+// Data handed from one workgroup to another inside a kernel is written with
+// device-scope stores and read with device-scope loads (sc1: coherent across
+// the separate L2 caches of the XCDs), so no cache writeback or invalidation
+// is ever issued; a producer only drains its own stores before it signals.
+// Counters and flags are zeroed by the other kernel of the call (kernel
+// boundaries order that), so every signal is a single relaxed atomic.
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(double* p, double v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_dev(const double* p) {
+  return __hip_atomic_load(const_cast<double*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int ld_dev(const int* p) {
+  return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev4(float* p, float4 v) {
+  st_dev(p, v.x);
+  st_dev(p + 1, v.y);
+  st_dev(p + 2, v.z);
+  st_dev(p + 3, v.w);
+}
+__device__ __forceinline__ float4 ld_dev4(const float* p) {
+  return make_float4(ld_dev(p), ld_dev(p + 1), ld_dev(p + 2), ld_dev(p + 3));
 }
 
-// Waits until *c >= target (thread 0 polls), then acquires. Bounded: on
-// timeout the error counter is raised and the caller proceeds, so the grid
-// always drains.
-__device__ __forceinline__ void wait_geq(const Args& A, int* c, int target) {
+// Waits for this wave's outstanding memory operations (s_waitcnt vmcnt(0)).
+__device__ __forceinline__ void drain_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// One arrival on counter c once every wave's stores have completed.
+__device__ __forceinline__ void publish(int* c) {
+  drain_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Sets flag f once every wave's stores have completed.
+__device__ __forceinline__ void set_flag(int* f) {
+  drain_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) st_dev(f, 1);
+}
+
+// Waits until *c >= target (thread 0 polls). Bounded: on timeout the status
+// counter is raised and the caller proceeds, so the grid always drains.
+__device__ __forceinline__ void wait_geq(const Args& A, const int* c, int target) {
   if (threadIdx.x == 0) {
     unsigned it = 0;
-    while (__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      __builtin_amdgcn_s_sleep(2);
+    while (ld_dev(c) < target) {
+      __builtin_amdgcn_s_sleep(4);
       if (++it > kSpinLimit) {
         atomicAdd(ctr(A, C_ERR), 1);
         break;
       }
     }
+    trace_wait_done();
   }
   __syncthreads();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
-// Ticket: after every wave released its writes, returns true in the one
-// workgroup that arrives last of `total` (which then acquires and resets).
+// Waits until cond(i) holds for every i in [0, n) (threads test in parallel).
+template <typename F>
+__device__ __forceinline__ void wait_all(const Args& A, int n, F cond) {
+  unsigned it = 0;
+  for (;;) {
+    bool mine = true;
+    for (int i = threadIdx.x; i < n; i += kWG) mine = mine && cond(i);
+    if (__syncthreads_and(mine)) {
+      trace_wait_done();
+      break;
+    }
+    __builtin_amdgcn_s_sleep(4);
+    if (++it > kSpinLimit) {
+      if (threadIdx.x == 0) atomicAdd(ctr(A, C_ERR), 1);
+      break;
+    }
+  }
+}
+
+// Ticket: true in the one workgroup that arrives last of `total`; every
+// workgroup drains its stores first, so the last one may read them all.
 __device__ __forceinline__ bool last_of(int* tick, int total, int* s_flag) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  drain_stores();
   __syncthreads();
-  if (threadIdx.x == 0) *s_flag = (atomicAdd(tick, 1) == total - 1);
+  if (threadIdx.x == 0)
+    *s_flag = (__hip_atomic_fetch_add(tick, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == total - 1);
   __syncthreads();
-  const bool last = *s_flag;
-  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  return last;
+  return *s_flag;
 }
 
 // Exclusive prefix sum of arr[0..n) (n <= 4 * kWG) in place; returns the total.
@@ -131,7 +228,7 @@ __device__ int block_exclusive_scan(int* arr, int n, int* tmp4) {
 // four lane groups (lane >> 4) own rows h = 4i + (lane >> 4). float64
 // accumulation of exact bf16 products; the four row groups are combined with
 // a fixed shuffle tree.
-__device__ void item_router_chunk(const Plan& P, const Args& A, int c, int g, uint8_t* smem) {
+__device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c, int g, uint8_t* smem) {
   float* xs = reinterpret_cast<float*>(smem);  // [16][64] (bf16 values are exact in f32)
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int E = P.E, H = P.H, B = P.B, h0 = c * kRowsRouter;
@@ -149,6 +246,7 @@ __device__ void item_router_chunk(const Plan& P, const Args& A, int c, int g, ui
       xs[i] = t < nt ? bf(A.x[(size_t)(tg + t) * H + h0 + h]) : 0.0f;
     }
     __syncthreads();
+    trace_mark(0);
     double acc[kTokPass];
 #pragma unroll
     for (int t = 0; t < kTokPass; ++t) acc[t] = 0.0;
@@ -157,21 +255,26 @@ __device__ void item_router_chunk(const Plan& P, const Args& A, int c, int g, ui
       const double wd = (double)bf(wv[i]);
       const int h = rq + 4 * i;
 #pragma unroll
-      for (int t = 0; t < kTokPass; ++t) acc[t] = fma(wd, (double)xs[t * kRowsRouter + h], acc[t]);
+      for (int t = 0; t < kTokPass; ++t)
+        if (t < nt) acc[t] = fma(wd, (double)xs[t * kRowsRouter + h], acc[t]);
     }
 #pragma unroll
     for (int t = 0; t < kTokPass; ++t) {
-      acc[t] += __shfl_xor(acc[t], 16);
-      acc[t] += __shfl_xor(acc[t], 32);
+      if (t < nt) {
+        acc[t] += __shfl_xor(acc[t], 16);
+        acc[t] += __shfl_xor(acc[t], 32);
+      }
     }
+    trace_mark(1);
     if (rq == 0 && ev) {
 #pragma unroll
       for (int t = 0; t < kTokPass; ++t)
-        if (t < nt) rl[((size_t)c * B + tg + t) * E + e] = acc[t];
+        if (t < nt) st_dev(rl + ((size_t)c * B + tg + t) * E + e, acc[t]);
     }
     __syncthreads();
   }
-  arrive(ctr(A, C_ROUTE_ARR));
+  trace_mark(2);
+  set_flag(wsp<int>(A, P.o_rc_flag) + item);
 }
 
 // Groups the B*k routing slots by expert (single workgroup): per-expert
@@ -189,9 +292,10 @@ __device__ void group_slots(const Plan& P, const Args& A, const int32_t* __restr
   int* g_slot_tok = wsp<int>(A, P.o_slot_tok);
   float* g_slot_w = wsp<float>(A, P.o_slot_w);
   int* g_tok_slot = wsp<int>(A, P.o_tok_slot);
+  int* g_slot_e = wsp<int>(A, P.o_slot_e);
   for (int e = tid; e < E; e += kWG) s_cnt[e] = 0;
   for (int i = tid; i < S; i += kWG) {
-    const int e = idx[i];
+    const int e = ld_dev(idx + i);
     s_idx[i] = (e >= 0 && e < E) ? e : -1;
   }
   __syncthreads();
@@ -206,7 +310,7 @@ __device__ void group_slots(const Plan& P, const Args& A, const int32_t* __restr
     const int o = s_cnt[e];
     const int o1 = (e + 1 < E) ? s_cnt[e + 1] : total;
     g_off[e] = o;
-    if (o1 > o) g_act[s_flag[e]] = e;
+    if (o1 > o) reinterpret_cast<int4*>(g_act)[s_flag[e]] = make_int4(e, o, o1 - o, 0);
   }
   if (tid == 0) {
     g_off[E] = total;
@@ -222,7 +326,8 @@ __device__ void group_slots(const Plan& P, const Args& A, const int32_t* __restr
     for (int j = 0; j < i; ++j) rank += (s_idx[j] == e);
     const int pos = s_cnt[e] + rank;
     g_slot_tok[pos] = i / k;
-    g_slot_w[pos] = wts[i];
+    g_slot_w[pos] = ld_dev(wts + i);
+    g_slot_e[pos] = e;
     g_tok_slot[i] = pos;
   }
 }
@@ -239,22 +344,24 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
   if (P.flags & F_ROUTE) {
     double* lg = reinterpret_cast<double*>(smem);          // [E]
     int* sel = reinterpret_cast<int*>(lg + kMaxE);          // [k]
-    wait_geq(A, ctr(A, C_ROUTE_ARR), P.n_rc);
+    const int* rcf = wsp<const int>(A, P.o_rc_flag);
+    wait_all(A, P.n_rc, [&](int i) { return ld_dev(rcf + i) != 0; });
     const double* rl = wsp<const double>(A, P.o_rl);
     for (int e = tid; e < E; e += kWG) {
       double s = 0.0;
-      for (int c0 = 0; c0 < P.nch_r; c0 += 8) {
-        double v[8];
+      for (int c0 = 0; c0 < P.nch_r; c0 += 32) {
+        double v[32];
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-          v[i] = (c0 + i < P.nch_r) ? rl[((size_t)(c0 + i) * B + t) * E + e] : 0.0;
+        for (int i = 0; i < 32; ++i)
+          v[i] = (c0 + i < P.nch_r) ? ld_dev(rl + ((size_t)(c0 + i) * B + t) * E + e) : 0.0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) s += v[i];
+        for (int i = 0; i < 32; ++i) s += v[i];
       }
       if (A.L.router_bias) s += (double)A.L.router_bias[e];
       lg[e] = s;
     }
     __syncthreads();
+    trace_mark(0);
     if (w == 0) {
       for (int j = 0; j < k; ++j) {
         double bv = -INFINITY;
@@ -287,15 +394,17 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
       if (lane < k) {
-        A.topk_idx[t * k + lane] = sel[lane];
-        A.topk_w[t * k + lane] = (float)(ex / sum);
+        st_dev(A.topk_idx + t * k + lane, sel[lane]);
+        st_dev(A.topk_w + t * k + lane, (float)(ex / sum));
       }
     }
     if (!(P.flags & F_GROUP)) return;
-    if (!last_of(ctr(A, C_SEL_ARR), P.n_sel, &s_last)) return;
+    trace_mark(1);
+    if (!last_of(ctr(A, C_SEL_TICK), P.n_sel, &s_last)) return;
+    trace_mark(2);
     group_slots(P, A, A.topk_idx, A.topk_w, smem);
   } else {
-    group_slots(P, A, A.idx_in, A.w_in, smem);
+    group_slots(P, A, A.idx_in, A.w_in, smem);  // caller routing, written before the call
   }
 }
 
@@ -303,7 +412,8 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
 // fixed-order sum of its chunk partials (both halves from one basis when
 // U_up is U_gate).
 __device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
-  wait_geq(A, ctr(A, C_Z_ARR), P.n_zc);
+  const int* zcf = wsp<const int>(A, P.o_zc_flag);
+  wait_all(A, P.n_zc, [&](int f) { return ld_dev(zcf + f) != 0; });
   const int o = i * kWG + threadIdx.x;
   const int B = P.B, r = P.r;
   if (o < 2 * B * r) {
@@ -311,12 +421,12 @@ __device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
     const int src = P.z_sep ? pj : 0;
     const float* zp = wsp<const float>(A, P.o_zp) + ((size_t)src * P.nch_z * B) * r + rem;
     float s = 0.0f;
-    for (int c0 = 0; c0 < P.nch_z; c0 += 8) {
-      float v[8];
+    for (int c0 = 0; c0 < P.nch_z; c0 += 32) {
+      float v[32];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = (c0 + j < P.nch_z) ? zp[(size_t)(c0 + j) * B * r] : 0.0f;
+      for (int j = 0; j < 32; ++j) v[j] = (c0 + j < P.nch_z) ? ld_dev(zp + (size_t)(c0 + j) * B * r) : 0.0f;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) s += v[j];
+      for (int j = 0; j < 32; ++j) s += v[j];
     }
     A.z_out[o] = s;
   }
@@ -350,29 +460,32 @@ struct VqPipe {
   uint32_t buf[PD][W];
   const uint8_t* codes;
   int row_len, col, ks0, nks;
-  bool cv;
 
+  // Unconditional, branch-free loads: lanes past n_out read the last valid
+  // columns, whose results are never stored.
   __device__ __forceinline__ void load(int ks, uint32_t (&b)[W]) {
     const int g = (threadIdx.x & 63) >> 4;
-    if (D == 8) {
-      b[0] = cv ? *reinterpret_cast<const uint32_t*>(codes + (size_t)(ks * 4 + g) * row_len + col) : 0u;
+    if constexpr (D == 8) {
+      b[0] = *reinterpret_cast<const uint32_t*>(codes + (size_t)(ks * 4 + g) * row_len + col);
     } else {
       const size_t row = (size_t)(ks * 8 + 2 * g);
-      b[0] = cv ? *reinterpret_cast<const uint32_t*>(codes + row * row_len + col) : 0u;
-      b[1] = cv ? *reinterpret_cast<const uint32_t*>(codes + (row + 1) * row_len + col) : 0u;
+      b[0] = *reinterpret_cast<const uint32_t*>(codes + row * row_len + col);
+      b[1] = *reinterpret_cast<const uint32_t*>(codes + (row + 1) * row_len + col);
     }
   }
-  // codes [n_in/d][row_len] of one expert; columns [c0, c0 + 64) of n_out
+  // codes [n_in/d][row_len] of one expert; columns [c0, c0 + 64) of n_out.
+  // Every pipeline slot always holds an issued load (steps past the end
+  // re-read the last step, which is already cached), so the number of loads
+  // in flight is static and the compiler waits for exactly one step.
   __device__ __forceinline__ void prime(const uint8_t* c, int rl, int c0, int n_out, int k0, int k1) {
     codes = c;
     row_len = rl;
-    col = c0 + 4 * (threadIdx.x & 15);
-    cv = col < n_out;
+    col = min(c0 + 4 * (threadIdx.x & 15), n_out - 4);
     ks0 = k0;
     nks = k1 - k0;
+    if (nks <= 0) return;
 #pragma unroll
-    for (int u = 0; u < PD; ++u)
-      if (u < nks) load(ks0 + u, buf[u]);
+    for (int u = 0; u < PD; ++u) load(ks0 + min(u, nks - 1), buf[u]);
   }
   __device__ __forceinline__ void step(int ks, const uint32_t (&b)[W], const uint4* __restrict__ cb_s,
                                        const uint4* __restrict__ ops, int ops_ld, int ops_ks0, int nt,
@@ -386,7 +499,7 @@ struct VqPipe {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       uint4 w;
-      if (D == 8) {
+      if constexpr (D == 8) {
         w = cb_s[(b[0] >> (8 * q)) & 255u];
       } else {
         const uint2 lo = cb2[(b[0] >> (8 * q)) & 255u];
@@ -403,13 +516,11 @@ struct VqPipe {
 #pragma unroll
       for (int u = 0; u < PD; ++u) {
         const int i = i0 + u;
-        if (i < nks) {
-          step(ks0 + i, buf[u], cb_s, ops, ops_ld, ops_ks0, nt, acc);
-          if (i + PD < nks) load(ks0 + i + PD, buf[u]);
-          // keep each step's LDS operand reads inside the step: hoisting them
-          // across the unrolled pipeline costs registers, not time
-          __builtin_amdgcn_sched_barrier(0);
-        }
+        if (i < nks) step(ks0 + i, buf[u], cb_s, ops, ops_ld, ops_ks0, nt, acc);
+        load(ks0 + min(i + PD, nks - 1), buf[u]);
+        // keep each step's LDS operand reads inside the step: hoisting them
+        // across the unrolled pipeline costs registers, not time
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
@@ -430,30 +541,31 @@ struct DensePipe {
   uint2 buf[PD][8];
   const uint16_t* W;
   int ld, col, k_rows, ks0, nks;
-  bool cv;
 
+  // Unconditional, branch-free loads: rows past k_rows re-read the last row
+  // (every caller zero-pads the activations of those rows) and lanes past
+  // n_out read the last valid columns, whose results are never stored.
   __device__ __forceinline__ void load(int ks, uint2 (&b)[8]) {
     const int g = (threadIdx.x & 63) >> 4;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int row = ks * 32 + 8 * g + e;
-      b[e] = (cv && row < k_rows) ? *reinterpret_cast<const uint2*>(W + (size_t)row * ld + col)
-                                  : make_uint2(0, 0);
+      const int row = min(ks * 32 + 8 * g + e, k_rows - 1);
+      b[e] = *reinterpret_cast<const uint2*>(W + (size_t)row * ld + col);
     }
   }
-  // W [k_rows][ld] row-major bf16; columns [c0, c0 + 64) of n_out
+  // W [k_rows][ld] row-major bf16; columns [c0, c0 + 64) of n_out. Slots
+  // are always loaded, as in VqPipe.
   __device__ __forceinline__ void prime(const uint16_t* w, int ldw, int c0, int n_out, int kr, int k0,
                                         int k1) {
     W = w;
     ld = ldw;
-    col = c0 + 4 * (threadIdx.x & 15);
-    cv = col < n_out;
+    col = min(c0 + 4 * (threadIdx.x & 15), n_out - 4);
     k_rows = kr;
     ks0 = k0;
     nks = k1 - k0;
+    if (nks <= 0) return;
 #pragma unroll
-    for (int u = 0; u < PD; ++u)
-      if (u < nks) load(ks0 + u, buf[u]);
+    for (int u = 0; u < PD; ++u) load(ks0 + min(u, nks - 1), buf[u]);
   }
   __device__ __forceinline__ void step(int ks, const uint2 (&b)[8], const uint4* __restrict__ ops, int ops_ld,
                                        int ops_ks0, int nt, f32x4 acc[4]) {
@@ -479,26 +591,24 @@ struct DensePipe {
 #pragma unroll
       for (int u = 0; u < PD; ++u) {
         const int i = i0 + u;
-        if (i < nks) {
-          step(ks0 + i, buf[u], ops, ops_ld, ops_ks0, nt, acc);
-          if (i + PD < nks) load(ks0 + i + PD, buf[u]);
-          __builtin_amdgcn_sched_barrier(0);
-        }
+        if (i < nks) step(ks0 + i, buf[u], ops, ops_ld, ops_ks0, nt, acc);
+        load(ks0 + min(i + PD, nks - 1), buf[u]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
 };
 
 constexpr int kPdVq = 16;    // code K-steps in flight per wave (256 B each)
-constexpr int kPdDense = 1;  // dense K-steps in flight per wave (4 KB each)
+constexpr int kPdDense = 2;  // dense K-steps in flight per wave (4 KB each)
 
 __device__ __forceinline__ void zero_acc(f32x4 acc[4]) {
 #pragma unroll
   for (int q = 0; q < 4; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
-// Stores token rows 4g + i < nt of the wave's accumulators: row t goes to
-// dst(t) + c0 + 4n as one float4 (the 4 MFMAs' columns).
+// Stores token rows 4g + i < nt of the wave's accumulators with device-scope
+// stores: row t goes to dst(t) + c0 + 4n (the 4 MFMAs' columns).
 template <typename F>
 __device__ __forceinline__ void store_acc(const f32x4 acc[4], int nt, int c0, int n_out, F dst) {
   const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
@@ -507,7 +617,7 @@ __device__ __forceinline__ void store_acc(const f32x4 acc[4], int nt, int c0, in
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int t = 4 * g + i;
-    if (t < nt) *reinterpret_cast<float4*>(dst(t) + col) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+    if (t < nt) st_dev4(dst(t) + col, make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]));
   }
 }
 
@@ -523,14 +633,15 @@ __device__ __forceinline__ void stage_bf16(uint4* ops, int ld, int nt, int n8, F
   }
 }
 
-// Stages float32 activation rows as bf16 hi/lo pairs: ops[t * ld + 2 j] (hi)
-// and [.. + 1] (lo) hold inputs 8 j .. 8 j + 7 of row src(t), value = hi + lo.
+// Stages float32 activation rows (produced in this kernel: device-scope
+// loads) as bf16 hi/lo pairs: ops[t * ld + 2 j] (hi) and [.. + 1] (lo) hold
+// inputs 8 j .. 8 j + 7 of row src(t), value = hi + lo.
 template <typename F>
 __device__ __forceinline__ void stage_split(uint4* ops, int ld, int nt, int n8, F src) {
   for (int i = threadIdx.x; i < nt * n8; i += kWG) {
     const int t = i / n8, j = i % n8;
-    const float4* p = reinterpret_cast<const float4*>(src(t) + 8 * j);
-    const float4 v0 = p[0], v1 = p[1];
+    const float* p = src(t) + 8 * j;
+    const float4 v0 = ld_dev4(p), v1 = ld_dev4(p + 4);
     const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
     uint32_t h[8], lw[8];
 #pragma unroll
@@ -584,7 +695,7 @@ __device__ void item_z(const Plan& P, const Args& A, int j, uint8_t* smem) {
       store_acc(acc, nt, c0, r, [&](int t) { return zp + (((size_t)pj * P.nch_z + s) * B + tg + t) * r; });
     }
   }
-  arrive(ctr(A, C_Z_ARR));
+  set_flag(wsp<int>(A, P.o_zc_flag) + j);
 }
 
 // ===========================================================================
@@ -594,11 +705,10 @@ struct Routing {
   int e, s0, ne;
 };
 
+// (expert, first slot, slot count) of active expert a: one 16-byte load
 __device__ __forceinline__ Routing expert_of(const Plan& P, const Args& A, int a) {
-  const int e = wsp<const int>(A, P.o_act)[a];
-  const int* off = wsp<const int>(A, P.o_off);
-  const int s0 = off[e];
-  return {e, s0, off[e + 1] - s0};
+  const int4 v = wsp<const int4>(A, P.o_act)[a];
+  return {v.x, v.y, v.z};
 }
 
 // Gate/up tile (a, pj, cg, s): 256 output columns of projection pj over
@@ -662,15 +772,20 @@ __device__ void item_gateup(const Plan& P, const Args& A, int jt, const uint4* c
       }
     }
     __syncthreads();
+    trace_mark(0);
     f32x4 acc[4];
     zero_acc(acc);
     vq.run(cb, xs, ldx, x0, nt, acc);
+    trace_mark(1);
     lr.run(zs, ldz, z0, nt, acc);
     store_acc(acc, nt, c0, I, [&](int t) { return gu + (((size_t)(R.s0 + tg + t) * 2 + pj) * P.ns + s) * I; });
+    trace_mark(2);
   }
 
   int* tick = wsp<int>(A, P.o_gu_tick) + a * P.ncg + cg;
-  if (!last_of(tick, 2 * P.ns, &s_last)) return;
+  const bool last = last_of(tick, 2 * P.ns, &s_last);
+  trace_mark(3);
+  if (!last) return;
   // the last tile of (a, cg): p = silu(sum of gate splits) * (sum of up splits)
   const int cc = cg * kColsPerGroup + threadIdx.x;
   float* pbuf = wsp<float>(A, P.o_p);
@@ -678,24 +793,24 @@ __device__ void item_gateup(const Plan& P, const Args& A, int jt, const uint4* c
     for (int t = 0; t < R.ne; ++t) {
       const float* src = gu + (size_t)(R.s0 + t) * 2 * P.ns * I + cc;
       float gs = 0.0f, us = 0.0f;
-      for (int j0 = 0; j0 < P.ns; j0 += 8) {
-        float vg[8], vu[8];
+      for (int j0 = 0; j0 < P.ns; j0 += 16) {
+        float vg[16], vu[16];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          vg[j] = (j0 + j < P.ns) ? src[(size_t)(j0 + j) * I] : 0.0f;
-          vu[j] = (j0 + j < P.ns) ? src[(size_t)(P.ns + j0 + j) * I] : 0.0f;
+        for (int j = 0; j < 16; ++j) {
+          vg[j] = (j0 + j < P.ns) ? ld_dev(src + (size_t)(j0 + j) * I) : 0.0f;
+          vu[j] = (j0 + j < P.ns) ? ld_dev(src + (size_t)(P.ns + j0 + j) * I) : 0.0f;
         }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < 16; ++j) {
           gs += vg[j];
           us += vu[j];
         }
       }
-      pbuf[(size_t)(R.s0 + t) * I + cc] = gs / (1.0f + expf(-gs)) * us;
+      st_dev(pbuf + (size_t)(R.s0 + t) * I + cc, gs / (1.0f + expf(-gs)) * us);
     }
   }
   if (threadIdx.x == 0) *tick = 0;
-  arrive(wsp<int>(A, P.o_gu_done) + a);
+  publish(wsp<int>(A, P.o_gu_done) + R.e);
 }
 
 // Down tile (a, cgx, s) over split s of I, 256 output columns: for cgx <
@@ -704,10 +819,10 @@ __device__ void item_gateup(const Plan& P, const Args& A, int jt, const uint4* c
 // expert's p.
 template <typename Pipe, typename Prime, typename Run, typename Dst>
 __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Routing& R, int a, int s,
-                                          int ks0, int ks1, int c0, int n_out, Pipe& pipe, Prime prime,
+                                          int cgx, int ks0, int ks1, int c0, int n_out, Pipe& pipe, Prime prime,
                                           Run run, Dst dst, uint8_t* smem) {
   prime();
-  wait_geq(A, wsp<int>(A, P.o_gu_done) + a, P.ncg);
+  wait_geq(A, wsp<int>(A, P.o_gu_done) + R.e, P.ncg);
   const int I = P.I;
   const int ld = (ks1 - ks0) * 8 + 1;
   uint4* ps = reinterpret_cast<uint4*>(smem);
@@ -724,9 +839,10 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
     run(ps, ld, nt, acc);
     store_acc(acc, nt, c0, n_out, [&](int t) { return dst(R.s0 + tg + t); });
   }
-  arrive(ctr(A, C_DOWN_DONE));
+  publish(wsp<int>(A, P.o_dn_done) + R.e * (P.ncgh + P.ncgr) + cgx);
   (void)pipe;
   (void)s;
+  (void)a;
 }
 
 template <int D>
@@ -739,7 +855,7 @@ __device__ void item_down_vq(const Plan& P, const Args& A, int a, int cgx, int s
   const uint8_t* codes = A.L.codes_down + (size_t)R.e * (I / D) * H;
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
   VqPipe<D, 2, kPdVq> pipe;
-  down_body(P, A, R, a, s, ks0, ks1, c0, H, pipe, [&]() { pipe.prime(codes, H, c0, H, ks0, ks1); },
+  down_body(P, A, R, a, s, cgx, ks0, ks1, c0, H, pipe, [&]() { pipe.prime(codes, H, c0, H, ks0, ks1); },
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs + 2 * 256, ps, ld, ks0, nt, acc); },
             [&](int slot) { return dn + (size_t)slot * H; }, smem);
 }
@@ -753,7 +869,7 @@ __device__ void item_down_lr(const Plan& P, const Args& A, int a, int cgr, int s
   const uint16_t* Ae = A.L.A_down + (size_t)R.e * I * r;
   float* uap = wsp<float>(A, P.o_uap) + (size_t)s * S * r;
   DensePipe<2, kPdDense> pipe;
-  down_body(P, A, R, a, s, ks0, ks1, c0, r, pipe, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); },
+  down_body(P, A, R, a, s, P.ncgh + cgr, ks0, ks1, c0, r, pipe, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); },
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(ps, ld, ks0, nt, acc); },
             [&](int slot) { return uap + (size_t)slot * r; }, smem);
 }
@@ -772,10 +888,23 @@ __device__ void item_combine(const Plan& P, const Args& A, int jc, int nact, uin
   DensePipe<2, kPdDense> bp;
   if (r > 0) bp.prime(A.L.B_down, H, c0, H, r, 0, KSR);
 
-  wait_geq(A, ctr(A, C_DOWN_DONE), nact * down_tiles_per_expert(P));
-
   const float* slot_w = wsp<const float>(A, P.o_slot_w);
   const int* tok_slot = wsp<const int>(A, P.o_tok_slot);
+  {
+    // every down tile of this column group (and of the low-rank columns) of
+    // every expert of these tokens
+    const int* slot_e = wsp<const int>(A, P.o_slot_e);
+    const int* dnd = wsp<const int>(A, P.o_dn_done);
+    const int ncol = 1 + P.ncgr, per_e = P.ncgh + P.ncgr;
+    wait_all(A, nt * k * ncol, [&](int i) {
+      const int c = i % ncol, tj = i / ncol;
+      const int sl = tok_slot[t0 * k + tj];
+      if (sl < 0) return true;
+      const int cgx = c == 0 ? cgy : P.ncgh + c - 1;
+      return ld_dev(dnd + slot_e[sl] * per_e + cgx) >= P.nsd;
+    });
+  }
+  (void)nact;
   const float* dn = wsp<const float>(A, P.o_dn);
   const float* uap = wsp<const float>(A, P.o_uap);
   f32x4 acc[4];
@@ -786,21 +915,39 @@ __device__ void item_combine(const Plan& P, const Args& A, int jc, int nact, uin
     for (int i = threadIdx.x; i < nt * KSR * 4; i += kWG) {
       const int t = i / (KSR * 4), jj = i % (KSR * 4);
       uint32_t h[8], lw[8];
+      // u[t][8 jj .. 8 jj + 8) = sum_j a_j sum_s uap[s][slot_j][q]: all (j, s)
+      // partials of 8 ranks in flight at once
+      float uq[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      const int npair = k * P.nsd;
+      for (int p0 = 0; p0 < npair; p0 += 4) {
+        float4 v[4][2];
+        float wj[4];
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp) {
+          const int pr = p0 + pp, j = pr / P.nsd, ss = pr % P.nsd;
+          const int sl = pr < npair ? tok_slot[(t0 + t) * k + j] : -1;
+          wj[pp] = sl >= 0 ? slot_w[sl] : 0.0f;
+          const float* src = uap + ((size_t)ss * S + (sl >= 0 ? sl : 0)) * r + 8 * jj;
+          const bool ok = sl >= 0 && 8 * jj < r;
+          v[pp][0] = ok ? ld_dev4(src) : make_float4(0.f, 0.f, 0.f, 0.f);
+          v[pp][1] = ok ? ld_dev4(src + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp) {
+          uq[0] = fmaf(wj[pp], v[pp][0].x, uq[0]);
+          uq[1] = fmaf(wj[pp], v[pp][0].y, uq[1]);
+          uq[2] = fmaf(wj[pp], v[pp][0].z, uq[2]);
+          uq[3] = fmaf(wj[pp], v[pp][0].w, uq[3]);
+          uq[4] = fmaf(wj[pp], v[pp][1].x, uq[4]);
+          uq[5] = fmaf(wj[pp], v[pp][1].y, uq[5]);
+          uq[6] = fmaf(wj[pp], v[pp][1].z, uq[6]);
+          uq[7] = fmaf(wj[pp], v[pp][1].w, uq[7]);
+        }
+      }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int q = 8 * jj + u;
-        float v = 0.0f;
-        if (q < r) {
-          for (int j = 0; j < k; ++j) {
-            const int sl = tok_slot[(t0 + t) * k + j];
-            if (sl < 0) continue;
-            float sv = 0.0f;
-            for (int ss = 0; ss < P.nsd; ++ss) sv += uap[((size_t)ss * S + sl) * r + q];
-            v = fmaf(slot_w[sl], sv, v);
-          }
-        }
-        h[u] = rne_bf16(v);
-        lw[u] = rne_bf16(v - bf(h[u]));
+        h[u] = rne_bf16(uq[u]);
+        lw[u] = rne_bf16(uq[u] - bf(h[u]));
       }
       us[t * ld + 2 * jj] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
                                        h[6] | (h[7] << 16));
@@ -808,7 +955,9 @@ __device__ void item_combine(const Plan& P, const Args& A, int jc, int nact, uin
                                            lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
     }
     __syncthreads();
+    trace_mark(0);
     bp.run(us, ld, 0, nt, acc);
+    trace_mark(1);
   }
   // VQ part and output: token rows 4g + i of this wave's 64 columns
   const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
@@ -818,23 +967,26 @@ __device__ void item_combine(const Plan& P, const Args& A, int jc, int nact, uin
     for (int i = 0; i < 4; ++i) {
       const int t = 4 * g + i;
       if (t >= nt) continue;
+      // sum_j a_j sum_s dn[s][slot_j][col..col+4): 8 (j, s) partials in flight
       float4 vq = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int j = 0; j < k; ++j) {
-        const int sl = tok_slot[(t0 + t) * k + j];
-        if (sl < 0) continue;
-        float4 sv = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int ss = 0; ss < P.nsd; ++ss) {
-          const float4 d = *reinterpret_cast<const float4*>(dn + ((size_t)ss * S + sl) * H + col);
-          sv.x += d.x;
-          sv.y += d.y;
-          sv.z += d.z;
-          sv.w += d.w;
+      const int npair = k * P.nsd;
+      for (int p0 = 0; p0 < npair; p0 += 8) {
+        float4 d[8];
+        float wj[8];
+#pragma unroll
+        for (int pp = 0; pp < 8; ++pp) {
+          const int pr = p0 + pp, j = pr / P.nsd, ss = pr % P.nsd;
+          const int sl = pr < npair ? tok_slot[(t0 + t) * k + j] : -1;
+          wj[pp] = sl >= 0 ? slot_w[sl] : 0.0f;
+          d[pp] = sl >= 0 ? ld_dev4(dn + ((size_t)ss * S + sl) * H + col) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        const float wj = slot_w[sl];
-        vq.x = fmaf(wj, sv.x, vq.x);
-        vq.y = fmaf(wj, sv.y, vq.y);
-        vq.z = fmaf(wj, sv.z, vq.z);
-        vq.w = fmaf(wj, sv.w, vq.w);
+#pragma unroll
+        for (int pp = 0; pp < 8; ++pp) {
+          vq.x = fmaf(wj[pp], d[pp].x, vq.x);
+          vq.y = fmaf(wj[pp], d[pp].y, vq.y);
+          vq.z = fmaf(wj[pp], d[pp].z, vq.z);
+          vq.w = fmaf(wj[pp], d[pp].w, vq.w);
+        }
       }
       *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) =
           make_float4(vq.x + acc[0][i], vq.y + acc[1][i], vq.z + acc[2][i], vq.w + acc[3][i]);
@@ -845,48 +997,45 @@ __device__ void item_combine(const Plan& P, const Args& A, int jc, int nact, uin
 // ===========================================================================
 // the two persistent kernels of a layer call
 // ===========================================================================
-// The last workgroup to leave a kernel clears that kernel's counters, so the
-// workspace is ready for the next call.
-__device__ __forceinline__ void exit_and_reset(const Args& A, int exit_ctr, const int* clear,
-                                               int n_clear, int* arr, int n_arr) {
-  __shared__ int s_last;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = (atomicAdd(ctr(A, exit_ctr), 1) == (int)gridDim.x - 1);
-  __syncthreads();
-  if (!s_last) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  if (threadIdx.x < n_clear) *ctr(A, clear[threadIdx.x]) = 0;
-  for (int e = threadIdx.x; e < n_arr; e += kWG) arr[e] = 0;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+// Each kernel clears the counters of the other kernel of the call before
+// any of them is used again (the stream orders the two kernels).
+__device__ __forceinline__ void clear_ints(int* p, int n) {
+  for (int i = threadIdx.x; i < n; i += kWG) p[i] = 0;
 }
 
 // Routing-independent work and the routing itself: router chunks, z units,
 // per-token select (the last one groups the slots), z reduce.
 __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  if (blockIdx.x == 0 && (P.flags & F_EXPERTS)) {
+    clear_ints(wsp<int>(A, P.o_gu_done), P.E);
+    clear_ints(wsp<int>(A, P.o_dn_done), P.E * (P.ncgh + P.ncgr));
+  }
   for (int j = blockIdx.x; j < P.n_pre; j += gridDim.x) {
     __syncthreads();
-    int jj = j;
+    ItemTrace tr;
+    int jj = j, kind = 0;
     if (jj < P.n_rc) {
-      item_router_chunk(P, A, jj % P.nch_r, jj / P.nch_r, smem);
-      continue;
-    }
-    jj -= P.n_rc;
-    if (jj < P.n_zc) {
+      item_router_chunk(P, A, jj, jj % P.nch_r, jj / P.nch_r, smem);
+    } else if ((jj -= P.n_rc) < P.n_zc) {
+      kind = 1;
       item_z(P, A, jj, smem);
-      continue;
-    }
-    jj -= P.n_zc;
-    if (jj < P.n_sel) {
+    } else if ((jj -= P.n_zc) < P.n_sel) {
+      kind = 2;
       item_select(P, A, jj, smem);
-      continue;
+    } else {
+      kind = 3;
+      item_z_reduce(P, A, jj - P.n_sel);
     }
-    jj -= P.n_sel;
-    item_z_reduce(P, A, jj);
+    tr.done(A, P, j, kind);
   }
-  const int clear[4] = {C_ROUTE_ARR, C_Z_ARR, C_SEL_ARR, C_EXIT_R};
-  exit_and_reset(A, C_EXIT_R, clear, 4, nullptr, 0);
+}
+
+// Clears the routing kernel's counters (after calls that run k_route alone).
+__global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
+  clear_ints(ctr(A, C_SEL_TICK), 1);
+  clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags);
+  clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags);
 }
 
 // Expert work of the active experts (count published by k_route): gate/up
@@ -899,39 +1048,53 @@ __global__ __launch_bounds__(kWG) void k_expert(Plan P, Args A) {
   const int tid = threadIdx.x;
   {
     // code word c of book b at cbs[b * 256 + c] (d = 8) or at the 8-byte
-    // slot b * 512 + c of the uint2 view (d = 4)
-    uint16_t* c16 = reinterpret_cast<uint16_t*>(cbs);
+    // slot b * 512 + c of the uint2 view (d = 4); one load per thread per
+    // book (code books are 16-byte aligned, K * d * 2 bytes long)
     const uint16_t* src[3] = {A.L.cb_gate, A.L.cb_up, A.L.cb_down};
-    for (int b = 0; b < 3; ++b)
-      for (int i = tid; i < 256 * D; i += kWG) {
-        const int word = i / D;
-        c16[b * 256 * 8 + i] = word < P.K ? src[b][i] : (uint16_t)0;
+    const int n16 = P.K * D * 2;  // bytes of a code book
+#pragma unroll
+    for (int b = 0; b < 3; ++b) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      const int byte0 = tid * 16;
+      if (byte0 + 16 <= n16) {
+        v = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(src[b]) + byte0);
+      } else if (byte0 < n16) {  // ragged end of the book
+        uint16_t e[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int u = 0; byte0 + 2 * u < n16; ++u) e[u] = src[b][byte0 / 2 + u];
+        v = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16));
       }
+      if (tid < 256 * D / 8) reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(cbs) + b * 256 * 8)[tid] = v;
+    }
+  }
+  if (blockIdx.x == 0) {
+    clear_ints(ctr(A, C_SEL_TICK), 1);
+    clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags);
+    clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags);
   }
   const int nact = *wsp<const int>(A, P.o_nact);
   const int tgu = gateup_tiles_per_expert(P), tdn = down_tiles_per_expert(P);
   const int n_items = nact * (tgu + tdn) + P.n_cb;
   for (int jp = blockIdx.x; jp < n_items; jp += gridDim.x) {
     __syncthreads();
-    int j = jp;
+    ItemTrace tr;
+    int j = jp, kind = 4;
     if (j < nact * tgu) {
       item_gateup<D>(P, A, j, cbs, smem);
-      continue;
-    }
-    j -= nact * tgu;
-    if (j < nact * tdn) {
+    } else if ((j -= nact * tgu) < nact * tdn) {
       const int a = j / tdn, rem = j % tdn, cgx = rem / P.nsd, s = rem % P.nsd;
-      if (cgx < P.ncgh)
+      if (cgx < P.ncgh) {
+        kind = 5;
         item_down_vq<D>(P, A, a, cgx, s, cbs, smem);
-      else
+      } else {
+        kind = 6;
         item_down_lr(P, A, a, cgx - P.ncgh, s, smem);
-      continue;
+      }
+    } else {
+      kind = 7;
+      item_combine(P, A, j - nact * tdn, nact, smem);
     }
-    j -= nact * tdn;
-    item_combine(P, A, j, nact, smem);
+    tr.done(A, P, P.n_pre + jp, kind);
   }
-  const int clear[2] = {C_DOWN_DONE, C_EXIT_E};
-  exit_and_reset(A, C_EXIT_E, clear, 2, wsp<int>(A, P.o_gu_done), P.E);
 }
 
 // x_next = bf16_rne(y / sqrt(mean(y^2) + eps)) per token.
@@ -963,6 +1126,11 @@ const void* expert_kernel(int d) {
 
 hipError_t launch_route(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st) {
   hipLaunchKernelGGL(k_route, dim3(grid), dim3(kWG), lds, st, P, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_route_reset(const Plan& P, const Args& A, hipStream_t st) {
+  hipLaunchKernelGGL(k_route_reset, dim3(1), dim3(kWG), 0, st, P, A);
   return hipGetLastError();
 }
 

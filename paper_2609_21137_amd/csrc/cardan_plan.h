@@ -39,8 +39,9 @@ constexpr int kMaxE = 1024, kMaxK = 32, kMaxR = 512, kMaxB = 64;
 // flags of one call
 enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8 };
 
-// counters at the start of the workspace, one per 64-byte slot
-enum { C_ERR = 0, C_ROUTE_ARR, C_Z_ARR, C_SEL_ARR, C_EXIT_R, C_DOWN_DONE, C_EXIT_E, C_NUM };
+// counters at the start of the workspace, one per 64-byte slot: the status
+// count of timed-out waits and the select ticket
+enum { C_ERR = 0, C_SEL_TICK, C_NUM };
 constexpr int kCtrStride = 16;      // ints between counters
 
 struct Plan {
@@ -62,9 +63,11 @@ struct Plan {
   int n_cb;       // combine tiles
   // item counts of this call
   int n_rc, n_zc, n_sel, n_zr, n_pre;
+  int n_rc_flags, n_zc_flags;  // flag slots (shape-wide maxima of n_rc, n_zc)
   // workspace byte offsets
-  size_t o_ctr, o_gu_tick, o_gu_done, o_rl, o_zp, o_z, o_off, o_act, o_nact, o_slot_tok, o_slot_w,
-      o_tok_slot, o_gu, o_p, o_dn, o_uap, total;
+  size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_tick, o_gu_done, o_dn_done;  // counters
+  size_t o_rl, o_zp, o_z, o_off, o_act, o_nact, o_slot_tok, o_slot_w, o_slot_e, o_tok_slot, o_gu, o_p,
+      o_dn, o_uap, total;
   size_t lds_route, lds_expert;  // dynamic LDS of the two kernels
 };
 
