@@ -38,6 +38,16 @@ def parse():
     ap.add_argument("--also", default="qwen3_30b_a3b_moe_layer_b16,wide_h4096_i1536_e64_top6_b4_skewed",
                     help="comma-separated extra workloads timed the same way (reported under 'also')")
     ap.add_argument("--layers", type=int, default=8, help="independently seeded layers rotated")
+    ap.add_argument("--inputs", type=int, default=64,
+                    help="distinct seeded inputs rotated (a multiple of --layers), so that the "
+                         "experts touched over a rotation exceed the 256 MB last-level cache")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV",
+                                                         "CAL_WRITE_CSV"),
+                    help="write profiles/k_expert_<workload>_pmc.json from rocprofv3 --pmc "
+                         "FETCH_SIZE / WRITE_SIZE counter CSVs of a bench run and of a "
+                         "--calibrate-copy-mb run, then exit")
+    ap.add_argument("--calibrate-copy-mb", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     return ap.parse_args()
@@ -86,7 +96,7 @@ def load_traffic(kernel: str, workload: str, src_hash: str):
     return rec.get("hbm_bytes_per_launch")
 
 
-def time_workload(C, torch, w, steps, warmup, n_layers, layers_cache):
+def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache):
     from paper_2609_21137_amd import synth
     shape = C.shape_of(w)
     key = (w.H, w.I, w.E, w.d, w.K, w.r, w.seed, w.hot_experts, w.hot_bias)
@@ -98,7 +108,9 @@ def time_workload(C, torch, w, steps, warmup, n_layers, layers_cache):
             dls.append(C.DeviceLayer.from_numpy(synth.workload_layer(w, li)))
         layers_cache[key] = dls
     dls = layers_cache[key]
-    xs = [C.bf16_tensor(synth.workload_input(w, li)) for li in range(n_layers)]
+    # input j always runs on layer j % n_layers
+    xs = [C.bf16_tensor(synth.workload_input(w, j % n_layers, step=j // n_layers))
+          for j in range(n_inputs)]
     ws = C.new_workspace(shape, w.B)
     y = torch.empty((w.B, w.H), dtype=torch.float32, device="cuda")
     idx = torch.empty((w.B, w.top_k), dtype=torch.int32, device="cuda")
@@ -107,22 +119,22 @@ def time_workload(C, torch, w, steps, warmup, n_layers, layers_cache):
 
     # routing (hence the active-expert count) is fixed per (layer, input)
     n_act = []
-    for li in range(n_layers):
-        C.moe_layer(shape, xs[li], dls[li], ws=ws, out=y, idx=idx, w=wt)
+    for j in range(n_inputs):
+        C.moe_layer(shape, xs[j], dls[j % n_layers], ws=ws, out=y, idx=idx, w=wt)
         torch.cuda.synchronize()
         n_act.append(len(np.unique(idx.cpu().numpy())))
 
     import ctypes
     lib = C.lib()
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    ptrs = [(ctypes.c_void_p(xs[li].data_ptr()), structs[li]) for li in range(n_layers)]
+    ptrs = [(ctypes.c_void_p(xs[j].data_ptr()), structs[j % n_layers]) for j in range(n_inputs)]
     args_tail = (ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(idx.data_ptr()),
                  ctypes.c_void_p(wt.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(), stream)
     fn = lib.cardan_moe_layer
     B = w.B
 
     def step(i):
-        xp, st = ptrs[i % n_layers]
+        xp, st = ptrs[i % n_inputs]
         rc = fn(ctypes.byref(shape), B, xp, ctypes.byref(st), *args_tail)
         if rc != 0:
             raise RuntimeError(lib.cardan_last_error().decode())
@@ -131,33 +143,33 @@ def time_workload(C, torch, w, steps, warmup, n_layers, layers_cache):
         step(i)
     torch.cuda.synchronize()
 
-    # timed region: exactly `steps` layer calls, bracketed by device syncs;
-    # HIP events around every kernel on the call's stream give kernel times
-    C.profile_begin(steps)
+    # timed region: exactly `steps` layer calls, bracketed by device syncs
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
         step(i)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    prof = C.profile_end()
 
-    # same loop without kernel events, for the event overhead
+    # the same steps again with HIP events around every kernel, recorded by
+    # the library on the stream the kernels run on: per-kernel durations
+    C.profile_begin(steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     for i in range(steps):
         step(i)
     torch.cuda.synchronize()
-    wall_clean = time.perf_counter() - t1
+    wall_events = time.perf_counter() - t1
+    prof = C.profile_end()
 
-    acts = [n_act[i % n_layers] for i in range(steps)]
+    acts = [n_act[i % n_inputs] for i in range(steps)]
     tot = {"compressed": 0, "expert_kernel": 0, "route_kernel": 0}
     for a in acts:
         b = compressed_bytes(w, a)
         for k in tot:
             tot[k] += b[k]
-    return {"wall_s": wall, "wall_clean_s": wall_clean, "prof": prof, "bytes": tot,
-            "mean_active": float(np.mean(acts)), "layers": n_layers}
+    return {"wall_s": wall, "wall_events_s": wall_events, "prof": prof, "bytes": tot,
+            "mean_active": float(np.mean(acts)), "layers": n_layers, "inputs": n_inputs}
 
 
 def cpu_baseline(w, budget_s):
@@ -194,9 +206,8 @@ def summarize(w, r, src_hash):
         "workload": w.name,
         "B": w.B,
         "us_per_layer": round(1e6 * r["wall_s"] / steps, 3),
-        "us_per_layer_no_kernel_events": round(1e6 * r["wall_clean_s"] / steps, 3),
+        "us_per_layer_with_kernel_events": round(1e6 * r["wall_events_s"] / steps, 3),
         "GBps": round(r["bytes"]["compressed"] / r["wall_s"] / 1e9, 2),
-        "GBps_no_kernel_events": round(r["bytes"]["compressed"] / r["wall_clean_s"] / 1e9, 2),
         "mean_active_experts": r["mean_active"],
         "kernel_us": {k: round(1e3 * v[0] / max(1, v[1]), 3) for k, v in prof.items() if v[1]},
         "roofline": {"kernel": "k_expert", "bound": "hbm", "achieved": round(achieved, 2),
@@ -206,8 +217,67 @@ def summarize(w, r, src_hash):
     }
 
 
+def calibrate_copy(torch, mib):
+    """A plain device-to-device copy of `mib` MiB, run 5 times: under
+    rocprofv3 --pmc its FETCH_SIZE / WRITE_SIZE per dispatch against the
+    known byte count gives the counter scale."""
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n * 4, "launches": 5}))
+
+
+def _pmc_means(path):
+    """Mean counter value (KiB) per kernel name of a rocprofv3 counter CSV."""
+    import csv
+    acc = {}
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            acc.setdefault(row["Kernel_Name"], []).append(float(row["Counter_Value"]))
+    return {k: (len(v), sum(v) / len(v)) for k, v in acc.items()}
+
+
+def summarize_pmc(args):
+    """HBM bytes per k_expert launch: FETCH_SIZE and WRITE_SIZE per dispatch,
+    each scaled by what the same counter reads for a plain copy of known size."""
+    fetch, write, cal_f, cal_w = (_pmc_means(p) for p in args.summarize_pmc)
+    copy = "__amd_rocclr_copyBuffer"
+    copy_bytes = args.calibrate_copy_mb * (1 << 20)
+    f_scale = copy_bytes / (cal_f[copy][1] * 1024)
+    w_scale = copy_bytes / (cal_w[copy][1] * 1024)
+    name = next(k for k in fetch if "k_expert" in k)
+    rec = {
+        "kernel": name, "workload": args.workload, "kernel_source_hash": kernel_source_hash(),
+        "dispatches": fetch[name][0],
+        "FETCH_SIZE_KiB_per_dispatch": round(fetch[name][1], 3),
+        "WRITE_SIZE_KiB_per_dispatch": round(write[name][1], 3),
+        "copy_calibration": {"copy_bytes": copy_bytes, "FETCH_SIZE_KiB": round(cal_f[copy][1], 3),
+                             "WRITE_SIZE_KiB": round(cal_w[copy][1], 3),
+                             "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)},
+        "hbm_read_bytes_per_launch": round(fetch[name][1] * 1024 * f_scale),
+        "hbm_write_bytes_per_launch": round(write[name][1] * 1024 * w_scale),
+    }
+    rec["hbm_bytes_per_launch"] = rec["hbm_read_bytes_per_launch"] + rec["hbm_write_bytes_per_launch"]
+    out = os.path.join(ROOT, "profiles", f"k_expert_{args.workload}_pmc.json")
+    with open(out, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps(rec))
+
+
 def main():
     args = parse()
+    if args.summarize_pmc:
+        if not args.calibrate_copy_mb:
+            print("--summarize-pmc needs --calibrate-copy-mb (the calibration copy size)",
+                  file=sys.stderr)
+            sys.exit(2)
+        summarize_pmc(args)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
@@ -219,18 +289,24 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.calibrate_copy_mb:
+        calibrate_copy(torch, args.calibrate_copy_mb)
+        return
+    if args.inputs % args.layers:
+        print("--inputs must be a multiple of --layers", file=sys.stderr)
+        sys.exit(2)
     src_hash = kernel_source_hash()
     w = WORKLOADS[args.workload]
     cache = {}
     print(f"[bench] {w.name}: synthesizing {args.layers} layers", file=sys.stderr, flush=True)
-    r = time_workload(C, torch, w, args.steps, args.warmup, args.layers, cache)
+    r = time_workload(C, torch, w, args.steps, args.warmup, args.layers, args.inputs, cache)
     main_sum = summarize(w, r, src_hash)
     print(f"[bench] {w.name}: {main_sum['us_per_layer']} us/layer", file=sys.stderr, flush=True)
     also = []
     for name in [s for s in args.also.split(",") if s]:
         ww = WORKLOADS[name]
         print(f"[bench] {ww.name}", file=sys.stderr, flush=True)
-        rr = time_workload(C, torch, ww, args.steps, args.warmup, args.layers, cache)
+        rr = time_workload(C, torch, ww, args.steps, args.warmup, args.layers, args.inputs, cache)
         also.append(summarize(ww, rr, src_hash))
         print(f"[bench] {ww.name}: {also[-1]['us_per_layer']} us/layer", file=sys.stderr,
               flush=True)
@@ -255,13 +331,13 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "H": w.H, "I": w.I, "E": w.E, "top_k": w.top_k, "d": w.d,
                    "K": w.K, "r": w.r, "B": w.B, "layers_rotated": args.layers,
+                   "inputs_rotated": args.inputs,
                    "parallelism": "none"},
         "us_per_layer": main_sum["us_per_layer"],
         "hbm_frac_of_peak": round(main_sum["GBps"] / HBM_PEAK_GBPS, 4),
         "kernel_us": main_sum["kernel_us"],
         "mean_active_experts": main_sum["mean_active_experts"],
-        "no_kernel_events": {"us_per_layer": main_sum["us_per_layer_no_kernel_events"],
-                             "GBps": main_sum["GBps_no_kernel_events"]},
+        "us_per_layer_with_kernel_events": main_sum["us_per_layer_with_kernel_events"],
         "roofline": main_sum["roofline"],
         "cpu_baseline": cpu,
         "also": also,
