@@ -68,7 +68,8 @@ int check_shape(const cardan_shape* s, int32_t B) {
   return CARDAN_OK;
 }
 
-constexpr size_t kLdsBudget = 32 * 1024;  // dynamic LDS limit of either kernel
+constexpr size_t kLdsBudget = 32 * 1024;  // operand staging target when sizing the K splits
+constexpr size_t kLdsMax = 64 * 1024;     // dynamic LDS limit of either kernel
 
 int ks_max(int total, int splits) { return ceil_div(total, splits); }
 
@@ -90,8 +91,8 @@ size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
 // Dynamic LDS of k_route for a plan.
 size_t lds_route(const Plan& P) {
   const int KSX = P.H / 32;
-  size_t need = (size_t)kTokPass * kRowsRouter * 4;                    // router chunk
-  need = std::max(need, (size_t)kMaxE * 8 + kMaxK * 4);                 // select
+  size_t need = (size_t)kTokPass * kRowsRouter * (4 + 4 * 8);          // router chunk
+  need = std::max(need, (size_t)kMaxE * (8 + 4) + kMaxK * (8 + 4));    // select
   need = std::max(need, (size_t)(kMaxB * kMaxK + 2 * kMaxE + 4) * 4);   // grouping
   if (P.flags & F_Z)
     need = std::max(need, (size_t)4 * kTokPass * (ks_max(KSX, P.nch_z) * 4 + 1) * 16);
@@ -102,8 +103,11 @@ size_t lds_route(const Plan& P) {
 size_t lds_expert(const Plan& P) {
   const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KSD = P.I / 32;
   size_t need = (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns) * 16;
-  need = std::max(need, (size_t)P.nt_max * (ks_max(KSD, P.nsd) * 8 + 1) * 16);
-  need = std::max(need, (size_t)P.tpc * (KSZ * 8 + 1) * 16);
+  // down: p operand rows + split_sum reduction (2 float4 per thread)
+  need = std::max(need, (size_t)P.nt_max * (ks_max(KSD, P.nsd) * 8 + 1) * 16 + kWG * 2 * 16);
+  // combine: routing of the tokens, reduction, B^T u rows, u operand rows
+  need = std::max(need, (size_t)3 * kTokPass * kMaxK * 4 + kWG * 16 + (size_t)kTokPass * kColsPerGroup * 4 +
+                            (size_t)P.tpc * (KSZ * 8 + 1) * 16);
   return round256(need);
 }
 
@@ -149,7 +153,6 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);
   P.o_rc_flag = o; o = align256(o + (size_t)P.n_rc_flags * 4);
   P.o_zc_flag = o; o = align256(o + (size_t)P.n_zc_flags * 4);
-  P.o_gu_tick = o; o = align256(o + (size_t)P.E * P.ncg * 4);
   P.o_gu_done = o; o = align256(o + (size_t)P.E * 4);
   P.o_dn_done = o; o = align256(o + (size_t)P.E * (P.ncgh + P.ncgr) * 4);
   P.o_rl = o; o = align256(o + (size_t)P.nch_r * B * P.E * 8);
@@ -163,7 +166,6 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.o_slot_e = o; o = align256(o + (size_t)P.S * 4);
   P.o_tok_slot = o; o = align256(o + (size_t)P.S * 4);
   P.o_gu = o; o = align256(o + (size_t)P.S * 2 * P.ns * P.I * 4);
-  P.o_p = o; o = align256(o + (size_t)P.S * P.I * 4);
   P.o_dn = o; o = align256(o + (size_t)P.nsd * P.S * P.H * 4);
   P.o_uap = o; o = align256(o + (size_t)P.nsd * P.S * P.r * 4);
   P.total = o;
@@ -273,9 +275,9 @@ int hip_fail(hipError_t e, const char* what) {
 // Sizes the grids and launches k_route (if the call has routing items) and
 // k_expert (if it has expert work) for one call.
 int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
-  if (P.lds_route > kLdsBudget || P.lds_expert > kLdsBudget)
+  if (P.lds_route > kLdsMax || P.lds_expert > kLdsMax)
     return fail(CARDAN_ERR_UNSUPPORTED, "shape needs %zu/%zu bytes of LDS (> %zu)", P.lds_route,
-                P.lds_expert, kLdsBudget);
+                P.lds_expert, kLdsMax);
   hipError_t err;
   if (P.n_pre > 0) {
     const int cap = resident_grid(route_kernel(), P.lds_route, &err);

@@ -224,52 +224,64 @@ __device__ int block_exclusive_scan(int* arr, int n, int* tmp4) {
 }
 
 // Router chunk (c, g): partial logits over hidden rows [64c, 64c + 64) for
-// experts [64g, 64g + 64). Wave w owns experts 64g + 16w + (lane & 15); the
-// four lane groups (lane >> 4) own rows h = 4i + (lane >> 4). float64
-// accumulation of exact bf16 products; the four row groups are combined with
-// a fixed shuffle tree.
+// experts [64g, 64g + 64). Lane l of wave w owns expert 64g + l and rows
+// 64c + 16w .. + 16; float64 FMAs of exact bf16 products, four independent
+// chains per token, then the four waves' partials are added in wave order
+// through LDS.
 __device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c, int g, uint8_t* smem) {
-  float* xs = reinterpret_cast<float*>(smem);  // [16][64] (bf16 values are exact in f32)
+  float* xs = reinterpret_cast<float*>(smem);                          // [16][64]
+  double* part = reinterpret_cast<double*>(smem + kTokPass * kRowsRouter * 4);  // [4][16][64]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int E = P.E, H = P.H, B = P.B, h0 = c * kRowsRouter;
-  const int e = g * 64 + w * 16 + (lane & 15), rq = lane >> 4;
-  const bool ev = e < E;
-  const uint16_t* Wr = A.L.router_w;
+  const int e = min(g * 64 + lane, E - 1);  // lanes past E compute a copy that is never stored
+  const uint16_t* Wr = A.L.router_w + (size_t)(h0 + 16 * w) * E + e;
   uint32_t wv[16];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) wv[i] = ev ? Wr[(size_t)(h0 + rq + 4 * i) * E + e] : 0u;
+  for (int i = 0; i < 16; ++i) wv[i] = Wr[(size_t)i * E];
   double* rl = wsp<double>(A, P.o_rl);
   for (int tg = 0; tg < B; tg += kTokPass) {
     const int nt = min(kTokPass, B - tg);
-    for (int i = tid; i < kTokPass * kRowsRouter; i += kWG) {
+    for (int i = tid; i < nt * kRowsRouter; i += kWG) {
       const int t = i / kRowsRouter, h = i % kRowsRouter;
-      xs[i] = t < nt ? bf(A.x[(size_t)(tg + t) * H + h0 + h]) : 0.0f;
+      xs[i] = bf(A.x[(size_t)(tg + t) * H + h0 + h]);
     }
     __syncthreads();
     trace_mark(0);
-    double acc[kTokPass];
+    double wd[16];
 #pragma unroll
-    for (int t = 0; t < kTokPass; ++t) acc[t] = 0.0;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const double wd = (double)bf(wv[i]);
-      const int h = rq + 4 * i;
-#pragma unroll
-      for (int t = 0; t < kTokPass; ++t)
-        if (t < nt) acc[t] = fma(wd, (double)xs[t * kRowsRouter + h], acc[t]);
+    for (int i = 0; i < 16; ++i) wd[i] = (double)bf(wv[i]);
+    for (int t = 0; t < nt; ++t) {
+      // the wave's 16 inputs of token t: the same LDS words for every lane
+      const float4* xr = reinterpret_cast<const float4*>(xs + t * kRowsRouter + 16 * w);
+      const float4 x0 = xr[0], x1 = xr[1], x2 = xr[2], x3 = xr[3];
+      double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+      a0 = fma(wd[0], (double)x0.x, a0);
+      a1 = fma(wd[1], (double)x0.y, a1);
+      a2 = fma(wd[2], (double)x0.z, a2);
+      a3 = fma(wd[3], (double)x0.w, a3);
+      a0 = fma(wd[4], (double)x1.x, a0);
+      a1 = fma(wd[5], (double)x1.y, a1);
+      a2 = fma(wd[6], (double)x1.z, a2);
+      a3 = fma(wd[7], (double)x1.w, a3);
+      a0 = fma(wd[8], (double)x2.x, a0);
+      a1 = fma(wd[9], (double)x2.y, a1);
+      a2 = fma(wd[10], (double)x2.z, a2);
+      a3 = fma(wd[11], (double)x2.w, a3);
+      a0 = fma(wd[12], (double)x3.x, a0);
+      a1 = fma(wd[13], (double)x3.y, a1);
+      a2 = fma(wd[14], (double)x3.z, a2);
+      a3 = fma(wd[15], (double)x3.w, a3);
+      part[(w * kTokPass + t) * 64 + lane] = (a0 + a1) + (a2 + a3);
     }
-#pragma unroll
-    for (int t = 0; t < kTokPass; ++t) {
-      if (t < nt) {
-        acc[t] += __shfl_xor(acc[t], 16);
-        acc[t] += __shfl_xor(acc[t], 32);
-      }
-    }
+    __syncthreads();
     trace_mark(1);
-    if (rq == 0 && ev) {
-#pragma unroll
-      for (int t = 0; t < kTokPass; ++t)
-        if (t < nt) st_dev(rl + ((size_t)c * B + tg + t) * E + e, acc[t]);
+    for (int i = tid; i < nt * 64; i += kWG) {
+      const int t = i >> 6, el = i & 63;
+      if (g * 64 + el < E) {
+        const double v = (part[(0 * kTokPass + t) * 64 + el] + part[(1 * kTokPass + t) * 64 + el]) +
+                         (part[(2 * kTokPass + t) * 64 + el] + part[(3 * kTokPass + t) * 64 + el]);
+        st_dev(rl + ((size_t)c * B + tg + t) * E + g * 64 + el, v);
+      }
     }
     __syncthreads();
   }
@@ -339,11 +351,13 @@ __device__ void group_slots(const Plan& P, const Args& A, const int32_t* __restr
 // only groups.
 __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) {
   __shared__ int s_last;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x;
   const int E = P.E, k = P.k, B = P.B;
   if (P.flags & F_ROUTE) {
     double* lg = reinterpret_cast<double*>(smem);          // [E]
-    int* sel = reinterpret_cast<int*>(lg + kMaxE);          // [k]
+    double* ex = lg + kMaxE;                                // [k]
+    int* sel = reinterpret_cast<int*>(ex + kMaxK);          // [k]
+    int* rank = sel + kMaxK;                                // [E]
     const int* rcf = wsp<const int>(A, P.o_rc_flag);
     wait_all(A, P.n_rc, [&](int i) { return ld_dev(rcf + i) != 0; });
     const double* rl = wsp<const double>(A, P.o_rl);
@@ -360,43 +374,44 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
       if (A.L.router_bias) s += (double)A.L.router_bias[e];
       lg[e] = s;
     }
+    if (tid < kMaxK) sel[tid] = -1;
+    for (int e = tid; e < E; e += kWG) rank[e] = 0;
     __syncthreads();
     trace_mark(0);
-    if (w == 0) {
-      for (int j = 0; j < k; ++j) {
-        double bv = -INFINITY;
-        int be = 0x7fffffff;
-        for (int e = lane; e < E; e += 64) {
-          bool taken = false;
-          for (int jj = 0; jj < j; ++jj) taken |= (sel[jj] == e);
-          if (!taken) {
-            const double v = lg[e];
-            if (v > bv || (v == bv && e < be)) {
-              bv = v;
-              be = e;
-            }
-          }
+    // rank of expert e = number of experts before it under (descending logit,
+    // ascending index); the experts of rank < k are the selection, in order.
+    // The comparisons of one expert are split over `parts` thread groups.
+    {
+      const int parts = max(1, kWG / E);
+      const int per = (E + parts - 1) / parts;
+      for (int i = tid; i < parts * E; i += kWG) {
+        const int e = i % E, pt = i / E;
+        const double v = lg[e];
+        const int f1 = min(E, (pt + 1) * per);
+        int rk = 0;
+        for (int f = pt * per; f < f1; ++f) {
+          const double u = lg[f];
+          rk += (u > v) || (u == v && f < e);
         }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          const double ov = __shfl_xor(bv, o);
-          const int oe = __shfl_xor(be, o);
-          if (ov > bv || (ov == bv && oe < be)) {
-            bv = ov;
-            be = oe;
-          }
-        }
-        sel[j] = be;  // the same value in every lane
+        atomicAdd(&rank[e], rk);
       }
-      const double mx = lg[sel[0]];
-      const double ex = lane < k ? exp(lg[sel[lane]] - mx) : 0.0;
-      double sum = ex;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
-      if (lane < k) {
-        st_dev(A.topk_idx + t * k + lane, sel[lane]);
-        st_dev(A.topk_w + t * k + lane, (float)(ex / sum));
-      }
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += kWG)
+      if (rank[e] < k) sel[rank[e]] = e;
+    __syncthreads();
+    // softmax over the k selected logits, summed in selection order
+    if (tid < k) {
+      const int e = sel[tid];
+      const double mx = sel[0] >= 0 ? lg[sel[0]] : 0.0;
+      ex[tid] = e >= 0 ? exp(lg[e] - mx) : 0.0;
+    }
+    __syncthreads();
+    if (tid < k) {
+      double sum = 0.0;
+      for (int j = 0; j < k; ++j) sum += ex[j];
+      st_dev(A.topk_idx + t * k + tid, sel[tid]);
+      st_dev(A.topk_w + t * k + tid, (float)(ex[tid] / sum));
     }
     if (!(P.flags & F_GROUP)) return;
     trace_mark(1);
@@ -656,6 +671,83 @@ __device__ __forceinline__ void stage_split(uint4* ops, int ld, int nt, int n8, 
   }
 }
 
+// Writes 4 consecutive fp32 values as bf16 hi/lo halves of an LDS operand
+// row laid out as stage_split does: quad q of a row is half (q & 1) of the
+// uint4 pair at [2 (q >> 1)] (hi) and [2 (q >> 1) + 1] (lo).
+__device__ __forceinline__ void put_split_quad(uint4* row, int q, float4 v) {
+  const float f[4] = {v.x, v.y, v.z, v.w};
+  uint32_t h[4], lw[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    h[u] = rne_bf16(f[u]);
+    lw[u] = rne_bf16(f[u] - bf(h[u]));
+  }
+  uint2* hi = reinterpret_cast<uint2*>(row + 2 * (q >> 1)) + (q & 1);
+  uint2* lo = reinterpret_cast<uint2*>(row + 2 * (q >> 1) + 1) + (q & 1);
+  *hi = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+  *lo = make_uint2(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16));
+}
+
+__device__ __forceinline__ float4 fma4(float w, float4 v, float4 a) {
+  return make_float4(fmaf(w, v.x, a.x), fmaf(w, v.y, a.y), fmaf(w, v.z, a.z), fmaf(w, v.w, a.w));
+}
+
+// Sums of many partials with every load in flight at once. For each of
+// `items` outputs (NV float4 values each) it adds `npair` weighted terms:
+// the workgroup is split into G groups (G * items <= 256 threads) that take
+// every G-th term, BATCH terms' loads issued together; the group partials
+// meet in LDS (`red`, G * items * NV float4) and are added in group order,
+// so the result is deterministic. load(item, p, v, w) fills term p (p < 0:
+// no term, return zeros); done(item, sum) receives the result. All threads of
+// the workgroup must call it.
+template <int NV, int BATCH, typename Load, typename Done>
+__device__ __forceinline__ void split_sum(int items, int npair, float4* red, Load load, Done done) {
+  const int tid = threadIdx.x;
+  const int G = items >= kWG ? 1 : min(16, kWG / items);
+  for (int base = 0; base < items * G; base += kWG) {
+    const int idx = base + tid;
+    const int item = idx % items, g = idx / items;
+    float4 acc[NV];
+#pragma unroll
+    for (int u = 0; u < NV; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (idx < items * G) {
+      for (int p0 = g; p0 < npair; p0 += G * BATCH) {
+        float4 v[BATCH][NV];
+        float wt[BATCH];
+#pragma unroll
+        for (int b = 0; b < BATCH; ++b) {
+          const int p = p0 + b * G;
+          load(item, p < npair ? p : -1, v[b], wt[b]);
+        }
+#pragma unroll
+        for (int b = 0; b < BATCH; ++b)
+#pragma unroll
+          for (int u = 0; u < NV; ++u) acc[u] = fma4(wt[b], v[b][u], acc[u]);
+      }
+    }
+    if (G == 1) {
+      if (idx < items) done(item, acc);
+    } else {
+#pragma unroll
+      for (int u = 0; u < NV; ++u) red[(g * items + item) * NV + u] = acc[u];
+      __syncthreads();
+      if (tid < items) {
+        float4 sum[NV];
+#pragma unroll
+        for (int u = 0; u < NV; ++u) sum[u] = red[tid * NV + u];
+        for (int gg = 1; gg < G; ++gg)
+#pragma unroll
+          for (int u = 0; u < NV; ++u) {
+            const float4 q = red[(gg * items + tid) * NV + u];
+            sum[u] = make_float4(sum[u].x + q.x, sum[u].y + q.y, sum[u].z + q.z, sum[u].w + q.w);
+          }
+        done(tid, sum);
+      }
+      __syncthreads();
+    }
+  }
+}
+
 // ===========================================================================
 // shared projections on MFMA
 // ===========================================================================
@@ -713,11 +805,10 @@ __device__ __forceinline__ Routing expert_of(const Plan& P, const Args& A, int a
 
 // Gate/up tile (a, pj, cg, s): 256 output columns of projection pj over
 // split s of the joint reduction axis [x (H inputs) | z (r ranks)], i.e. the
-// VQ gather sum and V^T z accumulate in the same MFMA accumulators. The last
-// of the 2 ns tiles of (a, cg) applies p = silu(g) * u.
+// VQ gather sum and V^T z accumulate in the same MFMA accumulators. Each
+// tile writes its partial sums and counts itself done for its expert.
 template <int D>
 __device__ void item_gateup(const Plan& P, const Args& A, int jt, const uint4* cbs, uint8_t* smem) {
-  __shared__ int s_last;
   const int s = jt % P.ns;
   jt /= P.ns;
   const int cg = jt % P.ncg;
@@ -782,34 +873,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, int jt, const uint4* c
     trace_mark(2);
   }
 
-  int* tick = wsp<int>(A, P.o_gu_tick) + a * P.ncg + cg;
-  const bool last = last_of(tick, 2 * P.ns, &s_last);
   trace_mark(3);
-  if (!last) return;
-  // the last tile of (a, cg): p = silu(sum of gate splits) * (sum of up splits)
-  const int cc = cg * kColsPerGroup + threadIdx.x;
-  float* pbuf = wsp<float>(A, P.o_p);
-  if (cc < I) {
-    for (int t = 0; t < R.ne; ++t) {
-      const float* src = gu + (size_t)(R.s0 + t) * 2 * P.ns * I + cc;
-      float gs = 0.0f, us = 0.0f;
-      for (int j0 = 0; j0 < P.ns; j0 += 16) {
-        float vg[16], vu[16];
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          vg[j] = (j0 + j < P.ns) ? ld_dev(src + (size_t)(j0 + j) * I) : 0.0f;
-          vu[j] = (j0 + j < P.ns) ? ld_dev(src + (size_t)(P.ns + j0 + j) * I) : 0.0f;
-        }
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          gs += vg[j];
-          us += vu[j];
-        }
-      }
-      st_dev(pbuf + (size_t)(R.s0 + t) * I + cc, gs / (1.0f + expf(-gs)) * us);
-    }
-  }
-  if (threadIdx.x == 0) *tick = 0;
   publish(wsp<int>(A, P.o_gu_done) + R.e);
 }
 
@@ -822,18 +886,42 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
                                           int cgx, int ks0, int ks1, int c0, int n_out, Pipe& pipe, Prime prime,
                                           Run run, Dst dst, uint8_t* smem) {
   prime();
-  wait_geq(A, wsp<int>(A, P.o_gu_done) + R.e, P.ncg);
-  const int I = P.I;
+  wait_geq(A, wsp<int>(A, P.o_gu_done) + R.e, gateup_tiles_per_expert(P));
+  const int I = P.I, ns = P.ns;
   const int ld = (ks1 - ks0) * 8 + 1;
+  const int nq = (ks1 - ks0) * 8;  // quads of inputs of this split
   uint4* ps = reinterpret_cast<uint4*>(smem);
-  const float* pbuf = wsp<const float>(A, P.o_p);
+  float4* red = reinterpret_cast<float4*>(ps + P.nt_max * ld);
+  const float* gu = wsp<const float>(A, P.o_gu);
   for (int tg = 0; tg < R.ne; tg += kTokPass) {
     const int nt = min(kTokPass, R.ne - tg);
     if (tg > 0) prime();
     __syncthreads();
-    stage_split(ps, ld, nt, (ks1 - ks0) * 4,
-                [&](int t) { return pbuf + (size_t)(R.s0 + tg + t) * I + ks0 * 32; });
+    // p = silu(sum of the gate splits) * (sum of the up splits) for inputs
+    // [32 ks0, 32 ks1) of the tokens, staged as bf16 hi/lo
+    split_sum<2, 4>(
+        nt * nq, ns, red,
+        [&](int item, int sp, float4(&v)[2], float& wt) {
+          const int t = item / nq, q = item % nq;
+          if (sp < 0) {
+            v[0] = v[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+            wt = 0.f;
+            return;
+          }
+          const float* src = gu + ((size_t)(R.s0 + tg + t) * 2 * ns + sp) * I + ks0 * 32 + 4 * q;
+          v[0] = ld_dev4(src);
+          v[1] = ld_dev4(src + (size_t)ns * I);
+          wt = 1.f;
+        },
+        [&](int item, const float4(&gsum)[2]) {
+          const int t = item / nq, q = item % nq;
+          const float4 g = gsum[0], u = gsum[1];
+          const float4 pv = make_float4(g.x / (1.0f + expf(-g.x)) * u.x, g.y / (1.0f + expf(-g.y)) * u.y,
+                                        g.z / (1.0f + expf(-g.z)) * u.z, g.w / (1.0f + expf(-g.w)) * u.w);
+          put_split_quad(ps + t * ld, q, pv);
+        });
     __syncthreads();
+    trace_mark(0);
     f32x4 acc[4];
     zero_acc(acc);
     run(ps, ld, nt, acc);
@@ -877,121 +965,113 @@ __device__ void item_down_lr(const Plan& P, const Args& A, int a, int cgr, int s
 // Combine tile (cgy, tq): output columns [256 cgy, +256) of tokens
 // [tpc tq, tpc tq + tpc): y[t] = sum_j a_j sum_s dn[s][slot_j] + B^T u[t]
 // with u[t] = sum_j a_j sum_s uap[s][slot_j]. B rows are loaded before the
-// wait; B^T u runs on MFMA with u as bf16 hi/lo.
-__device__ void item_combine(const Plan& P, const Args& A, int jc, int nact, uint8_t* smem) {
+// wait; B^T u runs on MFMA with u as bf16 hi/lo. The routing of the tile's
+// tokens is read once into LDS; every partial sum keeps all its loads in
+// flight (split_sum).
+__device__ void item_combine(const Plan& P, const Args& A, int jc, uint8_t* smem) {
   const int cgy = jc % P.ncgh, tq = jc / P.ncgh;
-  const int H = P.H, r = P.r, k = P.k, S = P.S;
+  const int H = P.H, r = P.r, k = P.k, S = P.S, nsd = P.nsd;
   const int t0 = tq * P.tpc, nt = min(P.tpc, P.B - t0);
-  const int w = threadIdx.x >> 6;
-  const int c0 = cgy * kColsPerGroup + w * 64;
+  const int tid = threadIdx.x, w = tid >> 6;
+  const int cbase = cgy * kColsPerGroup;
   const int KSR = (r + 31) / 32;
   DensePipe<2, kPdDense> bp;
-  if (r > 0) bp.prime(A.L.B_down, H, c0, H, r, 0, KSR);
+  if (r > 0) bp.prime(A.L.B_down, H, cbase + w * 64, H, r, 0, KSR);
 
-  const float* slot_w = wsp<const float>(A, P.o_slot_w);
-  const int* tok_slot = wsp<const int>(A, P.o_tok_slot);
+  int* s_slot = reinterpret_cast<int*>(smem);      // [nt * k]
+  float* s_w = reinterpret_cast<float*>(s_slot + kTokPass * kMaxK);
+  int* s_e = reinterpret_cast<int*>(s_w + kTokPass * kMaxK);
+  float4* red = reinterpret_cast<float4*>(s_e + kTokPass * kMaxK);  // [256]
+  float* bt = reinterpret_cast<float*>(red + kWG);                  // [nt][256] B^T u
+  uint4* us = reinterpret_cast<uint4*>(bt + kTokPass * kColsPerGroup);
+  const int ntk = nt * k;
+  {
+    const int* tok_slot = wsp<const int>(A, P.o_tok_slot) + t0 * k;
+    const float* slot_w = wsp<const float>(A, P.o_slot_w);
+    const int* slot_e = wsp<const int>(A, P.o_slot_e);
+    for (int i = tid; i < ntk; i += kWG) {
+      const int sl = tok_slot[i];
+      s_slot[i] = sl;
+      s_w[i] = sl >= 0 ? slot_w[sl] : 0.0f;
+      s_e[i] = sl >= 0 ? slot_e[sl] : 0;
+    }
+  }
+  __syncthreads();
   {
     // every down tile of this column group (and of the low-rank columns) of
     // every expert of these tokens
-    const int* slot_e = wsp<const int>(A, P.o_slot_e);
     const int* dnd = wsp<const int>(A, P.o_dn_done);
     const int ncol = 1 + P.ncgr, per_e = P.ncgh + P.ncgr;
-    wait_all(A, nt * k * ncol, [&](int i) {
+    wait_all(A, ntk * ncol, [&](int i) {
       const int c = i % ncol, tj = i / ncol;
-      const int sl = tok_slot[t0 * k + tj];
-      if (sl < 0) return true;
+      if (s_slot[tj] < 0) return true;
       const int cgx = c == 0 ? cgy : P.ncgh + c - 1;
-      return ld_dev(dnd + slot_e[sl] * per_e + cgx) >= P.nsd;
+      return ld_dev(dnd + s_e[tj] * per_e + cgx) >= nsd;
     });
   }
-  (void)nact;
-  const float* dn = wsp<const float>(A, P.o_dn);
-  const float* uap = wsp<const float>(A, P.o_uap);
-  f32x4 acc[4];
-  zero_acc(acc);
+  const int npair = k * nsd;  // (j, s) partials per output
   if (r > 0) {
-    const int ld = KSR * 8 + 1;
-    uint4* us = reinterpret_cast<uint4*>(smem);
-    for (int i = threadIdx.x; i < nt * KSR * 4; i += kWG) {
-      const int t = i / (KSR * 4), jj = i % (KSR * 4);
-      uint32_t h[8], lw[8];
-      // u[t][8 jj .. 8 jj + 8) = sum_j a_j sum_s uap[s][slot_j][q]: all (j, s)
-      // partials of 8 ranks in flight at once
-      float uq[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      const int npair = k * P.nsd;
-      for (int p0 = 0; p0 < npair; p0 += 4) {
-        float4 v[4][2];
-        float wj[4];
-#pragma unroll
-        for (int pp = 0; pp < 4; ++pp) {
-          const int pr = p0 + pp, j = pr / P.nsd, ss = pr % P.nsd;
-          const int sl = pr < npair ? tok_slot[(t0 + t) * k + j] : -1;
-          wj[pp] = sl >= 0 ? slot_w[sl] : 0.0f;
-          const float* src = uap + ((size_t)ss * S + (sl >= 0 ? sl : 0)) * r + 8 * jj;
-          const bool ok = sl >= 0 && 8 * jj < r;
-          v[pp][0] = ok ? ld_dev4(src) : make_float4(0.f, 0.f, 0.f, 0.f);
-          v[pp][1] = ok ? ld_dev4(src + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-#pragma unroll
-        for (int pp = 0; pp < 4; ++pp) {
-          uq[0] = fmaf(wj[pp], v[pp][0].x, uq[0]);
-          uq[1] = fmaf(wj[pp], v[pp][0].y, uq[1]);
-          uq[2] = fmaf(wj[pp], v[pp][0].z, uq[2]);
-          uq[3] = fmaf(wj[pp], v[pp][0].w, uq[3]);
-          uq[4] = fmaf(wj[pp], v[pp][1].x, uq[4]);
-          uq[5] = fmaf(wj[pp], v[pp][1].y, uq[5]);
-          uq[6] = fmaf(wj[pp], v[pp][1].z, uq[6]);
-          uq[7] = fmaf(wj[pp], v[pp][1].w, uq[7]);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        h[u] = rne_bf16(uq[u]);
-        lw[u] = rne_bf16(uq[u] - bf(h[u]));
-      }
-      us[t * ld + 2 * jj] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                                       h[6] | (h[7] << 16));
-      us[t * ld + 2 * jj + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
-                                           lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
-    }
+    // u[t] in quads of ranks (zero past r), staged as bf16 hi/lo
+    const float* uap = wsp<const float>(A, P.o_uap);
+    const int nq = KSR * 8, ld = KSR * 8 + 1;
+    split_sum<1, 8>(
+        nt * nq, npair, red,
+        [&](int item, int p, float4(&v)[1], float& wt) {
+          const int t = item / nq, q = item % nq;
+          const int j = p / nsd, ss = p % nsd;
+          const int sl = p >= 0 ? s_slot[t * k + j] : -1;
+          if (sl < 0 || 4 * q >= r) {
+            v[0] = make_float4(0.f, 0.f, 0.f, 0.f);
+            wt = 0.f;
+            return;
+          }
+          v[0] = ld_dev4(uap + ((size_t)ss * S + sl) * r + 4 * q);
+          wt = s_w[t * k + j];
+        },
+        [&](int item, const float4(&u)[1]) { put_split_quad(us + (item / nq) * ld, item % nq, u[0]); });
     __syncthreads();
     trace_mark(0);
+    f32x4 acc[4];
+    zero_acc(acc);
     bp.run(us, ld, 0, nt, acc);
-    trace_mark(1);
-  }
-  // VQ part and output: token rows 4g + i of this wave's 64 columns
-  const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
-  const int col = c0 + 4 * n;
-  if (col < H) {
+    // B^T u into LDS: token rows 4g + i, columns 64 w + 4 n + q
+    const int l = tid & 63, n = l & 15, g = l >> 4;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = 4 * g + i;
-      if (t >= nt) continue;
-      // sum_j a_j sum_s dn[s][slot_j][col..col+4): 8 (j, s) partials in flight
-      float4 vq = make_float4(0.f, 0.f, 0.f, 0.f);
-      const int npair = k * P.nsd;
-      for (int p0 = 0; p0 < npair; p0 += 8) {
-        float4 d[8];
-        float wj[8];
-#pragma unroll
-        for (int pp = 0; pp < 8; ++pp) {
-          const int pr = p0 + pp, j = pr / P.nsd, ss = pr % P.nsd;
-          const int sl = pr < npair ? tok_slot[(t0 + t) * k + j] : -1;
-          wj[pp] = sl >= 0 ? slot_w[sl] : 0.0f;
-          d[pp] = sl >= 0 ? ld_dev4(dn + ((size_t)ss * S + sl) * H + col) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-#pragma unroll
-        for (int pp = 0; pp < 8; ++pp) {
-          vq.x = fmaf(wj[pp], d[pp].x, vq.x);
-          vq.y = fmaf(wj[pp], d[pp].y, vq.y);
-          vq.z = fmaf(wj[pp], d[pp].z, vq.z);
-          vq.w = fmaf(wj[pp], d[pp].w, vq.w);
-        }
-      }
-      *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) =
-          make_float4(vq.x + acc[0][i], vq.y + acc[1][i], vq.z + acc[2][i], vq.w + acc[3][i]);
+      if (t < nt)
+        *reinterpret_cast<float4*>(bt + t * kColsPerGroup + w * 64 + 4 * n) =
+            make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
     }
+    __syncthreads();
+    trace_mark(1);
   }
+  // VQ part and output, one float4 of 4 columns per item
+  const float* dn = wsp<const float>(A, P.o_dn);
+  split_sum<1, 8>(
+      nt * 64, npair, red,
+      [&](int item, int p, float4(&v)[1], float& wt) {
+        const int t = item >> 6, col = cbase + 4 * (item & 63);
+        const int j = p / nsd, ss = p % nsd;
+        const int sl = p >= 0 ? s_slot[t * k + j] : -1;
+        if (sl < 0 || col >= H) {
+          v[0] = make_float4(0.f, 0.f, 0.f, 0.f);
+          wt = 0.f;
+          return;
+        }
+        v[0] = ld_dev4(dn + ((size_t)ss * S + sl) * H + col);
+        wt = s_w[t * k + j];
+      },
+      [&](int item, const float4(&q)[1]) {
+        const int t = item >> 6, c4 = item & 63, col = cbase + 4 * c4;
+        if (col >= H) return;
+        float4 o = q[0];
+        if (r > 0) {
+          const float4 b = *reinterpret_cast<const float4*>(bt + t * kColsPerGroup + 4 * c4);
+          o = make_float4(o.x + b.x, o.y + b.y, o.z + b.z, o.w + b.w);
+        }
+        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) = o;
+      });
 }
 
 // ===========================================================================
@@ -1042,7 +1122,7 @@ __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
 // tiles, down tiles (waiting per expert for p), combine tiles (waiting for
 // every down tile).
 template <int D>
-__global__ __launch_bounds__(kWG) void k_expert(Plan P, Args A) {
+__global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ uint4 cbs[3 * 256];  // gate, up, down code books (zero-padded to 256 words)
   const int tid = threadIdx.x;
@@ -1091,7 +1171,7 @@ __global__ __launch_bounds__(kWG) void k_expert(Plan P, Args A) {
       }
     } else {
       kind = 7;
-      item_combine(P, A, j - nact * tdn, nact, smem);
+      item_combine(P, A, j - nact * tdn, smem);
     }
     tr.done(A, P, P.n_pre + jp, kind);
   }

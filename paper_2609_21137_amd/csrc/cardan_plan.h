@@ -65,8 +65,8 @@ struct Plan {
   int n_rc, n_zc, n_sel, n_zr, n_pre;
   int n_rc_flags, n_zc_flags;  // flag slots (shape-wide maxima of n_rc, n_zc)
   // workspace byte offsets
-  size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_tick, o_gu_done, o_dn_done;  // counters
-  size_t o_rl, o_zp, o_z, o_off, o_act, o_nact, o_slot_tok, o_slot_w, o_slot_e, o_tok_slot, o_gu, o_p,
+  size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_done, o_dn_done;  // counters
+  size_t o_rl, o_zp, o_z, o_off, o_act, o_nact, o_slot_tok, o_slot_w, o_slot_e, o_tok_slot, o_gu,
       o_dn, o_uap, total;
   size_t lds_route, lds_expert;  // dynamic LDS of the two kernels
 };
