@@ -68,17 +68,17 @@ int check_shape(const cardan_shape* s, int32_t B) {
   return CARDAN_OK;
 }
 
-constexpr size_t kLdsBudget = 32 * 1024;  // operand staging target when sizing the K splits
-constexpr size_t kLdsMax = 64 * 1024;     // dynamic LDS limit of either kernel
+constexpr size_t kLdsBudget = 60 * 1024;  // operand staging limit when sizing the K splits
+constexpr size_t kLdsMax = 96 * 1024;     // dynamic LDS limit of either kernel
 
 int ks_max(int total, int splits) { return ceil_div(total, splits); }
 
 // Largest x/z staging of a gate/up split (uint4 per token row).
-int gateup_ld(int KSX, int KSZ, int ns) {
+int gateup_ld(int KSX, int KSZ, int d, int ns) {
   int best = 0;
-  const int KS = KSX + KSZ;
   for (int s = 0; s < ns; ++s) {
-    const int k0 = s * KS / ns, k1 = (s + 1) * KS / ns;
+    int k0, k1;
+    joint_split(s, ns, KSX, KSZ, d, k0, k1);
     const int x = std::min(k1, KSX) - std::min(k0, KSX);
     const int z = std::max(k1, KSX) - std::max(k0, KSX);
     best = std::max(best, (x * 4 + 1) + (z * 8 + 1));
@@ -102,9 +102,10 @@ size_t lds_route(const Plan& P) {
 // Dynamic LDS of k_expert for a plan.
 size_t lds_expert(const Plan& P) {
   const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KSD = P.I / 32;
-  size_t need = (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns) * 16;
+  size_t need = (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.d, P.ns) * 16;
   // down: p operand rows + split_sum reduction (2 float4 per thread)
-  need = std::max(need, (size_t)P.nt_max * (ks_max(KSD, P.nsd) * 8 + 1) * 16 + kWG * 2 * 16);
+  const int ksd = std::max(ks_max(KSD, P.nsd), ks_max(KSD, P.nsdl));
+  need = std::max(need, (size_t)P.nt_max * (ksd * 8 + 1) * 16 + kWG * 2 * 16);
   // combine: routing of the tokens, reduction, B^T u rows, u operand rows
   need = std::max(need, (size_t)3 * kTokPass * kMaxK * 4 + kWG * 16 + (size_t)kTokPass * kColsPerGroup * 4 +
                             (size_t)P.tpc * (KSZ * 8 + 1) * 16);
@@ -128,21 +129,45 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.tpc = std::min(kTokPass, ceil_div(B, 4));
   const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KS = KSX + KSZ, KSD = P.I / 32;
   P.nch_z = std::max(1, KSX / 2);                  // two K-steps of U per z unit
-  // expected active experts under uniform routing, to size the splits
+  // Tile sizes: the expected active experts' weight bytes spread over a
+  // nominal grid of 512 workgroups (2 per CU), kept between 16 and 64 KB per
+  // tile, so small batches run every tile in one round and large ones stream
+  // long tiles. Bytes per tile: a gate/up (expert, projection, 256 columns)
+  // holds 256 (H/d) code bytes and 256 r * 2 coefficient bytes; a VQ down
+  // (expert, 256 columns) 256 I/d; a low-rank down (expert, <= 256 ranks)
+  // min(r, 256) I * 2.
   const double exp_act = fmax(1.0, P.E * (1.0 - pow(1.0 - (double)P.k / P.E, (double)B)));
+  const double per_expert = 3.0 * P.H * P.I / P.d + 3.0 * P.I * P.r * 2;
+  // A VQ down K-step costs twice a gate/up one (p enters as hi + lo), so its
+  // bytes count double. While the expected items exceed the nominal grid
+  // the tile grows (small batches then run in one round).
+  double tile = fmin(64.0 * 1024, fmax(16.0 * 1024, exp_act * per_expert / 512.0));
+  auto splits = [&](double bytes, int max_splits) {
+    return std::max(1, std::min(max_splits, (int)lround(bytes / tile)));
+  };
   P.ncg = ceil_div(P.I, kColsPerGroup);
-  P.ns = std::min(KS, pow2_floor(1024.0 / (exp_act * 2 * P.ncg)));
-  while (P.ns < KS && (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns) * 16 > kLdsBudget) ++P.ns;
   P.ncgh = ceil_div(P.H, kColsPerGroup);
   P.ncgr = ceil_div(P.r, kColsPerGroup);
-  P.nsd = std::min(KSD, pow2_floor(512.0 / (exp_act * (P.ncgh + P.ncgr))));
-  while (P.nsd < KSD && (size_t)P.nt_max * (ks_max(KSD, P.nsd) * 8 + 1) * 16 > kLdsBudget) ++P.nsd;
+  for (;;) {
+    P.ns = splits(256.0 * (KSX * 32 / P.d) + 256.0 * P.r * 2, KS);
+    P.nsd = splits(2.0 * 256.0 * P.I / P.d, KSD);
+    P.nsdl = P.r > 0 ? splits((double)std::min(P.r, kColsPerGroup) * P.I * 2, KSD) : 1;
+    const double items = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
+    if (items <= 512.0 || tile >= 64.0 * 1024) break;
+    tile *= 1.05;
+  }
+  while (P.ns < KS && (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.d, P.ns) * 16 > kLdsBudget) ++P.ns;
+  auto down_fits = [&](int n) {
+    return (size_t)P.nt_max * (ks_max(KSD, n) * 8 + 1) * 16 + kWG * 2 * 16 <= kLdsBudget;
+  };
+  while (P.nsd < KSD && !down_fits(P.nsd)) ++P.nsd;
+  while (P.nsdl < KSD && !down_fits(P.nsdl)) ++P.nsdl;
   P.n_cb = P.ncgh * ceil_div(B, P.tpc);
 
   const int z_units = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nch_z;
   P.n_rc = (flags & F_ROUTE) ? P.nch_r * P.n_eg : 0;
   P.n_zc = (flags & F_Z) ? ceil_div(z_units, 4) : 0;
-  P.n_sel = (flags & F_ROUTE) ? B : ((flags & F_GROUP) ? 1 : 0);
+  P.n_sel = (flags & F_ROUTE) ? B : 0;
   P.n_zr = (flags & F_Z) ? ceil_div(2 * B * P.r, kWG) : 0;
   P.n_pre = P.n_rc + P.n_zc + P.n_sel + P.n_zr;
 
@@ -153,24 +178,25 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);
   P.o_rc_flag = o; o = align256(o + (size_t)P.n_rc_flags * 4);
   P.o_zc_flag = o; o = align256(o + (size_t)P.n_zc_flags * 4);
+  P.o_gu_tick = o; o = align256(o + (size_t)P.E * ceil_div(P.I, kColsPerGroup) * 4);
   P.o_gu_done = o; o = align256(o + (size_t)P.E * 4);
-  P.o_dn_done = o; o = align256(o + (size_t)P.E * (P.ncgh + P.ncgr) * 4);
+  P.o_lr_tick = o; o = align256(o + (size_t)P.E * 4);
+  P.o_dn_done = o; o = align256(o + (size_t)P.E * (ceil_div(P.H, kColsPerGroup) + 1) * 4);
   P.o_rl = o; o = align256(o + (size_t)P.nch_r * B * P.E * 8);
   P.o_zp = o; o = align256(o + (size_t)2 * P.nch_z * B * P.r * 4);
   P.o_z = o; o = align256(o + (size_t)2 * B * P.r * 4);
-  P.o_off = o; o = align256(o + (size_t)(P.E + 1) * 4);
-  P.o_act = o; o = align256(o + (size_t)P.E * 16);  // int4 (expert, first slot, count, 0)
-  P.o_nact = o; o = align256(o + 4);
-  P.o_slot_tok = o; o = align256(o + (size_t)P.S * 4);
-  P.o_slot_w = o; o = align256(o + (size_t)P.S * 4);
-  P.o_slot_e = o; o = align256(o + (size_t)P.S * 4);
-  P.o_tok_slot = o; o = align256(o + (size_t)P.S * 4);
   P.o_gu = o; o = align256(o + (size_t)P.S * 2 * P.ns * P.I * 4);
+  P.o_p = o; o = align256(o + (size_t)P.S * P.I * 4);
   P.o_dn = o; o = align256(o + (size_t)P.nsd * P.S * P.H * 4);
-  P.o_uap = o; o = align256(o + (size_t)P.nsd * P.S * P.r * 4);
+  P.o_uap = o; o = align256(o + (size_t)P.nsdl * P.S * P.r * 4);
+  P.o_u = o; o = align256(o + (size_t)P.S * P.r * 4);
   P.total = o;
   P.lds_route = lds_route(P);
-  P.lds_expert = lds_expert(P);
+  // routing tables: active-expert records and four per-slot arrays
+  P.lds_routing = round256((size_t)P.max_act * 16 + (size_t)4 * P.S * 4);
+  // item LDS, also the grouping scratch at the start of the kernel
+  const size_t group_scratch = round256((size_t)2 * P.S * 4 + (size_t)2 * P.E * 4 + 16);
+  P.lds_expert = P.lds_routing + std::max(lds_expert(P), group_scratch);
   return P;
 }
 
@@ -279,11 +305,13 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
     return fail(CARDAN_ERR_UNSUPPORTED, "shape needs %zu/%zu bytes of LDS (> %zu)", P.lds_route,
                 P.lds_expert, kLdsMax);
   hipError_t err;
-  if (P.n_pre > 0) {
+  // k_route also clears k_expert's counters, so it runs (as one workgroup
+  // if it has no items) whenever the call has expert work
+  if (P.n_pre > 0 || (P.flags & F_EXPERTS)) {
     const int cap = resident_grid(route_kernel(), P.lds_route, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_ROUTE);
-    err = launch_route(P, A, std::min(cap, P.n_pre), P.lds_route, stream);
+    err = launch_route(P, A, std::max(1, std::min(cap, P.n_pre)), P.lds_route, stream);
     if (err != hipSuccess) return hip_fail(err, "k_route launch");
     tm.done();
     if (!(P.flags & F_EXPERTS)) {  // k_expert would clear these counters

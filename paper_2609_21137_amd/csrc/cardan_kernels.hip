@@ -71,18 +71,20 @@ __device__ __forceinline__ void trace_mark(int i) {
   if (threadIdx.x == 0) s_trace[1 + i] = rt_clock();
 }
 struct ItemTrace {
-  unsigned long long t0;
-  __device__ __forceinline__ ItemTrace() : t0(rt_clock()) {
+  unsigned long long t0, c0;
+  __device__ __forceinline__ ItemTrace() : t0(rt_clock()), c0(__builtin_amdgcn_s_memtime()) {
     if (threadIdx.x < 5) s_trace[threadIdx.x] = 0;
   }
   __device__ __forceinline__ void done(const Args& A, const Plan& P, int slot, int kind) {
     if (threadIdx.x != 0) return;
-    unsigned long long* rec = reinterpret_cast<unsigned long long*>(A.ws + P.total) + 8 * (size_t)slot;
+    unsigned long long* rec = reinterpret_cast<unsigned long long*>(A.ws + P.total) + 10 * (size_t)slot;
     rec[0] = ((unsigned long long)kind << 48) | ((unsigned long long)blockIdx.x << 24) | (unsigned)slot;
     rec[1] = t0;
     rec[2] = s_trace[0];
     rec[3] = rt_clock();
     for (int i = 0; i < 4; ++i) rec[4 + i] = s_trace[1 + i];
+    rec[8] = __builtin_amdgcn_s_memtime() - c0;  // core clock cycles of the item
+    rec[9] = 0;
   }
 };
 #else
@@ -289,26 +291,43 @@ __device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c,
   set_flag(wsp<int>(A, P.o_rc_flag) + item);
 }
 
-// Groups the B*k routing slots by expert (single workgroup): per-expert
-// offsets, the ascending list of active experts, slot -> token and weight,
-// and (token, j) -> slot. Slots of one expert keep (token, j) order.
-__device__ void group_slots(const Plan& P, const Args& A, const int32_t* __restrict__ idx,
-                            const float* __restrict__ wts, uint8_t* smem) {
-  int* s_idx = reinterpret_cast<int*>(smem);  // [S]
-  int* s_cnt = s_idx + kMaxB * kMaxK;         // [E]
-  int* s_flag = s_cnt + kMaxE;                // [E]
-  int* s_tmp = s_flag + kMaxE;                // [4]
+// Routing tables of a call in LDS. Every workgroup of k_expert rebuilds them
+// from the B*k selections; the construction is deterministic, so all
+// workgroups agree on every slot number.
+struct RouteTab {
+  const int4* act;       // [nact] (expert, first slot, slot count, 0), experts ascending
+  const int* slot_tok;   // [S] token of each slot
+  const float* slot_w;   // [S] gating weight of each slot
+  const int* slot_e;     // [S] expert of each slot
+  const int* tok_slot;   // [S] slot of selection (t, j), -1 if the expert is invalid
+  int nact;
+};
+
+// Groups the B*k selections by expert into LDS (`tab`, route_lds_bytes):
+// per-expert slot ranges in (token, j) order, the ascending list of active
+// experts, slot -> token / weight / expert and (token, j) -> slot. `scratch`
+// is item LDS, free before the first item. Selections come from the routing
+// kernel of the same call or from the caller, both complete before this
+// kernel starts.
+__device__ RouteTab build_routing(const Plan& P, const int32_t* __restrict__ idx,
+                                  const float* __restrict__ wts, uint8_t* tab, uint8_t* scratch) {
   const int tid = threadIdx.x, E = P.E, S = P.S, k = P.k;
-  int* g_off = wsp<int>(A, P.o_off);
-  int* g_act = wsp<int>(A, P.o_act);
-  int* g_slot_tok = wsp<int>(A, P.o_slot_tok);
-  float* g_slot_w = wsp<float>(A, P.o_slot_w);
-  int* g_tok_slot = wsp<int>(A, P.o_tok_slot);
-  int* g_slot_e = wsp<int>(A, P.o_slot_e);
+  int4* act = reinterpret_cast<int4*>(tab);
+  int* slot_tok = reinterpret_cast<int*>(act + P.max_act);
+  float* slot_w = reinterpret_cast<float*>(slot_tok + S);
+  int* slot_e = reinterpret_cast<int*>(slot_w + S);
+  int* tok_slot = slot_e + S;
+  int* s_idx = reinterpret_cast<int*>(scratch);  // [S]
+  float* s_w = reinterpret_cast<float*>(s_idx + S);
+  int* s_cnt = reinterpret_cast<int*>(s_w + S);  // [E]
+  int* s_flag = s_cnt + E;                       // [E]
+  int* s_tmp = s_flag + E;                       // [4]
+  __shared__ int s_nact;
   for (int e = tid; e < E; e += kWG) s_cnt[e] = 0;
   for (int i = tid; i < S; i += kWG) {
-    const int e = ld_dev(idx + i);
+    const int e = idx[i];
     s_idx[i] = (e >= 0 && e < E) ? e : -1;
+    s_w[i] = wts[i];
   }
   __syncthreads();
   for (int i = tid; i < S; i += kWG)
@@ -321,39 +340,41 @@ __device__ void group_slots(const Plan& P, const Args& A, const int32_t* __restr
   for (int e = tid; e < E; e += kWG) {
     const int o = s_cnt[e];
     const int o1 = (e + 1 < E) ? s_cnt[e + 1] : total;
-    g_off[e] = o;
-    if (o1 > o) reinterpret_cast<int4*>(g_act)[s_flag[e]] = make_int4(e, o, o1 - o, 0);
+    if (o1 > o) act[s_flag[e]] = make_int4(e, o, o1 - o, 0);
   }
-  if (tid == 0) {
-    g_off[E] = total;
-    *wsp<int>(A, P.o_nact) = nact;
-  }
+  if (tid == 0) s_nact = nact;
+  // slot of selection i: the expert's first slot + the number of earlier
+  // selections of the same expert
   for (int i = tid; i < S; i += kWG) {
     const int e = s_idx[i];
     if (e < 0) {
-      g_tok_slot[i] = -1;
+      tok_slot[i] = -1;
       continue;
     }
     int rank = 0;
-    for (int j = 0; j < i; ++j) rank += (s_idx[j] == e);
+    int j = 0;
+    for (; j + 4 <= i; j += 4) {
+      const int4 v = *reinterpret_cast<const int4*>(s_idx + j);
+      rank += (v.x == e) + (v.y == e) + (v.z == e) + (v.w == e);
+    }
+    for (; j < i; ++j) rank += (s_idx[j] == e);
     const int pos = s_cnt[e] + rank;
-    g_slot_tok[pos] = i / k;
-    g_slot_w[pos] = ld_dev(wts + i);
-    g_slot_e[pos] = e;
-    g_tok_slot[i] = pos;
+    slot_tok[pos] = i / k;
+    slot_w[pos] = s_w[i];
+    slot_e[pos] = e;
+    tok_slot[i] = pos;
   }
+  __syncthreads();
+  return {act, slot_tok, slot_w, slot_e, tok_slot, s_nact};
 }
 
 // Select item for token t: logits (fixed-order sum of the chunk partials plus
 // bias), top-k by descending logit with ties to the lower index, softmax over
-// the k selected logits. The last select item groups the slots and publishes
-// the routing. With routing given by the caller there is one select item that
-// only groups.
+// the k selected logits, written to topk_idx / topk_w.
 __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) {
-  __shared__ int s_last;
   const int tid = threadIdx.x;
   const int E = P.E, k = P.k, B = P.B;
-  if (P.flags & F_ROUTE) {
+  {
     double* lg = reinterpret_cast<double*>(smem);          // [E]
     double* ex = lg + kMaxE;                                // [k]
     int* sel = reinterpret_cast<int*>(ex + kMaxK);          // [k]
@@ -364,12 +385,13 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
     for (int e = tid; e < E; e += kWG) {
       double s = 0.0;
       for (int c0 = 0; c0 < P.nch_r; c0 += 32) {
+        // 32 chunk partials in flight; chunks past the end re-read the last
+        // one and are masked out of the sum
         double v[32];
 #pragma unroll
-        for (int i = 0; i < 32; ++i)
-          v[i] = (c0 + i < P.nch_r) ? ld_dev(rl + ((size_t)(c0 + i) * B + t) * E + e) : 0.0;
+        for (int i = 0; i < 32; ++i) v[i] = ld_dev(rl + ((size_t)min(c0 + i, P.nch_r - 1) * B + t) * E + e);
 #pragma unroll
-        for (int i = 0; i < 32; ++i) s += v[i];
+        for (int i = 0; i < 32; ++i) s += (c0 + i < P.nch_r) ? v[i] : 0.0;
       }
       if (A.L.router_bias) s += (double)A.L.router_bias[e];
       lg[e] = s;
@@ -387,19 +409,27 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
       for (int i = tid; i < parts * E; i += kWG) {
         const int e = i % E, pt = i / E;
         const double v = lg[e];
-        const int f1 = min(E, (pt + 1) * per);
+        const int f0 = pt * per, f1 = min(E, f0 + per);
         int rk = 0;
-        for (int f = pt * per; f < f1; ++f) {
-          const double u = lg[f];
-          rk += (u > v) || (u == v && f < e);
+        // 8 logits per round, read together (broadcast LDS reads)
+        for (int f = f0; f < f1; f += 8) {
+          double u[8];
+#pragma unroll
+          for (int b = 0; b < 8; ++b) u[b] = lg[min(f + b, E - 1)];
+          // bitwise (not short-circuit) logic: no branches in the loop
+#pragma unroll
+          for (int b = 0; b < 8; ++b)
+            rk += ((int)(u[b] > v) | ((int)(u[b] == v) & (int)(f + b < e))) & (int)(f + b < f1);
         }
         atomicAdd(&rank[e], rk);
       }
     }
+    trace_mark(3);
     __syncthreads();
     for (int e = tid; e < E; e += kWG)
       if (rank[e] < k) sel[rank[e]] = e;
     __syncthreads();
+    trace_mark(1);
     // softmax over the k selected logits, summed in selection order
     if (tid < k) {
       const int e = sel[tid];
@@ -413,13 +443,7 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
       st_dev(A.topk_idx + t * k + tid, sel[tid]);
       st_dev(A.topk_w + t * k + tid, (float)(ex[tid] / sum));
     }
-    if (!(P.flags & F_GROUP)) return;
-    trace_mark(1);
-    if (!last_of(ctr(A, C_SEL_TICK), P.n_sel, &s_last)) return;
     trace_mark(2);
-    group_slots(P, A, A.topk_idx, A.topk_w, smem);
-  } else {
-    group_slots(P, A, A.idx_in, A.w_in, smem);  // caller routing, written before the call
   }
 }
 
@@ -465,8 +489,16 @@ __device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
 // prime() issues the first PD steps so callers can start the HBM traffic
 // before they wait for their activations.
 
-__device__ __forceinline__ uint4 a_operand(const uint4* __restrict__ ops, int idx, bool valid) {
-  return valid ? ops[idx] : make_uint4(0, 0, 0, 0);
+// MFMA rows are independent, so token rows past nt simply repeat row nt - 1
+// (never stored) instead of branching around the LDS read.
+__device__ __forceinline__ int a_row(int n, int nt) { return min(n, nt - 1); }
+
+// Scheduling of one K-step: all LDS operand reads first, then the MFMAs, so
+// the reads' latencies overlap instead of each MFMA waiting for its own.
+template <int NREAD, int NMFMA>
+__device__ __forceinline__ void sched_step() {
+  __builtin_amdgcn_sched_group_barrier(0x100, NREAD, 0);  // DS reads
+  __builtin_amdgcn_sched_group_barrier(0x008, NMFMA, 0);  // MFMA
 }
 
 template <int D, int NOPS, int PD>
@@ -506,24 +538,28 @@ struct VqPipe {
                                        const uint4* __restrict__ ops, int ops_ld, int ops_ks0, int nt,
                                        f32x4 acc[4]) {
     const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
-    const int oi = n * ops_ld + ((ks - ops_ks0) * 4 + g) * NOPS;
-    const uint4 a0 = a_operand(ops, oi, n < nt);
+    const int oi = a_row(n, nt) * ops_ld + ((ks - ops_ks0) * 4 + g) * NOPS;
+    const uint4 a0 = ops[oi];
     uint4 a1 = a0;
-    if (NOPS == 2) a1 = a_operand(ops, oi + 1, n < nt);
+    if (NOPS == 2) a1 = ops[oi + 1];
     const uint2* cb2 = reinterpret_cast<const uint2*>(cb_s);
+    uint4 w[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      uint4 w;
       if constexpr (D == 8) {
-        w = cb_s[(b[0] >> (8 * q)) & 255u];
+        w[q] = cb_s[(b[0] >> (8 * q)) & 255u];
       } else {
         const uint2 lo = cb2[(b[0] >> (8 * q)) & 255u];
         const uint2 hi = cb2[(b[1] >> (8 * q)) & 255u];
-        w = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        w[q] = make_uint4(lo.x, lo.y, hi.x, hi.y);
       }
-      acc[q] = mfma_bf16(a0, w, acc[q]);
-      if (NOPS == 2) acc[q] = mfma_bf16(a1, w, acc[q]);
     }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc[q] = mfma_bf16(a0, w[q], acc[q]);
+      if (NOPS == 2) acc[q] = mfma_bf16(a1, w[q], acc[q]);
+    }
+    sched_step<NOPS + (D == 8 ? 4 : 8), 4 * NOPS>();
   }
   __device__ __forceinline__ void run(const uint4* cb_s, const uint4* ops, int ops_ld, int ops_ks0,
                                       int nt, f32x4 acc[4]) {
@@ -585,10 +621,10 @@ struct DensePipe {
   __device__ __forceinline__ void step(int ks, const uint2 (&b)[8], const uint4* __restrict__ ops, int ops_ld,
                                        int ops_ks0, int nt, f32x4 acc[4]) {
     const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
-    const int oi = n * ops_ld + ((ks - ops_ks0) * 4 + g) * NOPS;
-    const uint4 a0 = a_operand(ops, oi, n < nt);
+    const int oi = a_row(n, nt) * ops_ld + ((ks - ops_ks0) * 4 + g) * NOPS;
+    const uint4 a0 = ops[oi];
     uint4 a1 = a0;
-    if (NOPS == 2) a1 = a_operand(ops, oi + 1, n < nt);
+    if (NOPS == 2) a1 = ops[oi + 1];
     const uint4 w0 = dense_w<0>(b), w1 = dense_w<1>(b), w2 = dense_w<2>(b), w3 = dense_w<3>(b);
     acc[0] = mfma_bf16(a0, w0, acc[0]);
     acc[1] = mfma_bf16(a0, w1, acc[1]);
@@ -600,6 +636,7 @@ struct DensePipe {
       acc[2] = mfma_bf16(a1, w2, acc[2]);
       acc[3] = mfma_bf16(a1, w3, acc[3]);
     }
+    sched_step<NOPS, 4 * NOPS>();
   }
   __device__ __forceinline__ void run(const uint4* ops, int ops_ld, int ops_ks0, int nt, f32x4 acc[4]) {
     for (int i0 = 0; i0 < nks; i0 += PD) {
@@ -797,27 +834,29 @@ struct Routing {
   int e, s0, ne;
 };
 
-// (expert, first slot, slot count) of active expert a: one 16-byte load
-__device__ __forceinline__ Routing expert_of(const Plan& P, const Args& A, int a) {
-  const int4 v = wsp<const int4>(A, P.o_act)[a];
+// (expert, first slot, slot count) of active expert a
+__device__ __forceinline__ Routing expert_of(const RouteTab& RT, int a) {
+  const int4 v = RT.act[a];
   return {v.x, v.y, v.z};
 }
 
 // Gate/up tile (a, pj, cg, s): 256 output columns of projection pj over
 // split s of the joint reduction axis [x (H inputs) | z (r ranks)], i.e. the
 // VQ gather sum and V^T z accumulate in the same MFMA accumulators. Each
-// tile writes its partial sums and counts itself done for its expert.
+// tile writes its partial sums.
 template <int D>
-__device__ void item_gateup(const Plan& P, const Args& A, int jt, const uint4* cbs, uint8_t* smem) {
+__device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, int jt, const uint4* cbs,
+                            uint8_t* smem) {
   const int s = jt % P.ns;
   jt /= P.ns;
   const int cg = jt % P.ncg;
   jt /= P.ncg;
   const int pj = jt & 1, a = jt >> 1;
-  const Routing R = expert_of(P, A, a);
+  const Routing R = expert_of(RT, a);
   const int H = P.H, I = P.I, r = P.r, B = P.B;
-  const int KSX = H / 32, KSZ = (r + 31) / 32, KS = KSX + KSZ;
-  const int ks0 = s * KS / P.ns, ks1 = (s + 1) * KS / P.ns;
+  const int KSX = H / 32, KSZ = (r + 31) / 32;
+  int ks0, ks1;
+  joint_split(s, P.ns, KSX, KSZ, D, ks0, ks1);
   const int x0 = min(ks0, KSX), x1 = min(ks1, KSX);
   const int z0 = max(ks0, KSX) - KSX, z1 = max(ks1, KSX) - KSX;
   const int w = threadIdx.x >> 6;
@@ -829,7 +868,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, int jt, const uint4* c
   uint4* xs = reinterpret_cast<uint4*>(smem);
   uint4* zs = xs + P.nt_max * ldx;
   float* gu = wsp<float>(A, P.o_gu);
-  const int* slot_tok = wsp<const int>(A, P.o_slot_tok);
+  const int* slot_tok = RT.slot_tok;
   const float* zsrc = (P.flags & F_Z) ? A.z_out : A.z_in;
   const uint4* cb = cbs + pj * 256;
 
@@ -873,53 +912,63 @@ __device__ void item_gateup(const Plan& P, const Args& A, int jt, const uint4* c
     trace_mark(2);
   }
 
+  // The last of the 2 ns tiles of (a, cg) forms p = silu(g) * u for the
+  // expert's tokens on these 256 columns from all partial sums, once, and
+  // counts the column group done for the expert.
+  __shared__ int s_last;
+  int* tick = wsp<int>(A, P.o_gu_tick) + a * P.ncg + cg;
+  const bool last = last_of(tick, 2 * P.ns, &s_last);
   trace_mark(3);
+  if (!last) return;
+  const int ns = P.ns, nq = kColsPerGroup / 4, cbase = cg * kColsPerGroup;
+  float* pbuf = wsp<float>(A, P.o_p);
+  float4* red = reinterpret_cast<float4*>(smem);
+  split_sum<2, 8>(
+      R.ne * nq, ns, red,
+      [&](int item, int sp, float4(&v)[2], float& wt) {
+        const int t = item / nq, col = cbase + 4 * (item % nq);
+        if (sp < 0 || col >= I) {
+          v[0] = v[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+          wt = 0.f;
+          return;
+        }
+        const float* src = gu + ((size_t)(R.s0 + t) * 2 * ns + sp) * I + col;
+        v[0] = ld_dev4(src);
+        v[1] = ld_dev4(src + (size_t)ns * I);
+        wt = 1.f;
+      },
+      [&](int item, const float4(&gsum)[2]) {
+        const int t = item / nq, col = cbase + 4 * (item % nq);
+        if (col >= I) return;
+        const float4 g = gsum[0], u = gsum[1];
+        st_dev4(pbuf + (size_t)(R.s0 + t) * I + col,
+                make_float4(g.x / (1.0f + expf(-g.x)) * u.x, g.y / (1.0f + expf(-g.y)) * u.y,
+                            g.z / (1.0f + expf(-g.z)) * u.z, g.w / (1.0f + expf(-g.w)) * u.w));
+      });
+  if (threadIdx.x == 0) *tick = 0;
   publish(wsp<int>(A, P.o_gu_done) + R.e);
 }
 
 // Down tile (a, cgx, s) over split s of I, 256 output columns: for cgx <
-// ncgh the VQ columns of H (Q^T p -> dn[s]), else the low-rank columns of r
-// (A_e^T p -> uap[s]). Weight loads are issued before waiting for the
-// expert's p.
-template <typename Pipe, typename Prime, typename Run, typename Dst>
-__device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Routing& R, int a, int s,
-                                          int cgx, int ks0, int ks1, int c0, int n_out, Pipe& pipe, Prime prime,
-                                          Run run, Dst dst, uint8_t* smem) {
+// ncgh the VQ columns of H (Q^T p -> dn[s], nsd splits), else the low-rank
+// columns of r (A_e^T p -> uap[s], nsdl splits: the coefficient bytes of a
+// K-step are 16x the code bytes). Weight loads are issued before waiting
+// for the expert's p.
+template <typename Prime, typename Run, typename Dst>
+__device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Routing& R, int ks0, int ks1,
+                                          int c0, int n_out, Prime prime, Run run, Dst dst, uint8_t* smem) {
   prime();
-  wait_geq(A, wsp<int>(A, P.o_gu_done) + R.e, gateup_tiles_per_expert(P));
-  const int I = P.I, ns = P.ns;
+  wait_geq(A, wsp<int>(A, P.o_gu_done) + R.e, P.ncg);
+  const int I = P.I;
   const int ld = (ks1 - ks0) * 8 + 1;
-  const int nq = (ks1 - ks0) * 8;  // quads of inputs of this split
   uint4* ps = reinterpret_cast<uint4*>(smem);
-  float4* red = reinterpret_cast<float4*>(ps + P.nt_max * ld);
-  const float* gu = wsp<const float>(A, P.o_gu);
+  const float* pbuf = wsp<const float>(A, P.o_p);
   for (int tg = 0; tg < R.ne; tg += kTokPass) {
     const int nt = min(kTokPass, R.ne - tg);
     if (tg > 0) prime();
     __syncthreads();
-    // p = silu(sum of the gate splits) * (sum of the up splits) for inputs
-    // [32 ks0, 32 ks1) of the tokens, staged as bf16 hi/lo
-    split_sum<2, 4>(
-        nt * nq, ns, red,
-        [&](int item, int sp, float4(&v)[2], float& wt) {
-          const int t = item / nq, q = item % nq;
-          if (sp < 0) {
-            v[0] = v[1] = make_float4(0.f, 0.f, 0.f, 0.f);
-            wt = 0.f;
-            return;
-          }
-          const float* src = gu + ((size_t)(R.s0 + tg + t) * 2 * ns + sp) * I + ks0 * 32 + 4 * q;
-          v[0] = ld_dev4(src);
-          v[1] = ld_dev4(src + (size_t)ns * I);
-          wt = 1.f;
-        },
-        [&](int item, const float4(&gsum)[2]) {
-          const int t = item / nq, q = item % nq;
-          const float4 g = gsum[0], u = gsum[1];
-          const float4 pv = make_float4(g.x / (1.0f + expf(-g.x)) * u.x, g.y / (1.0f + expf(-g.y)) * u.y,
-                                        g.z / (1.0f + expf(-g.z)) * u.z, g.w / (1.0f + expf(-g.w)) * u.w);
-          put_split_quad(ps + t * ld, q, pv);
-        });
+    stage_split(ps, ld, nt, (ks1 - ks0) * 4,
+                [&](int t) { return pbuf + (size_t)(R.s0 + tg + t) * I + ks0 * 32; });
     __syncthreads();
     trace_mark(0);
     f32x4 acc[4];
@@ -927,48 +976,66 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
     run(ps, ld, nt, acc);
     store_acc(acc, nt, c0, n_out, [&](int t) { return dst(R.s0 + tg + t); });
   }
-  publish(wsp<int>(A, P.o_dn_done) + R.e * (P.ncgh + P.ncgr) + cgx);
-  (void)pipe;
-  (void)s;
-  (void)a;
 }
 
 template <int D>
-__device__ void item_down_vq(const Plan& P, const Args& A, int a, int cgx, int s,
-                                          const uint4* cbs, uint8_t* smem) {
-  const Routing R = expert_of(P, A, a);
+__device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgx, int s,
+                             const uint4* cbs, uint8_t* smem) {
+  const Routing R = expert_of(RT, a);
   const int H = P.H, I = P.I, S = P.S, KS = I / 32;
   const int ks0 = s * KS / P.nsd, ks1 = (s + 1) * KS / P.nsd;
   const int c0 = cgx * kColsPerGroup + (threadIdx.x >> 6) * 64;
   const uint8_t* codes = A.L.codes_down + (size_t)R.e * (I / D) * H;
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
   VqPipe<D, 2, kPdVq> pipe;
-  down_body(P, A, R, a, s, cgx, ks0, ks1, c0, H, pipe, [&]() { pipe.prime(codes, H, c0, H, ks0, ks1); },
+  down_body(P, A, R, ks0, ks1, c0, H, [&]() { pipe.prime(codes, H, c0, H, ks0, ks1); },
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs + 2 * 256, ps, ld, ks0, nt, acc); },
             [&](int slot) { return dn + (size_t)slot * H; }, smem);
+  publish(wsp<int>(A, P.o_dn_done) + R.e * (P.ncgh + 1) + cgx);
 }
 
-__device__ void item_down_lr(const Plan& P, const Args& A, int a, int cgr, int s,
-                                          uint8_t* smem) {
-  const Routing R = expert_of(P, A, a);
-  const int I = P.I, r = P.r, S = P.S, KS = I / 32;
-  const int ks0 = s * KS / P.nsd, ks1 = (s + 1) * KS / P.nsd;
+// Low-rank down tile (a, cgr, s): partial A_e^T p over split s of I. The
+// last of the expert's ncgr * nsdl tiles sums the splits into u_e[slot]
+// (r values per slot) and flags the expert's low-rank part done.
+__device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgr, int s,
+                             uint8_t* smem) {
+  __shared__ int s_last;
+  const Routing R = expert_of(RT, a);
+  const int I = P.I, r = P.r, S = P.S, KS = I / 32, nsdl = P.nsdl;
+  const int ks0 = s * KS / nsdl, ks1 = (s + 1) * KS / nsdl;
   const int c0 = cgr * kColsPerGroup + (threadIdx.x >> 6) * 64;
   const uint16_t* Ae = A.L.A_down + (size_t)R.e * I * r;
-  float* uap = wsp<float>(A, P.o_uap) + (size_t)s * S * r;
+  float* uap = wsp<float>(A, P.o_uap);
   DensePipe<2, kPdDense> pipe;
-  down_body(P, A, R, a, s, P.ncgh + cgr, ks0, ks1, c0, r, pipe, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); },
+  down_body(P, A, R, ks0, ks1, c0, r, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); },
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(ps, ld, ks0, nt, acc); },
-            [&](int slot) { return uap + (size_t)slot * r; }, smem);
+            [&](int slot) { return uap + ((size_t)s * S + slot) * r; }, smem);
+  int* tick = wsp<int>(A, P.o_lr_tick) + R.e;
+  if (!last_of(tick, P.ncgr * nsdl, &s_last)) return;
+  const int nq = r / 4;
+  float* u = wsp<float>(A, P.o_u);
+  split_sum<1, 8>(
+      R.ne * nq, nsdl, reinterpret_cast<float4*>(smem),
+      [&](int item, int sp, float4(&v)[1], float& wt) {
+        if (sp < 0) {
+          v[0] = make_float4(0.f, 0.f, 0.f, 0.f);
+          wt = 0.f;
+          return;
+        }
+        v[0] = ld_dev4(uap + ((size_t)sp * S + R.s0 + item / nq) * r + 4 * (item % nq));
+        wt = 1.f;
+      },
+      [&](int item, const float4(&q)[1]) { st_dev4(u + (size_t)(R.s0 + item / nq) * r + 4 * (item % nq), q[0]); });
+  if (threadIdx.x == 0) *tick = 0;
+  publish(wsp<int>(A, P.o_dn_done) + R.e * (P.ncgh + 1) + P.ncgh);
 }
 
 // Combine tile (cgy, tq): output columns [256 cgy, +256) of tokens
 // [tpc tq, tpc tq + tpc): y[t] = sum_j a_j sum_s dn[s][slot_j] + B^T u[t]
-// with u[t] = sum_j a_j sum_s uap[s][slot_j]. B rows are loaded before the
-// wait; B^T u runs on MFMA with u as bf16 hi/lo. The routing of the tile's
-// tokens is read once into LDS; every partial sum keeps all its loads in
-// flight (split_sum).
-__device__ void item_combine(const Plan& P, const Args& A, int jc, uint8_t* smem) {
+// with u[t] = sum_j a_j u_e[slot_j]. B rows are loaded before the
+// wait; B^T u runs on MFMA with u as bf16 hi/lo. Every partial sum keeps all
+// its loads in flight (split_sum).
+__device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, int jc, uint8_t* smem) {
   const int cgy = jc % P.ncgh, tq = jc / P.ncgh;
   const int H = P.H, r = P.r, k = P.k, S = P.S, nsd = P.nsd;
   const int t0 = tq * P.tpc, nt = min(P.tpc, P.B - t0);
@@ -978,55 +1045,42 @@ __device__ void item_combine(const Plan& P, const Args& A, int jc, uint8_t* smem
   DensePipe<2, kPdDense> bp;
   if (r > 0) bp.prime(A.L.B_down, H, cbase + w * 64, H, r, 0, KSR);
 
-  int* s_slot = reinterpret_cast<int*>(smem);      // [nt * k]
-  float* s_w = reinterpret_cast<float*>(s_slot + kTokPass * kMaxK);
-  int* s_e = reinterpret_cast<int*>(s_w + kTokPass * kMaxK);
-  float4* red = reinterpret_cast<float4*>(s_e + kTokPass * kMaxK);  // [256]
-  float* bt = reinterpret_cast<float*>(red + kWG);                  // [nt][256] B^T u
+  const int* s_slot = RT.tok_slot + t0 * k;  // (t, j) -> slot of the tile's tokens
+  const float* s_w_slot = RT.slot_w;
+  const int* s_e_slot = RT.slot_e;
+  float4* red = reinterpret_cast<float4*>(smem);                      // [256]
+  float* bt = reinterpret_cast<float*>(red + kWG);                    // [nt][256] B^T u
   uint4* us = reinterpret_cast<uint4*>(bt + kTokPass * kColsPerGroup);
   const int ntk = nt * k;
-  {
-    const int* tok_slot = wsp<const int>(A, P.o_tok_slot) + t0 * k;
-    const float* slot_w = wsp<const float>(A, P.o_slot_w);
-    const int* slot_e = wsp<const int>(A, P.o_slot_e);
-    for (int i = tid; i < ntk; i += kWG) {
-      const int sl = tok_slot[i];
-      s_slot[i] = sl;
-      s_w[i] = sl >= 0 ? slot_w[sl] : 0.0f;
-      s_e[i] = sl >= 0 ? slot_e[sl] : 0;
-    }
-  }
-  __syncthreads();
   {
     // every down tile of this column group (and of the low-rank columns) of
     // every expert of these tokens
     const int* dnd = wsp<const int>(A, P.o_dn_done);
-    const int ncol = 1 + P.ncgr, per_e = P.ncgh + P.ncgr;
+    const int ncol = r > 0 ? 2 : 1, per_e = P.ncgh + 1;
     wait_all(A, ntk * ncol, [&](int i) {
       const int c = i % ncol, tj = i / ncol;
-      if (s_slot[tj] < 0) return true;
-      const int cgx = c == 0 ? cgy : P.ncgh + c - 1;
-      return ld_dev(dnd + s_e[tj] * per_e + cgx) >= nsd;
+      const int sl = s_slot[tj];
+      if (sl < 0) return true;
+      return ld_dev(dnd + s_e_slot[sl] * per_e + (c == 0 ? cgy : P.ncgh)) >= (c == 0 ? nsd : 1);
     });
   }
-  const int npair = k * nsd;  // (j, s) partials per output
   if (r > 0) {
-    // u[t] in quads of ranks (zero past r), staged as bf16 hi/lo
-    const float* uap = wsp<const float>(A, P.o_uap);
+    // u[t] = sum_j a_j u_ej[slot_j] in quads of ranks (zero past r), staged
+    // as bf16 hi/lo
+    const float* ue = wsp<const float>(A, P.o_u);
     const int nq = KSR * 8, ld = KSR * 8 + 1;
     split_sum<1, 8>(
-        nt * nq, npair, red,
-        [&](int item, int p, float4(&v)[1], float& wt) {
+        nt * nq, k, red,
+        [&](int item, int j, float4(&v)[1], float& wt) {
           const int t = item / nq, q = item % nq;
-          const int j = p / nsd, ss = p % nsd;
-          const int sl = p >= 0 ? s_slot[t * k + j] : -1;
+          const int sl = j >= 0 ? s_slot[t * k + j] : -1;
           if (sl < 0 || 4 * q >= r) {
             v[0] = make_float4(0.f, 0.f, 0.f, 0.f);
             wt = 0.f;
             return;
           }
-          v[0] = ld_dev4(uap + ((size_t)ss * S + sl) * r + 4 * q);
-          wt = s_w[t * k + j];
+          v[0] = ld_dev4(ue + (size_t)sl * r + 4 * q);
+          wt = s_w_slot[sl];
         },
         [&](int item, const float4(&u)[1]) { put_split_quad(us + (item / nq) * ld, item % nq, u[0]); });
     __syncthreads();
@@ -1049,7 +1103,7 @@ __device__ void item_combine(const Plan& P, const Args& A, int jc, uint8_t* smem
   // VQ part and output, one float4 of 4 columns per item
   const float* dn = wsp<const float>(A, P.o_dn);
   split_sum<1, 8>(
-      nt * 64, npair, red,
+      nt * 64, k * nsd, red,
       [&](int item, int p, float4(&v)[1], float& wt) {
         const int t = item >> 6, col = cbase + 4 * (item & 63);
         const int j = p / nsd, ss = p % nsd;
@@ -1060,7 +1114,7 @@ __device__ void item_combine(const Plan& P, const Args& A, int jc, uint8_t* smem
           return;
         }
         v[0] = ld_dev4(dn + ((size_t)ss * S + sl) * H + col);
-        wt = s_w[t * k + j];
+        wt = s_w_slot[sl];
       },
       [&](int item, const float4(&q)[1]) {
         const int t = item >> 6, c4 = item & 63, col = cbase + 4 * c4;
@@ -1088,8 +1142,10 @@ __device__ __forceinline__ void clear_ints(int* p, int n) {
 __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   if (blockIdx.x == 0 && (P.flags & F_EXPERTS)) {
+    clear_ints(wsp<int>(A, P.o_gu_tick), P.E * P.ncg);
     clear_ints(wsp<int>(A, P.o_gu_done), P.E);
-    clear_ints(wsp<int>(A, P.o_dn_done), P.E * (P.ncgh + P.ncgr));
+    clear_ints(wsp<int>(A, P.o_lr_tick), P.E);
+    clear_ints(wsp<int>(A, P.o_dn_done), P.E * (P.ncgh + 1));
   }
   for (int j = blockIdx.x; j < P.n_pre; j += gridDim.x) {
     __syncthreads();
@@ -1113,7 +1169,6 @@ __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
 
 // Clears the routing kernel's counters (after calls that run k_route alone).
 __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
-  clear_ints(ctr(A, C_SEL_TICK), 1);
   clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags);
   clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags);
 }
@@ -1147,11 +1202,14 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     }
   }
   if (blockIdx.x == 0) {
-    clear_ints(ctr(A, C_SEL_TICK), 1);
     clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags);
     clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags);
   }
-  const int nact = *wsp<const int>(A, P.o_nact);
+  // routing tables at the start of dynamic LDS, item LDS after them
+  uint8_t* item_smem = smem + P.lds_routing;
+  const RouteTab RT = (P.flags & F_ROUTE) ? build_routing(P, A.topk_idx, A.topk_w, smem, item_smem)
+                                          : build_routing(P, A.idx_in, A.w_in, smem, item_smem);
+  const int nact = RT.nact;
   const int tgu = gateup_tiles_per_expert(P), tdn = down_tiles_per_expert(P);
   const int n_items = nact * (tgu + tdn) + P.n_cb;
   for (int jp = blockIdx.x; jp < n_items; jp += gridDim.x) {
@@ -1159,19 +1217,19 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     ItemTrace tr;
     int j = jp, kind = 4;
     if (j < nact * tgu) {
-      item_gateup<D>(P, A, j, cbs, smem);
+      item_gateup<D>(P, A, RT, j, cbs, item_smem);
     } else if ((j -= nact * tgu) < nact * tdn) {
-      const int a = j / tdn, rem = j % tdn, cgx = rem / P.nsd, s = rem % P.nsd;
-      if (cgx < P.ncgh) {
+      const int a = j / tdn, rem = j % tdn, nvq = P.ncgh * P.nsd;
+      if (rem < nvq) {
         kind = 5;
-        item_down_vq<D>(P, A, a, cgx, s, cbs, smem);
+        item_down_vq<D>(P, A, RT, a, rem / P.nsd, rem % P.nsd, cbs, item_smem);
       } else {
         kind = 6;
-        item_down_lr(P, A, a, cgx - P.ncgh, s, smem);
+        item_down_lr(P, A, RT, a, (rem - nvq) / P.nsdl, (rem - nvq) % P.nsdl, item_smem);
       }
     } else {
       kind = 7;
-      item_combine(P, A, j - nact * tdn, smem);
+      item_combine(P, A, RT, j - nact * tdn, item_smem);
     }
     tr.done(A, P, P.n_pre + jp, kind);
   }

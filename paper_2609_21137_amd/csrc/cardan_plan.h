@@ -13,13 +13,16 @@
 //   router chunks   (64 hidden rows x 64 experts), float64 partial logits
 //   z items         four waves, each (basis, 64 ranks, split of H): partial
 //                   U^T x on MFMA
-//   select          per token: logits, top-k, gating; the last one groups the
-//                   slots by expert and publishes the routing
+//   select          per token: logits, top-k, gating
 //   z reduce        256 outputs of z = U^T x each
 //   gate/up tiles   (active expert a, gate|up, 256 columns, split of the
-//                   joint axis [H inputs | r ranks])
-//   down tiles      (a, 256 output columns of [H | r], split of I)
+//                   joint axis [H inputs | r ranks]), partial sums; the last
+//                   tile of (a, columns) forms p = silu(g) * u
+//   down tiles      (a, 256 output columns of [H | r], split of I); the last
+//                   low-rank tile of an expert sums its splits into u_e
 //   combine tiles   (256 output columns, group of tpc tokens)
+// Every k_expert workgroup first groups the selections by expert in its own
+// LDS (the routing tables), so items look up experts and slots in LDS.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -40,8 +43,8 @@ constexpr int kMaxE = 1024, kMaxK = 32, kMaxR = 512, kMaxB = 64;
 enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8 };
 
 // counters at the start of the workspace, one per 64-byte slot: the status
-// count of timed-out waits and the select ticket
-enum { C_ERR = 0, C_SEL_TICK, C_NUM };
+// count of timed-out waits
+enum { C_ERR = 0, C_NUM };
 constexpr int kCtrStride = 16;      // ints between counters
 
 struct Plan {
@@ -57,7 +60,8 @@ struct Plan {
   int ns;         // gate/up splits of the joint K axis (H/32 + ceil(r/32) steps)
   int ncgh;       // VQ down column groups (H / 256, rounded up)
   int ncgr;       // low-rank down column groups (r / 256, rounded up)
-  int nsd;        // down splits of the I K-steps
+  int nsd;        // VQ down splits of the I K-steps
+  int nsdl;       // low-rank down splits of the I K-steps
   int nt_max;     // most token slots one expert tile stages (min(B, 16))
   int tpc;        // tokens per combine tile
   int n_cb;       // combine tiles
@@ -65,15 +69,32 @@ struct Plan {
   int n_rc, n_zc, n_sel, n_zr, n_pre;
   int n_rc_flags, n_zc_flags;  // flag slots (shape-wide maxima of n_rc, n_zc)
   // workspace byte offsets
-  size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_done, o_dn_done;  // counters
-  size_t o_rl, o_zp, o_z, o_off, o_act, o_nact, o_slot_tok, o_slot_w, o_slot_e, o_tok_slot, o_gu,
-      o_dn, o_uap, total;
+  size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_tick, o_gu_done, o_lr_tick, o_dn_done;  // counters
+  size_t o_rl, o_zp, o_z, o_gu, o_p, o_dn, o_uap, o_u, total;
   size_t lds_route, lds_expert;  // dynamic LDS of the two kernels
+  size_t lds_routing;            // routing tables at the start of k_expert's dynamic LDS
 };
 
 __host__ __device__ inline int gateup_tiles_per_expert(const Plan& P) { return 2 * P.ncg * P.ns; }
 __host__ __device__ inline int down_tiles_per_expert(const Plan& P) {
-  return (P.ncgh + P.ncgr) * P.nsd;
+  return P.ncgh * P.nsd + P.ncgr * P.nsdl;
+}
+
+// Cost of one low-rank K-step of a gate/up tile relative to one VQ K-step:
+// a wave reads 64 x 32/d code bytes per VQ step and 32 x 64 bf16 (4 KB) per
+// low-rank step.
+__host__ __device__ inline int lr_step_cost(int d) { return 2 * d; }
+
+// K-steps [k0, k1) of gate/up split s of n over the joint axis of KSX VQ
+// steps and KSZ low-rank steps, balanced by bytes (lr_step_cost).
+__host__ __device__ inline void joint_split(int s, int n, int KSX, int KSZ, int d, int& k0, int& k1) {
+  const int wz = lr_step_cost(d);
+  const long total = KSX + (long)KSZ * wz;
+  auto step_at = [&](long c) -> int {
+    return c <= KSX ? (int)c : KSX + (int)((c - KSX + wz - 1) / wz);
+  };
+  k0 = step_at(s * total / n);
+  k1 = step_at((s + 1) * total / n);
 }
 
 // Device pointers of one call.
