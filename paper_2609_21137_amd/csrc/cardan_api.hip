@@ -195,7 +195,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // routing tables: active-expert records and four per-slot arrays
   P.lds_routing = round256((size_t)P.max_act * 16 + (size_t)4 * P.S * 4);
   // item LDS, also the grouping scratch at the start of the kernel
-  const size_t group_scratch = round256((size_t)2 * P.S * 4 + (size_t)2 * P.E * 4 + 16);
+  const size_t group_scratch = round256((size_t)2 * P.S * 4 + (size_t)4 * P.E * 4 + 32);
   P.lds_expert = P.lds_routing + std::max(lds_expert(P), group_scratch);
   return P;
 }

@@ -194,6 +194,18 @@ __device__ __forceinline__ bool last_of(int* tick, int total, int* s_flag) {
   return *s_flag;
 }
 
+// Inclusive prefix sum across a wave64 with DPP row shifts and row
+// broadcasts (lanes without a source add the 0 `old` operand).
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15 into rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
 // Exclusive prefix sum of arr[0..n) (n <= 4 * kWG) in place; returns the total.
 __device__ int block_exclusive_scan(int* arr, int n, int* tmp4) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -204,12 +216,7 @@ __device__ int block_exclusive_scan(int* arr, int n, int* tmp4) {
     v[j] = (base + j < n) ? arr[base + j] : 0;
     s += v[j];
   }
-  int incl = s;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int t = __shfl_up(incl, o);
-    if (lane >= o) incl += t;
-  }
+  const int incl = wave_inclusive_scan(s);
   if (lane == 63) tmp4[w] = incl;
   __syncthreads();
   int pre = 0;
@@ -306,45 +313,63 @@ struct RouteTab {
 // Groups the B*k selections by expert into LDS (`tab`, route_lds_bytes):
 // per-expert slot ranges in (token, j) order, the ascending list of active
 // experts, slot -> token / weight / expert and (token, j) -> slot. `scratch`
-// is item LDS, free before the first item. Selections come from the routing
-// kernel of the same call or from the caller, both complete before this
-// kernel starts.
-__device__ RouteTab build_routing(const Plan& P, const int32_t* __restrict__ idx,
-                                  const float* __restrict__ wts, uint8_t* tab, uint8_t* scratch) {
+// is item LDS, free before the first expert item. Selections come from the
+// routing kernel of the same call or from the caller, both complete before
+// this kernel starts. `distinct`: no token selects an expert twice (top-k
+// output), so a slot's rank among its expert's slots comes from a token mask.
+__device__ RouteTab build_routing(const Plan& P, const int32_t* idx, const float* wts, uint8_t* tab,
+                                  uint8_t* scratch, bool distinct) {
   const int tid = threadIdx.x, E = P.E, S = P.S, k = P.k;
   int4* act = reinterpret_cast<int4*>(tab);
   int* slot_tok = reinterpret_cast<int*>(act + P.max_act);
   float* slot_w = reinterpret_cast<float*>(slot_tok + S);
   int* slot_e = reinterpret_cast<int*>(slot_w + S);
   int* tok_slot = slot_e + S;
-  int* s_idx = reinterpret_cast<int*>(scratch);  // [S]
-  float* s_w = reinterpret_cast<float*>(s_idx + S);
-  int* s_cnt = reinterpret_cast<int*>(s_w + S);  // [E]
-  int* s_flag = s_cnt + E;                       // [E]
-  int* s_tmp = s_flag + E;                       // [4]
+  int* s_idx = reinterpret_cast<int*>(scratch);            // [S]
+  float* s_w = reinterpret_cast<float*>(s_idx + S);        // [S]
+  int* s_cnt = reinterpret_cast<int*>(s_w + S);            // [E] count | active << 16
+  unsigned* s_mask = reinterpret_cast<unsigned*>(s_cnt + E);  // [E][2] tokens of each expert
+  int* s_tmp = reinterpret_cast<int*>(s_mask + 2 * E);     // [4]
   __shared__ int s_nact;
-  for (int e = tid; e < E; e += kWG) s_cnt[e] = 0;
-  for (int i = tid; i < S; i += kWG) {
-    const int e = idx[i];
-    s_idx[i] = (e >= 0 && e < E) ? e : -1;
-    s_w[i] = wts[i];
-  }
-  __syncthreads();
-  for (int i = tid; i < S; i += kWG)
-    if (s_idx[i] >= 0) atomicAdd(&s_cnt[s_idx[i]], 1);
-  __syncthreads();
-  for (int e = tid; e < E; e += kWG) s_flag[e] = s_cnt[e] > 0;
-  __syncthreads();
-  const int total = block_exclusive_scan(s_cnt, E, s_tmp);
-  const int nact = block_exclusive_scan(s_flag, E, s_tmp);
   for (int e = tid; e < E; e += kWG) {
-    const int o = s_cnt[e];
-    const int o1 = (e + 1 < E) ? s_cnt[e + 1] : total;
-    if (o1 > o) act[s_flag[e]] = make_int4(e, o, o1 - o, 0);
+    s_cnt[e] = 0;
+    s_mask[2 * e] = s_mask[2 * e + 1] = 0u;
   }
-  if (tid == 0) s_nact = nact;
+  for (int i = tid; i < S; i += kWG) {
+    const int e = ld_dev(idx + i);
+    s_idx[i] = (e >= 0 && e < E) ? e : -1;
+    s_w[i] = ld_dev(wts + i);
+  }
+  __syncthreads();
+  trace_mark(0);
+  for (int i = tid; i < S; i += kWG) {
+    const int e = s_idx[i];
+    if (e < 0) continue;
+    atomicAdd(&s_cnt[e], 1);
+    if (distinct) {
+      const int t = i / k;
+      atomicOr(&s_mask[2 * e + (t >> 5)], 1u << (t & 31));
+    }
+  }
+  __syncthreads();
+  // one scan gives both the first slot of every expert (low 16 bits) and
+  // its index among the active experts (high bits)
+  for (int e = tid; e < E; e += kWG) s_cnt[e] += (s_cnt[e] > 0) << 16;
+  __syncthreads();
+  int* s_cnt0 = s_tmp + 4;  // [E] counts kept for the records
+  for (int e = tid; e < E; e += kWG) s_cnt0[e] = s_cnt[e] & 0xFFFF;
+  const int total = block_exclusive_scan(s_cnt, E, s_tmp);
+  trace_mark(1);
+  for (int e = tid; e < E; e += kWG) {
+    const int c = s_cnt0[e];
+    const int a = s_cnt[e] >> 16;
+    if (c > 0 && a < P.max_act) act[a] = make_int4(e, s_cnt[e] & 0xFFFF, c, 0);
+  }
+  if (tid == 0) s_nact = min(total >> 16, P.max_act);
+  trace_mark(2);
   // slot of selection i: the expert's first slot + the number of earlier
-  // selections of the same expert
+  // selections of the same expert (earlier tokens from the token mask when
+  // a token's experts are distinct, else counted)
   for (int i = tid; i < S; i += kWG) {
     const int e = s_idx[i];
     if (e < 0) {
@@ -352,19 +377,26 @@ __device__ RouteTab build_routing(const Plan& P, const int32_t* __restrict__ idx
       continue;
     }
     int rank = 0;
-    int j = 0;
-    for (; j + 4 <= i; j += 4) {
-      const int4 v = *reinterpret_cast<const int4*>(s_idx + j);
-      rank += (v.x == e) + (v.y == e) + (v.z == e) + (v.w == e);
+    if (distinct) {
+      const int t = i / k;
+      const unsigned lo = s_mask[2 * e], hi = s_mask[2 * e + 1];
+      rank = t < 32 ? __popc(lo & ((1u << t) - 1u)) : __popc(lo) + __popc(hi & ((1u << (t - 32)) - 1u));
+    } else {
+      int j = 0;
+      for (; j + 4 <= i; j += 4) {
+        const int4 v = *reinterpret_cast<const int4*>(s_idx + j);
+        rank += (v.x == e) + (v.y == e) + (v.z == e) + (v.w == e);
+      }
+      for (; j < i; ++j) rank += (s_idx[j] == e);
     }
-    for (; j < i; ++j) rank += (s_idx[j] == e);
-    const int pos = s_cnt[e] + rank;
+    const int pos = min((s_cnt[e] & 0xFFFF) + rank, S - 1);
     slot_tok[pos] = i / k;
     slot_w[pos] = s_w[i];
     slot_e[pos] = e;
     tok_slot[i] = pos;
   }
   __syncthreads();
+  trace_mark(3);
   return {act, slot_tok, slot_w, slot_e, tok_slot, s_nact};
 }
 
@@ -434,7 +466,9 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
     if (tid < k) {
       const int e = sel[tid];
       const double mx = sel[0] >= 0 ? lg[sel[0]] : 0.0;
-      ex[tid] = e >= 0 ? exp(lg[e] - mx) : 0.0;
+      // exp of a non-positive difference; single precision is far inside
+      // the weights' tolerance
+      ex[tid] = e >= 0 ? (double)expf((float)(lg[e] - mx)) : 0.0;
     }
     __syncthreads();
     if (tid < k) {
@@ -834,10 +868,12 @@ struct Routing {
   int e, s0, ne;
 };
 
-// (expert, first slot, slot count) of active expert a
-__device__ __forceinline__ Routing expert_of(const RouteTab& RT, int a) {
+// (expert, first slot, slot count) of active expert a, clamped to the valid
+// ranges so that no table content can address memory outside the layer
+__device__ __forceinline__ Routing expert_of(const Plan& P, const RouteTab& RT, int a) {
   const int4 v = RT.act[a];
-  return {v.x, v.y, v.z};
+  const int s0 = min(max(v.y, 0), P.S);
+  return {min(max(v.x, 0), P.E - 1), s0, min(max(v.z, 0), P.S - s0)};
 }
 
 // Gate/up tile (a, pj, cg, s): 256 output columns of projection pj over
@@ -852,7 +888,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
   const int cg = jt % P.ncg;
   jt /= P.ncg;
   const int pj = jt & 1, a = jt >> 1;
-  const Routing R = expert_of(RT, a);
+  const Routing R = expert_of(P, RT, a);
   const int H = P.H, I = P.I, r = P.r, B = P.B;
   const int KSX = H / 32, KSZ = (r + 31) / 32;
   int ks0, ks1;
@@ -981,7 +1017,7 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
 template <int D>
 __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgx, int s,
                              const uint4* cbs, uint8_t* smem) {
-  const Routing R = expert_of(RT, a);
+  const Routing R = expert_of(P, RT, a);
   const int H = P.H, I = P.I, S = P.S, KS = I / 32;
   const int ks0 = s * KS / P.nsd, ks1 = (s + 1) * KS / P.nsd;
   const int c0 = cgx * kColsPerGroup + (threadIdx.x >> 6) * 64;
@@ -1000,7 +1036,7 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
 __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgr, int s,
                              uint8_t* smem) {
   __shared__ int s_last;
-  const Routing R = expert_of(RT, a);
+  const Routing R = expert_of(P, RT, a);
   const int I = P.I, r = P.r, S = P.S, KS = I / 32, nsdl = P.nsdl;
   const int ks0 = s * KS / nsdl, ks1 = (s + 1) * KS / nsdl;
   const int c0 = cgr * kColsPerGroup + (threadIdx.x >> 6) * 64;
@@ -1207,8 +1243,8 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
   // routing tables at the start of dynamic LDS, item LDS after them
   uint8_t* item_smem = smem + P.lds_routing;
-  const RouteTab RT = (P.flags & F_ROUTE) ? build_routing(P, A.topk_idx, A.topk_w, smem, item_smem)
-                                          : build_routing(P, A.idx_in, A.w_in, smem, item_smem);
+  const RouteTab RT = (P.flags & F_ROUTE) ? build_routing(P, A.topk_idx, A.topk_w, smem, item_smem, true)
+                                          : build_routing(P, A.idx_in, A.w_in, smem, item_smem, false);
   const int nact = RT.nact;
   const int tgu = gateup_tiles_per_expert(P), tdn = down_tiles_per_expert(P);
   const int n_items = nact * (tgu + tdn) + P.n_cb;
