@@ -535,38 +535,46 @@ __device__ __forceinline__ void sched_step() {
   __builtin_amdgcn_sched_group_barrier(0x008, NMFMA, 0);  // MFMA
 }
 
+// Weight streams read through buffer resources: a load whose offset is past
+// the resource's size returns zeros without a memory access, so every
+// pipeline slot is always issued (a static number of loads in flight, hence
+// exact waits) while steps past the end cost no traffic.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOob = 0x80000000u;  // an offset past every resource
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 template <int D, int NOPS, int PD>
 struct VqPipe {
   static constexpr int W = D == 8 ? 1 : 2;
   uint32_t buf[PD][W];
-  const uint8_t* codes;
-  int row_len, col, ks0, nks;
+  rsrc_t rs;
+  uint32_t lane_off, step_bytes, row_len;
+  int ks0, nks;
 
-  // Unconditional, branch-free loads: lanes past n_out read the last valid
-  // columns, whose results are never stored.
-  __device__ __forceinline__ void load(int ks, uint32_t (&b)[W]) {
-    const int g = (threadIdx.x & 63) >> 4;
-    if constexpr (D == 8) {
-      b[0] = *reinterpret_cast<const uint32_t*>(codes + (size_t)(ks * 4 + g) * row_len + col);
-    } else {
-      const size_t row = (size_t)(ks * 8 + 2 * g);
-      b[0] = *reinterpret_cast<const uint32_t*>(codes + row * row_len + col);
-      b[1] = *reinterpret_cast<const uint32_t*>(codes + (row + 1) * row_len + col);
-    }
+  // steps i >= nks read zeros without touching memory
+  __device__ __forceinline__ void load(int i, uint32_t (&b)[W]) {
+    const uint32_t o = i < nks ? lane_off + (uint32_t)(ks0 + i) * step_bytes : kOob;
+    b[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, o, 0, 0);
+    if constexpr (D == 4) b[1] = __builtin_amdgcn_raw_buffer_load_b32(rs, o + row_len, 0, 0);
   }
-  // codes [n_in/d][row_len] of one expert; columns [c0, c0 + 64) of n_out.
-  // Every pipeline slot always holds an issued load (steps past the end
-  // re-read the last step, which is already cached), so the number of loads
-  // in flight is static and the compiler waits for exactly one step.
-  __device__ __forceinline__ void prime(const uint8_t* c, int rl, int c0, int n_out, int k0, int k1) {
-    codes = c;
+  // codes [n_rows][rl] of one expert; columns [c0, c0 + 64) of n_out (lanes
+  // past n_out read the last valid columns, whose results are never stored);
+  // K-steps [k0, k1).
+  __device__ __forceinline__ void prime(const uint8_t* c, int n_rows, int rl, int c0, int n_out, int k0,
+                                        int k1) {
+    rs = make_rsrc(c, (uint32_t)n_rows * rl);
     row_len = rl;
-    col = min(c0 + 4 * (threadIdx.x & 15), n_out - 4);
+    const int g = (threadIdx.x & 63) >> 4;
+    const int col = min(c0 + 4 * (threadIdx.x & 15), n_out - 4);
+    step_bytes = (uint32_t)(32 / D) * rl;
+    lane_off = (uint32_t)(g * (8 / D)) * rl + col;
     ks0 = k0;
     nks = k1 - k0;
-    if (nks <= 0) return;
 #pragma unroll
-    for (int u = 0; u < PD; ++u) load(ks0 + min(u, nks - 1), buf[u]);
+    for (int u = 0; u < PD; ++u) load(u, buf[u]);
   }
   __device__ __forceinline__ void step(int ks, const uint32_t (&b)[W], const uint4* __restrict__ cb_s,
                                        const uint4* __restrict__ ops, int ops_ld, int ops_ks0, int nt,
@@ -602,7 +610,7 @@ struct VqPipe {
       for (int u = 0; u < PD; ++u) {
         const int i = i0 + u;
         if (i < nks) step(ks0 + i, buf[u], cb_s, ops, ops_ld, ops_ks0, nt, acc);
-        load(ks0 + min(i + PD, nks - 1), buf[u]);
+        load(i + PD, buf[u]);
         // keep each step's LDS operand reads inside the step: hoisting them
         // across the unrolled pipeline costs registers, not time
         __builtin_amdgcn_sched_barrier(0);
@@ -624,33 +632,32 @@ __device__ __forceinline__ uint4 dense_w(const uint2 (&b)[8]) {
 template <int NOPS, int PD>
 struct DensePipe {
   uint2 buf[PD][8];
-  const uint16_t* W;
-  int ld, col, k_rows, ks0, nks;
+  rsrc_t rs;
+  uint32_t lane_off, step_bytes, row_bytes;
+  int ks0, nks;
 
-  // Unconditional, branch-free loads: rows past k_rows re-read the last row
-  // (every caller zero-pads the activations of those rows) and lanes past
-  // n_out read the last valid columns, whose results are never stored.
-  __device__ __forceinline__ void load(int ks, uint2 (&b)[8]) {
-    const int g = (threadIdx.x & 63) >> 4;
+  // rows past k_rows and steps i >= nks read zeros without touching memory
+  __device__ __forceinline__ void load(int i, uint2 (&b)[8]) {
+    const uint32_t o = i < nks ? lane_off + (uint32_t)(ks0 + i) * step_bytes : kOob;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int row = min(ks * 32 + 8 * g + e, k_rows - 1);
-      b[e] = *reinterpret_cast<const uint2*>(W + (size_t)row * ld + col);
-    }
+    for (int e = 0; e < 8; ++e)
+      b[e] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rs, o + e * row_bytes, 0, 0));
   }
-  // W [k_rows][ld] row-major bf16; columns [c0, c0 + 64) of n_out. Slots
-  // are always loaded, as in VqPipe.
+  // W [k_rows][ld] row-major bf16; columns [c0, c0 + 64) of n_out (lanes
+  // past n_out read the last valid columns, whose results are never stored);
+  // K-steps [k0, k1).
   __device__ __forceinline__ void prime(const uint16_t* w, int ldw, int c0, int n_out, int kr, int k0,
                                         int k1) {
-    W = w;
-    ld = ldw;
-    col = min(c0 + 4 * (threadIdx.x & 15), n_out - 4);
-    k_rows = kr;
+    rs = make_rsrc(w, (uint32_t)kr * ldw * 2);
+    const int g = (threadIdx.x & 63) >> 4;
+    const int col = min(c0 + 4 * (threadIdx.x & 15), n_out - 4);
+    row_bytes = (uint32_t)ldw * 2;
+    step_bytes = 32 * row_bytes;
+    lane_off = (uint32_t)(8 * g) * row_bytes + (uint32_t)col * 2;
     ks0 = k0;
     nks = k1 - k0;
-    if (nks <= 0) return;
 #pragma unroll
-    for (int u = 0; u < PD; ++u) load(ks0 + min(u, nks - 1), buf[u]);
+    for (int u = 0; u < PD; ++u) load(u, buf[u]);
   }
   __device__ __forceinline__ void step(int ks, const uint2 (&b)[8], const uint4* __restrict__ ops, int ops_ld,
                                        int ops_ks0, int nt, f32x4 acc[4]) {
@@ -678,7 +685,7 @@ struct DensePipe {
       for (int u = 0; u < PD; ++u) {
         const int i = i0 + u;
         if (i < nks) step(ks0 + i, buf[u], ops, ops_ld, ops_ks0, nt, acc);
-        load(ks0 + min(i + PD, nks - 1), buf[u]);
+        load(i + PD, buf[u]);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -912,7 +919,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
   DensePipe<2, kPdDense> lr;
   for (int tg = 0; tg < R.ne; tg += kTokPass) {
     const int nt = min(kTokPass, R.ne - tg);
-    vq.prime(codes, I, c0, I, x0, x1);
+    vq.prime(codes, H / D, I, c0, I, x0, x1);
     lr.prime(V, I, c0, I, r, z0, z1);
     __syncthreads();
     stage_bf16(xs, ldx, nt, (x1 - x0) * 4,
@@ -1024,7 +1031,7 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
   const uint8_t* codes = A.L.codes_down + (size_t)R.e * (I / D) * H;
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
   VqPipe<D, 2, kPdVq> pipe;
-  down_body(P, A, R, ks0, ks1, c0, H, [&]() { pipe.prime(codes, H, c0, H, ks0, ks1); },
+  down_body(P, A, R, ks0, ks1, c0, H, [&]() { pipe.prime(codes, I / D, H, c0, H, ks0, ks1); },
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs + 2 * 256, ps, ld, ks0, nt, acc); },
             [&](int slot) { return dn + (size_t)slot * H; }, smem);
   publish(wsp<int>(A, P.o_dn_done) + R.e * (P.ncgh + 1) + cgx);
