@@ -917,32 +917,63 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
 
   VqPipe<D, 1, kPdVq> vq;
   DensePipe<2, kPdDense> lr;
+  const int n8x = (x1 - x0) * 4, n8z = (z1 - z0) * 4;  // 8-element groups per token row
+  // z rows past r are zero-padded on both operands; r % 8 == 0, so a group
+  // of 8 ranks is either all valid or all padding
+  auto z_group = [&](int t, int jj) -> const float* {
+    const int q = z0 * 32 + 8 * jj;
+    return q < r ? zsrc + ((size_t)pj * B + slot_tok[R.s0 + t]) * r + q : nullptr;
+  };
+  auto put_z = [&](int t, int jj, float4 v0, float4 v1) {
+    const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    uint32_t h[8], lw[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      h[u] = rne_bf16(f[u]);
+      lw[u] = rne_bf16(f[u] - bf(h[u]));
+    }
+    zs[t * ldz + 2 * jj] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                                      h[6] | (h[7] << 16));
+    zs[t * ldz + 2 * jj + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
+                                          lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
+  };
+  constexpr int kRegStage = 2;  // activation groups per thread loaded ahead of the weights
   for (int tg = 0; tg < R.ne; tg += kTokPass) {
     const int nt = min(kTokPass, R.ne - tg);
+    // Activation loads go out before the weight prime: loads complete in
+    // issue order, so waiting for them does not wait for the weights.
+    uint4 xv[kRegStage];
+    float4 zv[kRegStage][2];
+#pragma unroll
+    for (int u = 0; u < kRegStage; ++u) {
+      const int i = threadIdx.x + u * kWG;
+      if (i < nt * n8x)
+        xv[u] = *reinterpret_cast<const uint4*>(A.x + (size_t)slot_tok[R.s0 + tg + i / n8x] * H + x0 * 32 +
+                                                8 * (i % n8x));
+      if (i < nt * n8z) {
+        const float* zp = z_group(tg + i / n8z, i % n8z);
+        zv[u][0] = zp ? ld_dev4(zp) : make_float4(0.f, 0.f, 0.f, 0.f);
+        zv[u][1] = zp ? ld_dev4(zp + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep the activation loads first
     vq.prime(codes, H / D, I, c0, I, x0, x1);
     lr.prime(V, I, c0, I, r, z0, z1);
     __syncthreads();
-    stage_bf16(xs, ldx, nt, (x1 - x0) * 4,
-               [&](int t) { return A.x + (size_t)slot_tok[R.s0 + tg + t] * H + x0 * 32; });
-    if (z1 > z0) {
-      // rank rows past r are zero-padded on both operands
-      const int nz = (z1 - z0) * 32;
-      for (int i = threadIdx.x; i < nt * (nz / 8); i += kWG) {
-        const int t = i / (nz / 8), jj = i % (nz / 8);
-        const float* zr = zsrc + ((size_t)pj * B + slot_tok[R.s0 + tg + t]) * r;
-        uint32_t h[8], lw[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int q = z0 * 32 + 8 * jj + u;
-          const float f = q < r ? zr[q] : 0.0f;
-          h[u] = rne_bf16(f);
-          lw[u] = rne_bf16(f - bf(h[u]));
-        }
-        zs[t * ldz + 2 * jj] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                                          h[6] | (h[7] << 16));
-        zs[t * ldz + 2 * jj + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
-                                              lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
-      }
+    for (int u = 0; u < kRegStage; ++u) {
+      const int i = threadIdx.x + u * kWG;
+      if (i < nt * n8x) xs[(i / n8x) * ldx + i % n8x] = xv[u];
+      if (i < nt * n8z) put_z(i / n8z, i % n8z, zv[u][0], zv[u][1]);
+    }
+    // groups beyond the register stage (many tokens) are loaded here
+    for (int i = threadIdx.x + kRegStage * kWG; i < nt * n8x; i += kWG)
+      xs[(i / n8x) * ldx + i % n8x] = *reinterpret_cast<const uint4*>(
+          A.x + (size_t)slot_tok[R.s0 + tg + i / n8x] * H + x0 * 32 + 8 * (i % n8x));
+    for (int i = threadIdx.x + kRegStage * kWG; i < nt * n8z; i += kWG) {
+      const float* zp = z_group(tg + i / n8z, i % n8z);
+      put_z(i / n8z, i % n8z, zp ? ld_dev4(zp) : make_float4(0.f, 0.f, 0.f, 0.f),
+            zp ? ld_dev4(zp + 4) : make_float4(0.f, 0.f, 0.f, 0.f));
     }
     __syncthreads();
     trace_mark(0);

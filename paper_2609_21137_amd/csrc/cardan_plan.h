@@ -87,12 +87,12 @@ __host__ __device__ inline int lr_step_cost(int d) { return 2 * d; }
 
 // K-steps [k0, k1) of gate/up split s of n over the joint axis of KSX VQ
 // steps and KSZ low-rank steps, balanced by bytes (lr_step_cost).
+// (32-bit arithmetic: 64-bit division is a long software sequence on the GPU;
+// total * n stays far below 2^31 for the supported shapes.)
 __host__ __device__ inline void joint_split(int s, int n, int KSX, int KSZ, int d, int& k0, int& k1) {
   const int wz = lr_step_cost(d);
-  const long total = KSX + (long)KSZ * wz;
-  auto step_at = [&](long c) -> int {
-    return c <= KSX ? (int)c : KSX + (int)((c - KSX + wz - 1) / wz);
-  };
+  const int total = KSX + KSZ * wz;
+  auto step_at = [&](int c) -> int { return c <= KSX ? c : KSX + (c - KSX + wz - 1) / wz; };
   k0 = step_at(s * total / n);
   k1 = step_at((s + 1) * total / n);
 }
