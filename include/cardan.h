@@ -105,7 +105,7 @@ int cardan_abi_version(void);
 const char* cardan_last_error(void);
 
 /* Workspace size in bytes needed by every ws-taking entry point for this
- * shape and batch B. Host-only; no device is touched. */
+ * shape and any batch up to B. Host-only; no device is touched. */
 int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out);
 
 /* Router and gating (paper Sec. 2.1): logits l[t][e] = sum_h x[t][h] *

@@ -74,11 +74,11 @@ constexpr size_t kLdsMax = 96 * 1024;     // dynamic LDS limit of either kernel
 int ks_max(int total, int splits) { return ceil_div(total, splits); }
 
 // Largest x/z staging of a gate/up split (uint4 per token row).
-int gateup_ld(int KSX, int KSZ, int d, int ns) {
+int gateup_ld(int KSX, int KSZ, int ns, int ns_v) {
   int best = 0;
   for (int s = 0; s < ns; ++s) {
     int k0, k1;
-    joint_split(s, ns, KSX, KSZ, d, k0, k1);
+    joint_split(s, ns, ns_v, KSX, KSZ, k0, k1);
     const int x = std::min(k1, KSX) - std::min(k0, KSX);
     const int z = std::max(k1, KSX) - std::max(k0, KSX);
     best = std::max(best, (x * 4 + 1) + (z * 8 + 1));
@@ -102,7 +102,7 @@ size_t lds_route(const Plan& P) {
 // Dynamic LDS of k_expert for a plan.
 size_t lds_expert(const Plan& P) {
   const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KSD = P.I / 32;
-  size_t need = (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.d, P.ns) * 16;
+  size_t need = (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns, P.ns_v) * 16;
   // down: p operand rows + split_sum reduction (2 float4 per thread)
   const int ksd = std::max(ks_max(KSD, P.nsd), ks_max(KSD, P.nsdl));
   need = std::max(need, (size_t)P.nt_max * (ksd * 8 + 1) * 16 + kWG * 2 * 16);
@@ -127,7 +127,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.z_sep = z_sep;
   P.nt_max = std::min(B, kTokPass);
   P.tpc = std::min(kTokPass, ceil_div(B, 4));
-  const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KS = KSX + KSZ, KSD = P.I / 32;
+  const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KSD = P.I / 32;
   P.nch_z = std::max(1, KSX / 2);                  // two K-steps of U per z unit
   // Tile sizes: the expected active experts' weight bytes spread over a
   // nominal grid of 512 workgroups (2 per CU), kept between 16 and 64 KB per
@@ -141,7 +141,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // A VQ down K-step costs twice a gate/up one (p enters as hi + lo), so its
   // bytes count double. While the expected items exceed the nominal grid
   // the tile grows (small batches then run in one round).
-  double tile = fmin(64.0 * 1024, fmax(16.0 * 1024, exp_act * per_expert / 512.0));
+  double tile = fmin(128.0 * 1024, fmax(16.0 * 1024, exp_act * per_expert / 512.0));
   auto splits = [&](double bytes, int max_splits) {
     return std::max(1, std::min(max_splits, (int)lround(bytes / tile)));
   };
@@ -149,14 +149,24 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.ncgh = ceil_div(P.H, kColsPerGroup);
   P.ncgr = ceil_div(P.r, kColsPerGroup);
   for (;;) {
-    P.ns = splits(256.0 * (KSX * 32 / P.d) + 256.0 * P.r * 2, KS);
+    // code splits and low-rank splits of a gate/up (expert, 256 columns)
+    P.ns_v = splits(256.0 * (KSX * 32 / P.d), KSX);
+    P.ns = P.ns_v + (KSZ > 0 ? splits(256.0 * P.r * 2, KSZ) : 0);
     P.nsd = splits(2.0 * 256.0 * P.I / P.d, KSD);
     P.nsdl = P.r > 0 ? splits((double)std::min(P.r, kColsPerGroup) * P.I * 2, KSD) : 1;
     const double items = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
-    if (items <= 512.0 || tile >= 64.0 * 1024) break;
+    if (items <= 512.0 || tile >= 128.0 * 1024) break;
     tile *= 1.05;
   }
-  while (P.ns < KS && (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.d, P.ns) * 16 > kLdsBudget) ++P.ns;
+  // token rows staged per pass: halve (down to 4) before splitting K further
+  // to fit the operand staging into LDS; experts with more tokens than one
+  // pass stream their weights again per pass (rare at these sizes)
+  while (P.nt_max > 4 && (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns, P.ns_v) * 16 > kLdsBudget)
+    P.nt_max = (P.nt_max + 1) / 2;
+  while (P.ns_v < KSX && (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns, P.ns_v) * 16 > kLdsBudget) {
+    ++P.ns_v;
+    ++P.ns;
+  }
   auto down_fits = [&](int n) {
     return (size_t)P.nt_max * (ks_max(KSD, n) * 8 + 1) * 16 + kWG * 2 * 16 <= kLdsBudget;
   };
@@ -352,7 +362,12 @@ int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out) {
   int rc = check_shape(shape, B);
   if (rc) return rc;
   if (!out) return fail(CARDAN_ERR_NULL_PTR, "out is NULL");
-  *out = make_plan(shape, B, 1, F_ROUTE | F_Z | F_GROUP | F_EXPERTS).total;
+  // the largest layout over batches 1..B, so one workspace serves any batch
+  // up to B (split counts, hence layouts, depend on the batch)
+  size_t need = 0;
+  for (int b = 1; b <= B; ++b)
+    need = std::max(need, make_plan(shape, b, 1, F_ROUTE | F_Z | F_GROUP | F_EXPERTS).total);
+  *out = need;
   return CARDAN_OK;
 }
 

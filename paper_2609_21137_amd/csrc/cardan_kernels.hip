@@ -888,18 +888,13 @@ __device__ __forceinline__ Routing expert_of(const Plan& P, const RouteTab& RT, 
 // VQ gather sum and V^T z accumulate in the same MFMA accumulators. Each
 // tile writes its partial sums.
 template <int D>
-__device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, int jt, const uint4* cbs,
-                            uint8_t* smem) {
-  const int s = jt % P.ns;
-  jt /= P.ns;
-  const int cg = jt % P.ncg;
-  jt /= P.ncg;
-  const int pj = jt & 1, a = jt >> 1;
+__device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg, int s,
+                            const uint4* cbs, uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);
   const int H = P.H, I = P.I, r = P.r, B = P.B;
   const int KSX = H / 32, KSZ = (r + 31) / 32;
   int ks0, ks1;
-  joint_split(s, P.ns, KSX, KSZ, D, ks0, ks1);
+  joint_split(s, P.ns, P.ns_v, KSX, KSZ, ks0, ks1);
   const int x0 = min(ks0, KSX), x1 = min(ks1, KSX);
   const int z0 = max(ks0, KSX) - KSX, z1 = max(ks1, KSX) - KSX;
   const int w = threadIdx.x >> 6;
@@ -938,8 +933,8 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
                                           lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
   };
   constexpr int kRegStage = 2;  // activation groups per thread loaded ahead of the weights
-  for (int tg = 0; tg < R.ne; tg += kTokPass) {
-    const int nt = min(kTokPass, R.ne - tg);
+  for (int tg = 0; tg < R.ne; tg += P.nt_max) {
+    const int nt = min(P.nt_max, R.ne - tg);
     // Activation loads go out before the weight prime: loads complete in
     // issue order, so waiting for them does not wait for the weights.
     uint4 xv[kRegStage];
@@ -1037,8 +1032,8 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
   const int ld = (ks1 - ks0) * 8 + 1;
   uint4* ps = reinterpret_cast<uint4*>(smem);
   const float* pbuf = wsp<const float>(A, P.o_p);
-  for (int tg = 0; tg < R.ne; tg += kTokPass) {
-    const int nt = min(kTokPass, R.ne - tg);
+  for (int tg = 0; tg < R.ne; tg += P.nt_max) {
+    const int nt = min(P.nt_max, R.ne - tg);
     if (tg > 0) prime();
     __syncthreads();
     stage_split(ps, ld, nt, (ks1 - ks0) * 4,
@@ -1202,6 +1197,41 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
       });
 }
 
+// Gate/up tile of position p. The tiles of splits s < s_vq read codes (LDS
+// code-book lookups bound the CU), the others only coefficients (HBM bound).
+// Workgroups b and b + G/2 share a CU when two are resident per CU, so code
+// tiles take the first half of every grid-sized round of positions and
+// coefficient tiles the second, each class in its natural (expert, gate|up,
+// column group, split) order; once one class runs out the other fills every
+// position. Gate/up tiles wait for nothing, so any order is deadlock-free.
+struct GateUpTile {
+  int a, pj, cg, s;
+};
+__device__ __forceinline__ GateUpTile gateup_at(const Plan& P, int p, int nact, int s_vq, int G) {
+  const int half = G >> 1;
+  const int n_v = nact * 2 * P.ncg * s_vq, n_l = nact * 2 * P.ncg * (P.ns - s_vq);
+  const int r = p / G, w = p - r * G;
+  const int v = r * half + min(w, half);  // code-preferring positions before p
+  const int l = p - v;                     // coefficient-preferring positions before p
+  // tiles of each class handed out before p (at most one class runs out)
+  int cv = v, cl = l;
+  if (v > n_v) {
+    cv = n_v;
+    cl = p - n_v;
+  } else if (l > n_l) {
+    cl = n_l;
+    cv = p - n_l;
+  }
+  const bool code = w < half ? cv < n_v : !(cl < n_l);
+  int i = code ? cv : cl;
+  const int nsc = code ? s_vq : P.ns - s_vq;
+  const int s = i % nsc + (code ? 0 : s_vq);
+  i /= nsc;
+  const int cg = i % P.ncg;
+  i /= P.ncg;
+  return {i >> 1, i & 1, cg, s};
+}
+
 // ===========================================================================
 // the two persistent kernels of a layer call
 // ===========================================================================
@@ -1281,17 +1311,22 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
   // routing tables at the start of dynamic LDS, item LDS after them
   uint8_t* item_smem = smem + P.lds_routing;
+  ItemTrace tr_route;
   const RouteTab RT = (P.flags & F_ROUTE) ? build_routing(P, A.topk_idx, A.topk_w, smem, item_smem, true)
                                           : build_routing(P, A.idx_in, A.w_in, smem, item_smem, false);
+  tr_route.done(A, P, P.n_pre + P.max_act * (gateup_tiles_per_expert(P) + down_tiles_per_expert(P)) + P.n_cb +
+                          blockIdx.x, 8);
   const int nact = RT.nact;
   const int tgu = gateup_tiles_per_expert(P), tdn = down_tiles_per_expert(P);
+  const int s_vq = P.ns_v;  // first gate/up split without code steps
   const int n_items = nact * (tgu + tdn) + P.n_cb;
   for (int jp = blockIdx.x; jp < n_items; jp += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
     int j = jp, kind = 4;
     if (j < nact * tgu) {
-      item_gateup<D>(P, A, RT, j, cbs, item_smem);
+      const GateUpTile t = gateup_at(P, j, nact, s_vq, gridDim.x);
+      item_gateup<D>(P, A, RT, t.a, t.pj, t.cg, t.s, cbs, item_smem);
     } else if ((j -= nact * tgu) < nact * tdn) {
       const int a = j / tdn, rem = j % tdn, nvq = P.ncgh * P.nsd;
       if (rem < nvq) {

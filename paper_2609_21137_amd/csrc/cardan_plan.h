@@ -58,11 +58,12 @@ struct Plan {
   int z_sep;      // 1 when U_up is a different array from U_gate
   int ncg;        // gate/up column groups (I / 256, rounded up)
   int ns;         // gate/up splits of the joint K axis (H/32 + ceil(r/32) steps)
+  int ns_v;       // of which splits over the code steps (the rest: low-rank steps)
   int ncgh;       // VQ down column groups (H / 256, rounded up)
   int ncgr;       // low-rank down column groups (r / 256, rounded up)
   int nsd;        // VQ down splits of the I K-steps
   int nsdl;       // low-rank down splits of the I K-steps
-  int nt_max;     // most token slots one expert tile stages (min(B, 16))
+  int nt_max;     // token slots an expert tile stages per pass (<= 16; more run in passes)
   int tpc;        // tokens per combine tile
   int n_cb;       // combine tiles
   // item counts of this call
@@ -80,21 +81,18 @@ __host__ __device__ inline int down_tiles_per_expert(const Plan& P) {
   return P.ncgh * P.nsd + P.ncgr * P.nsdl;
 }
 
-// Cost of one low-rank K-step of a gate/up tile relative to one VQ K-step:
-// a wave reads 64 x 32/d code bytes per VQ step and 32 x 64 bf16 (4 KB) per
-// low-rank step.
-__host__ __device__ inline int lr_step_cost(int d) { return 2 * d; }
-
-// K-steps [k0, k1) of gate/up split s of n over the joint axis of KSX VQ
-// steps and KSZ low-rank steps, balanced by bytes (lr_step_cost).
-// (32-bit arithmetic: 64-bit division is a long software sequence on the GPU;
-// total * n stays far below 2^31 for the supported shapes.)
-__host__ __device__ inline void joint_split(int s, int n, int KSX, int KSZ, int d, int& k0, int& k1) {
-  const int wz = lr_step_cost(d);
-  const int total = KSX + KSZ * wz;
-  auto step_at = [&](int c) -> int { return c <= KSX ? c : KSX + (c - KSX + wz - 1) / wz; };
-  k0 = step_at(s * total / n);
-  k1 = step_at((s + 1) * total / n);
+// K-steps [k0, k1) of gate/up split s over the joint axis of KSX code steps
+// and KSZ low-rank steps: splits s < ns_v divide the code steps evenly, the
+// remaining ns - ns_v splits divide the low-rank steps.
+__host__ __device__ inline void joint_split(int s, int ns, int ns_v, int KSX, int KSZ, int& k0, int& k1) {
+  if (s < ns_v) {
+    k0 = s * KSX / ns_v;
+    k1 = (s + 1) * KSX / ns_v;
+  } else {
+    const int nl = ns - ns_v, sl = s - ns_v;
+    k0 = KSX + sl * KSZ / nl;
+    k1 = KSX + (sl + 1) * KSZ / nl;
+  }
 }
 
 // Device pointers of one call.
