@@ -154,8 +154,10 @@ int cardan_rmsnorm_bf16(int32_t B, int32_t H, const float* y, float eps,
                         cardan_bf16* x_next, hipStream_t stream);
 
 /* Kernel timing for measurement. cardan_profile_begin(n) makes the next n
- * calls record a HIP event pair around each kernel they launch, on the
- * call's stream; cardan_profile_end() waits for those events and writes, per
+ * calls launch each kernel with a HIP start/stop event pair recorded by the
+ * dispatch itself (hipExtLaunchKernel), on the call's stream, so the pair
+ * brackets the kernel's execution; cardan_profile_end() waits for those
+ * events and writes, per
  * kernel kind, the summed milliseconds and the launch count (arrays of
  * length CARDAN_PROFILE_KINDS, ordered as the enum below). A layer call runs
  * the routing kernel (routing, shared projections, grouping) and then the

@@ -16,10 +16,10 @@
 namespace cardan {
 const void* route_kernel();
 const void* expert_kernel(int d);
-hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t);
-hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t);
+hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
+hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t);
-hipError_t launch_rmsnorm(hipStream_t, int, int, const float*, float, uint16_t*);
+hipError_t launch_rmsnorm(hipStream_t, int, int, const float*, float, uint16_t*, hipEvent_t, hipEvent_t);
 }  // namespace cardan
 
 using namespace cardan;
@@ -282,21 +282,23 @@ struct Profiler {
 };
 Profiler g_prof;
 
+// Event pair of the next launch of `kind` while profiling (else nulls): the
+// launch records them as part of the kernel's dispatch, so they bracket the
+// kernel itself.
 struct Timed {
-  hipStream_t st;
-  int kind;
-  bool rec;
-  Timed(hipStream_t s, int k) : st(s), kind(k), rec(false) {
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  size_t slot = 0;
+  Timed(hipStream_t, int kind) {
     if (g_prof.on && g_prof.calls < g_prof.cap) {
-      const size_t i = (size_t)g_prof.calls * CARDAN_PROFILE_KINDS + kind;
-      if (!g_prof.used[i] && hipEventRecord(g_prof.ev[2 * i], st) == hipSuccess) rec = true;
+      slot = (size_t)g_prof.calls * CARDAN_PROFILE_KINDS + kind;
+      if (!g_prof.used[slot]) {
+        ev0 = g_prof.ev[2 * slot];
+        ev1 = g_prof.ev[2 * slot + 1];
+      }
     }
   }
   void done() {
-    if (rec) {
-      const size_t i = (size_t)g_prof.calls * CARDAN_PROFILE_KINDS + kind;
-      if (hipEventRecord(g_prof.ev[2 * i + 1], st) == hipSuccess) g_prof.used[i] = 1;
-    }
+    if (ev0) g_prof.used[slot] = 1;
   }
 };
 
@@ -321,7 +323,7 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
     const int cap = resident_grid(route_kernel(), P.lds_route, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_ROUTE);
-    err = launch_route(P, A, std::max(1, std::min(cap, P.n_pre)), P.lds_route, stream);
+    err = launch_route(P, A, std::max(1, std::min(cap, P.n_pre)), P.lds_route, stream, tm.ev0, tm.ev1);
     if (err != hipSuccess) return hip_fail(err, "k_route launch");
     tm.done();
     if (!(P.flags & F_EXPERTS)) {  // k_expert would clear these counters
@@ -333,7 +335,7 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
     const int cap = resident_grid(expert_kernel(P.d), P.lds_expert, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_EXPERT);
-    err = launch_expert(P, A, cap, P.lds_expert, stream);
+    err = launch_expert(P, A, cap, P.lds_expert, stream, tm.ev0, tm.ev1);
     if (err != hipSuccess) return hip_fail(err, "k_expert launch");
     tm.done();
   }
@@ -475,7 +477,7 @@ int cardan_rmsnorm_bf16(int32_t B, int32_t H, const float* y, float eps, cardan_
   REQ(y, "y");
   REQ(x_next, "x_next");
   Timed tm(stream, CARDAN_KERNEL_RMSNORM);
-  hipError_t e = launch_rmsnorm(stream, B, H, y, eps, x_next);
+  hipError_t e = launch_rmsnorm(stream, B, H, y, eps, x_next, tm.ev0, tm.ev1);
   if (e != hipSuccess) return hip_fail(e, "rmsnorm launch");
   tm.done();
   prof_next_call();

@@ -20,6 +20,7 @@
 // enter the same accumulators as dense bf16 operands, which makes the VQ sum
 // and V^T z one float32 accumulation before the activation (Sec. 4.2, joint
 // accumulation).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -1371,8 +1372,20 @@ const void* expert_kernel(int d) {
                 : reinterpret_cast<const void*>(&k_expert<4>);
 }
 
-hipError_t launch_route(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st) {
-  hipLaunchKernelGGL(k_route, dim3(grid), dim3(kWG), lds, st, P, A);
+// With a start/stop event pair the launch records them as part of the
+// dispatch itself (the kernel's own begin and end), else a plain launch.
+#define CARDAN_LAUNCH(kernel, grid, lds, st, ev0, ev1, ...)                                        \
+  do {                                                                                            \
+    if (ev0)                                                                                      \
+      hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(kWG), (uint32_t)(lds), st, ev0, ev1, 0,     \
+                            __VA_ARGS__);                                                         \
+    else                                                                                          \
+      hipLaunchKernelGGL(kernel, dim3(grid), dim3(kWG), lds, st, __VA_ARGS__);                    \
+  } while (0)
+
+hipError_t launch_route(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st, hipEvent_t ev0,
+                        hipEvent_t ev1) {
+  CARDAN_LAUNCH(k_route, grid, lds, st, ev0, ev1, P, A);
   return hipGetLastError();
 }
 
@@ -1381,16 +1394,21 @@ hipError_t launch_route_reset(const Plan& P, const Args& A, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_expert(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st) {
+hipError_t launch_expert(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st, hipEvent_t ev0,
+                         hipEvent_t ev1) {
   if (P.d == 8)
-    hipLaunchKernelGGL(k_expert<8>, dim3(grid), dim3(kWG), lds, st, P, A);
+    CARDAN_LAUNCH(k_expert<8>, grid, lds, st, ev0, ev1, P, A);
   else
-    hipLaunchKernelGGL(k_expert<4>, dim3(grid), dim3(kWG), lds, st, P, A);
+    CARDAN_LAUNCH(k_expert<4>, grid, lds, st, ev0, ev1, P, A);
   return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm(hipStream_t st, int B, int H, const float* y, float eps, uint16_t* xn) {
-  hipLaunchKernelGGL(k_rmsnorm, dim3(B), dim3(kWG), 0, st, H, y, eps, xn);
+hipError_t launch_rmsnorm(hipStream_t st, int B, int H, const float* y, float eps, uint16_t* xn, hipEvent_t ev0,
+                          hipEvent_t ev1) {
+  if (ev0)
+    hipExtLaunchKernelGGL(k_rmsnorm, dim3(B), dim3(kWG), 0, st, ev0, ev1, 0, H, y, eps, xn);
+  else
+    hipLaunchKernelGGL(k_rmsnorm, dim3(B), dim3(kWG), 0, st, H, y, eps, xn);
   return hipGetLastError();
 }
 
