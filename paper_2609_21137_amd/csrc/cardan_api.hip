@@ -150,8 +150,13 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.ncgr = ceil_div(P.r, kColsPerGroup);
   for (;;) {
     // code splits and low-rank splits of a gate/up (expert, 256 columns)
-    P.ns_v = splits(256.0 * (KSX * 32 / P.d), KSX);
-    P.ns = P.ns_v + (KSZ > 0 ? splits(256.0 * P.r * 2, KSZ) : 0);
+    const double code_bytes = 256.0 * (KSX * 32 / P.d), lr_bytes = 256.0 * P.r * 2;
+    if (tile >= 0.75 * (code_bytes + lr_bytes)) {
+      P.ns_v = P.ns = 1;  // one tile holds the whole joint axis
+    } else {
+      P.ns_v = splits(code_bytes, KSX);
+      P.ns = P.ns_v + (KSZ > 0 ? splits(lr_bytes, KSZ) : 0);
+    }
     P.nsd = splits(2.0 * 256.0 * P.I / P.d, KSD);
     P.nsdl = P.r > 0 ? splits((double)std::min(P.r, kColsPerGroup) * P.I * 2, KSD) : 1;
     const double items = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
@@ -164,8 +169,11 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   while (P.nt_max > 4 && (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns, P.ns_v) * 16 > kLdsBudget)
     P.nt_max = (P.nt_max + 1) / 2;
   while (P.ns_v < KSX && (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns, P.ns_v) * 16 > kLdsBudget) {
-    ++P.ns_v;
-    ++P.ns;
+    if (P.ns == P.ns_v && KSZ > 0) ++P.ns;  // give the low-rank steps their own split first
+    else {
+      ++P.ns_v;
+      ++P.ns;
+    }
   }
   auto down_fits = [&](int n) {
     return (size_t)P.nt_max * (ks_max(KSD, n) * 8 + 1) * 16 + kWG * 2 * 16 <= kLdsBudget;

@@ -732,21 +732,35 @@ __device__ __forceinline__ void stage_bf16(uint4* ops, int ld, int nt, int n8, F
 // inputs 8 j .. 8 j + 7 of row src(t), value = hi + lo.
 template <typename F>
 __device__ __forceinline__ void stage_split(uint4* ops, int ld, int nt, int n8, F src) {
-  for (int i = threadIdx.x; i < nt * n8; i += kWG) {
-    const int t = i / n8, j = i % n8;
-    const float* p = src(t) + 8 * j;
-    const float4 v0 = ld_dev4(p), v1 = ld_dev4(p + 4);
-    const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-    uint32_t h[8], lw[8];
+  // four groups per thread per round, their loads in flight together
+  for (int i0 = threadIdx.x; i0 < nt * n8; i0 += 4 * kWG) {
+    float4 v[4][2];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      h[u] = rne_bf16(f[u]);
-      lw[u] = rne_bf16(f[u] - bf(h[u]));
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kWG;
+      if (i < nt * n8) {
+        const float* p = src(i / n8) + 8 * (i % n8);
+        v[u][0] = ld_dev4(p);
+        v[u][1] = ld_dev4(p + 4);
+      }
     }
-    ops[t * ld + 2 * j] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                                     h[6] | (h[7] << 16));
-    ops[t * ld + 2 * j + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
-                                         lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kWG;
+      if (i >= nt * n8) continue;
+      const int t = i / n8, j = i % n8;
+      const float f[8] = {v[u][0].x, v[u][0].y, v[u][0].z, v[u][0].w, v[u][1].x, v[u][1].y, v[u][1].z, v[u][1].w};
+      uint32_t h[8], lw[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        h[e] = rne_bf16(f[e]);
+        lw[e] = rne_bf16(f[e] - bf(h[e]));
+      }
+      ops[t * ld + 2 * j] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                                       h[6] | (h[7] << 16));
+      ops[t * ld + 2 * j + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
+                                           lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
+    }
   }
 }
 
@@ -890,7 +904,7 @@ __device__ __forceinline__ Routing expert_of(const Plan& P, const RouteTab& RT, 
 // tile writes its partial sums.
 template <int D>
 __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg, int s,
-                            const uint4* cbs, uint8_t* smem) {
+                            bool lr_first, const uint4* cbs, uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);
   const int H = P.H, I = P.I, r = P.r, B = P.B;
   const int KSX = H / 32, KSZ = (r + 31) / 32;
@@ -962,22 +976,46 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
       if (i < nt * n8x) xs[(i / n8x) * ldx + i % n8x] = xv[u];
       if (i < nt * n8z) put_z(i / n8z, i % n8z, zv[u][0], zv[u][1]);
     }
-    // groups beyond the register stage (many tokens) are loaded here
-    for (int i = threadIdx.x + kRegStage * kWG; i < nt * n8x; i += kWG)
-      xs[(i / n8x) * ldx + i % n8x] = *reinterpret_cast<const uint4*>(
-          A.x + (size_t)slot_tok[R.s0 + tg + i / n8x] * H + x0 * 32 + 8 * (i % n8x));
-    for (int i = threadIdx.x + kRegStage * kWG; i < nt * n8z; i += kWG) {
-      const float* zp = z_group(tg + i / n8z, i % n8z);
-      put_z(i / n8z, i % n8z, zp ? ld_dev4(zp) : make_float4(0.f, 0.f, 0.f, 0.f),
-            zp ? ld_dev4(zp + 4) : make_float4(0.f, 0.f, 0.f, 0.f));
+    // groups beyond the register stage (many tokens): batches of 4 per
+    // thread with their loads in flight together
+    for (int i0 = threadIdx.x + kRegStage * kWG; i0 < nt * n8x; i0 += 4 * kWG) {
+      uint4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * kWG;
+        if (i < nt * n8x)
+          v[u] = *reinterpret_cast<const uint4*>(A.x + (size_t)slot_tok[R.s0 + tg + i / n8x] * H + x0 * 32 +
+                                                 8 * (i % n8x));
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * kWG;
+        if (i < nt * n8x) xs[(i / n8x) * ldx + i % n8x] = v[u];
+      }
+    }
+    for (int i0 = threadIdx.x + kRegStage * kWG; i0 < nt * n8z; i0 += 2 * kWG) {
+      float4 v[2][2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int i = i0 + u * kWG;
+        const float* zp = i < nt * n8z ? z_group(tg + i / n8z, i % n8z) : nullptr;
+        v[u][0] = zp ? ld_dev4(zp) : make_float4(0.f, 0.f, 0.f, 0.f);
+        v[u][1] = zp ? ld_dev4(zp + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int i = i0 + u * kWG;
+        if (i < nt * n8z) put_z(i / n8z, i % n8z, v[u][0], v[u][1]);
+      }
     }
     __syncthreads();
     trace_mark(0);
     f32x4 acc[4];
     zero_acc(acc);
+    if (lr_first) lr.run(zs, ldz, z0, nt, acc);
     vq.run(cb, xs, ldx, x0, nt, acc);
     trace_mark(1);
-    lr.run(zs, ldz, z0, nt, acc);
+    if (!lr_first) lr.run(zs, ldz, z0, nt, acc);
     store_acc(acc, nt, c0, I, [&](int t) { return gu + (((size_t)(R.s0 + tg + t) * 2 + pj) * P.ns + s) * I; });
     trace_mark(2);
   }
@@ -1327,7 +1365,11 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     int j = jp, kind = 4;
     if (j < nact * tgu) {
       const GateUpTile t = gateup_at(P, j, nact, s_vq, gridDim.x);
-      item_gateup<D>(P, A, RT, t.a, t.pj, t.cg, t.s, cbs, item_smem);
+      // a tile holding both code and low-rank steps runs the low-rank part
+      // first in the second half of the grid, so the two workgroups sharing
+      // a CU overlap LDS-bound and HBM-bound phases
+      const bool lr_first = (int)(jp % gridDim.x) >= (int)(gridDim.x >> 1);
+      item_gateup<D>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem);
     } else if ((j -= nact * tgu) < nact * tdn) {
       const int a = j / tdn, rem = j % tdn, nvq = P.ncgh * P.nsd;
       if (rem < nvq) {

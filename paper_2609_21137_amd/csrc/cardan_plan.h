@@ -83,11 +83,13 @@ __host__ __device__ inline int down_tiles_per_expert(const Plan& P) {
 
 // K-steps [k0, k1) of gate/up split s over the joint axis of KSX code steps
 // and KSZ low-rank steps: splits s < ns_v divide the code steps evenly, the
-// remaining ns - ns_v splits divide the low-rank steps.
+// remaining ns - ns_v splits divide the low-rank steps (with none left, the
+// last code split also takes the low-rank steps).
 __host__ __device__ inline void joint_split(int s, int ns, int ns_v, int KSX, int KSZ, int& k0, int& k1) {
   if (s < ns_v) {
     k0 = s * KSX / ns_v;
     k1 = (s + 1) * KSX / ns_v;
+    if (s == ns_v - 1 && ns == ns_v) k1 = KSX + KSZ;
   } else {
     const int nl = ns - ns_v, sl = s - ns_v;
     k0 = KSX + sl * KSZ / nl;
