@@ -35,7 +35,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="qwen3_30b_a3b_moe_layer_b1")
-    ap.add_argument("--also", default="qwen3_30b_a3b_moe_layer_b16,wide_h4096_i1536_e64_top6_b4_skewed",
+    ap.add_argument("--also", default="qwen3_30b_a3b_moe_layer_b16,wide_h4096_i1536_e64_top6_b4_skewed,"
+                    "qwen3_48_layer_decode_step_b16",
                     help="comma-separated extra workloads timed the same way (reported under 'also')")
     ap.add_argument("--layers", type=int, default=8, help="independently seeded layers rotated")
     ap.add_argument("--inputs", type=int, default=64,
@@ -172,6 +173,89 @@ def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache):
             "mean_active": float(np.mean(acts)), "layers": n_layers, "inputs": n_inputs}
 
 
+def time_decode_step(C, torch, w, steps, warmup, n_distinct, layers_cache):
+    """The stacked-layer decode step: w.layers MoE layers, each layer's output
+    RMS-normalised (bf16) into the next layer's input. The layers cycle over
+    `n_distinct` independently seeded layers (every layer holds all E experts,
+    so the weights touched per step exceed the last-level cache). The step is
+    captured once as a HIP graph and replayed; eager timing is the fallback."""
+    import ctypes
+
+    from paper_2609_21137_amd import synth
+    shape = C.shape_of(w)
+    key = (w.H, w.I, w.E, w.d, w.K, w.r, w.seed, w.hot_experts, w.hot_bias)
+    if key not in layers_cache:
+        layers_cache.clear()
+        torch.cuda.empty_cache()
+        layers_cache[key] = [C.DeviceLayer.from_numpy(synth.workload_layer(w, li))
+                             for li in range(n_distinct)]
+    dls = layers_cache[key][:n_distinct]
+    n_distinct = len(dls)
+    structs = [dl.struct() for dl in dls]
+    B, L = w.B, w.layers
+    x0 = C.bf16_tensor(synth.workload_input(w, 0))
+    xa = torch.empty_like(x0)
+    xb = torch.empty_like(x0)
+    y = torch.empty((B, w.H), dtype=torch.float32, device="cuda")
+    idx = torch.empty((L, B, w.top_k), dtype=torch.int32, device="cuda")
+    wt = torch.empty((L, B, w.top_k), dtype=torch.float32, device="cuda")
+    ws = C.new_workspace(shape, B)
+    lib = C.lib()
+
+    def one_step(stream):
+        st = ctypes.c_void_p(stream)
+        xin = x0
+        for li in range(L):
+            xout = xa if li % 2 == 0 else xb
+            rc = lib.cardan_moe_layer(ctypes.byref(shape), B, ctypes.c_void_p(xin.data_ptr()),
+                                      ctypes.byref(structs[li % n_distinct]),
+                                      ctypes.c_void_p(y.data_ptr()),
+                                      ctypes.c_void_p(idx[li].data_ptr()),
+                                      ctypes.c_void_p(wt[li].data_ptr()),
+                                      ctypes.c_void_p(ws.data_ptr()), ws.numel(), st)
+            if rc != 0:
+                raise RuntimeError(lib.cardan_last_error().decode())
+            rc = lib.cardan_rmsnorm_bf16(B, w.H, ctypes.c_void_p(y.data_ptr()), ctypes.c_float(1e-6),
+                                         ctypes.c_void_p(xout.data_ptr()), st)
+            if rc != 0:
+                raise RuntimeError(lib.cardan_last_error().decode())
+            xin = xout
+
+    stream = torch.cuda.current_stream().cuda_stream
+    for _ in range(max(1, warmup)):
+        one_step(stream)
+    torch.cuda.synchronize()
+    n_act = [len(np.unique(idx[li].cpu().numpy())) for li in range(L)]
+    mode = "hip_graph"
+    try:
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                one_step(torch.cuda.current_stream().cuda_stream)
+        torch.cuda.current_stream().wait_stream(s)
+        g.replay()
+        torch.cuda.synchronize()
+        run = g.replay
+    except Exception as e:  # capture unsupported here: time the eager launches
+        print(f"[bench] graph capture failed ({e}); timing eager launches", file=sys.stderr)
+        mode = "eager"
+        run = lambda: one_step(stream)  # noqa: E731
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    bytes_step = sum(compressed_bytes(w, a)["compressed"] for a in n_act)
+    return {"workload": w.name, "B": B, "layers": L, "distinct_layers": n_distinct, "mode": mode,
+            "ms_per_step": round(1e3 * wall / steps, 4),
+            "us_per_layer": round(1e6 * wall / steps / L, 3),
+            "GBps": round(bytes_step * steps / wall / 1e9, 2),
+            "mean_active_experts": float(np.mean(n_act))}
+
+
 def cpu_baseline(w, budget_s):
     """The float64 oracle timed on this host's cores on a bounded sample."""
     import threadpoolctl
@@ -305,6 +389,11 @@ def main():
     also = []
     for name in [s for s in args.also.split(",") if s]:
         ww = WORKLOADS[name]
+        if ww.layers > 1:
+            print(f"[bench] {ww.name}: {ww.layers}-layer decode step", file=sys.stderr, flush=True)
+            also.append(time_decode_step(C, torch, ww, max(5, args.steps // 10), 2, args.layers, cache))
+            print(f"[bench] {ww.name}: {also[-1]['ms_per_step']} ms/step", file=sys.stderr, flush=True)
+            continue
         print(f"[bench] {ww.name}", file=sys.stderr, flush=True)
         rr = time_workload(C, torch, ww, args.steps, args.warmup, args.layers, args.inputs, cache)
         also.append(summarize(ww, rr, src_hash))
