@@ -92,7 +92,7 @@ size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
 size_t lds_route(const Plan& P) {
   const int KSX = P.H / 32;
   size_t need = (size_t)kTokPass * kRowsRouter * (4 + 4 * 8);          // router chunk
-  need = std::max(need, (size_t)kMaxE * (8 + 4) + kMaxK * (8 + 4));    // select
+  need = std::max(need, (size_t)kMaxE * 8 + kMaxK * (8 + 8 + 4 + 4) + (size_t)kWG * 8);  // select
   need = std::max(need, (size_t)(kMaxB * kMaxK + 2 * kMaxE + 4) * 4);   // grouping
   if (P.flags & F_Z)
     need = std::max(need, (size_t)4 * kTokPass * (ks_max(KSX, P.nch_z) * 4 + 1) * 16);
@@ -106,9 +106,7 @@ size_t lds_expert(const Plan& P) {
   // down: p operand rows + split_sum reduction (2 float4 per thread)
   const int ksd = std::max(ks_max(KSD, P.nsd), ks_max(KSD, P.nsdl));
   need = std::max(need, (size_t)P.nt_max * (ksd * 8 + 1) * 16 + kWG * 2 * 16);
-  // combine: routing of the tokens, reduction, B^T u rows, u operand rows
-  need = std::max(need, (size_t)3 * kTokPass * kMaxK * 4 + kWG * 16 + (size_t)kTokPass * kColsPerGroup * 4 +
-                            (size_t)P.tpc * (KSZ * 8 + 1) * 16);
+  need = std::max(need, combine_lds(P));
   return round256(need);
 }
 
@@ -198,7 +196,6 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.o_zc_flag = o; o = align256(o + (size_t)P.n_zc_flags * 4);
   P.o_gu_tick = o; o = align256(o + (size_t)P.E * ceil_div(P.I, kColsPerGroup) * 4);
   P.o_gu_done = o; o = align256(o + (size_t)P.E * 4);
-  P.o_lr_tick = o; o = align256(o + (size_t)P.E * 4);
   P.o_dn_done = o; o = align256(o + (size_t)P.E * (ceil_div(P.H, kColsPerGroup) + 1) * 4);
   P.o_rl = o; o = align256(o + (size_t)P.nch_r * B * P.E * 8);
   P.o_zp = o; o = align256(o + (size_t)2 * P.nch_z * B * P.r * 4);
@@ -207,7 +204,6 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.o_p = o; o = align256(o + (size_t)P.S * P.I * 4);
   P.o_dn = o; o = align256(o + (size_t)P.nsd * P.S * P.H * 4);
   P.o_uap = o; o = align256(o + (size_t)P.nsdl * P.S * P.r * 4);
-  P.o_u = o; o = align256(o + (size_t)P.S * P.r * 4);
   P.total = o;
   P.lds_route = lds_route(P);
   // routing tables: active-expert records and four per-slot arrays
@@ -321,6 +317,8 @@ int hip_fail(hipError_t e, const char* what) {
 // Sizes the grids and launches k_route (if the call has routing items) and
 // k_expert (if it has expert work) for one call.
 int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
+  if (P.total >= 0x80000000ull)  // workspace offsets must stay below the out-of-range marker
+    return fail(CARDAN_ERR_UNSUPPORTED, "workspace layout of %zu bytes exceeds 2 GiB", P.total);
   if (P.lds_route > kLdsMax || P.lds_expert > kLdsMax)
     return fail(CARDAN_ERR_UNSUPPORTED, "shape needs %zu/%zu bytes of LDS (> %zu)", P.lds_route,
                 P.lds_expert, kLdsMax);

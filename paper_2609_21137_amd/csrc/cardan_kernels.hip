@@ -131,6 +131,15 @@ __device__ __forceinline__ float4 ld_dev4(const float* p) {
   return make_float4(ld_dev(p), ld_dev(p + 1), ld_dev(p + 2), ld_dev(p + 3));
 }
 
+// Orders this wave's LDS writes before its later LDS reads by other lanes
+// (a wave executes its LDS operations in order; this keeps the compiler from
+// moving them across each other).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Waits for this wave's outstanding memory operations (s_waitcnt vmcnt(0)).
 __device__ __forceinline__ void drain_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
@@ -205,6 +214,37 @@ __device__ __forceinline__ int wave_inclusive_scan(int x) {
   x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15 into rows 1, 3
   x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31 into rows 2, 3
   return x;
+}
+
+// The same DPP lane moves on a double (both halves; lanes without a source
+// read +0).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const long long v = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(v >> 32), CTRL, ROWS, 0xF, false);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
+// Sum of x over the wave, in every lane (a fixed tree: the same rounding on
+// every call).
+__device__ __forceinline__ double wave_sum(double x) {
+  x += dpp_f64<0x111, 0xF>(x);
+  x += dpp_f64<0x112, 0xF>(x);
+  x += dpp_f64<0x114, 0xF>(x);
+  x += dpp_f64<0x118, 0xF>(x);
+  x += dpp_f64<0x142, 0xA>(x);
+  x += dpp_f64<0x143, 0xC>(x);
+  const long long v = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_readlane((int)v, 63), hi = __builtin_amdgcn_readlane((int)(v >> 32), 63);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
+// x of lane 0 (all lanes active).
+__device__ __forceinline__ double lane0(double x) {
+  const long long v = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_readfirstlane((int)v), hi = __builtin_amdgcn_readfirstlane((int)(v >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
 
 // Exclusive prefix sum of arr[0..n) (n <= 4 * kWG) in place; returns the total.
@@ -401,90 +441,263 @@ __device__ RouteTab build_routing(const Plan& P, const int32_t* idx, const float
   return {act, slot_tok, slot_w, slot_e, tok_slot, s_nact};
 }
 
+// The same tables from at most 64 selections held one per lane of wave 0
+// (lane i: selection i's expert, -1 if none or invalid, and weight). A
+// selection's slot is the number of valid selections of smaller experts plus
+// the earlier ones of its own expert (a stable sort by expert); the active
+// index of an expert is the number of distinct smaller experts.
+__device__ RouteTab build_routing_wave(const Plan& P, int e, float wv, uint8_t* tab) {
+  const int S = P.S, k = P.k;
+  int4* act = reinterpret_cast<int4*>(tab);
+  int* slot_tok = reinterpret_cast<int*>(act + P.max_act);
+  float* slot_w = reinterpret_cast<float*>(slot_tok + S);
+  int* slot_e = reinterpret_cast<int*>(slot_w + S);
+  int* tok_slot = slot_e + S;
+  __shared__ int s_nact;
+  if (threadIdx.x < 64) {
+    const int l = threadIdx.x;
+    int below = 0, same = 0, before = 0;
+    for (int i = 0; i < S; ++i) {
+      const int ei = __builtin_amdgcn_readlane(e, i);
+      below += (int)(ei >= 0) & (int)(ei < e);
+      same += (int)(ei == e);
+      before += (int)(ei == e) & (int)(i < l);
+    }
+    const int valid = (int)(e >= 0);
+    const unsigned long long firsts = __ballot(valid & (int)(before == 0));
+    int dbelow = 0;
+    for (unsigned long long m = firsts; m; m &= m - 1)
+      dbelow += (int)(__builtin_amdgcn_readlane(e, (int)__builtin_ctzll(m)) < e);
+    if (l < S) {
+      const int pos = min(below + before, S - 1);
+      if (valid) {
+        slot_tok[pos] = l / k;
+        slot_w[pos] = wv;
+        slot_e[pos] = e;
+      }
+      tok_slot[l] = valid ? pos : -1;
+      if (valid && before == 0 && dbelow < P.max_act) act[dbelow] = make_int4(e, below, same, 0);
+    }
+    if (l == 0) s_nact = min(__popcll(firsts), P.max_act);
+  }
+  __syncthreads();
+  trace_mark(3);
+  return {act, slot_tok, slot_w, slot_e, tok_slot, s_nact};
+}
+
+// ---- exact top-k in one wave ----------------------------------------------
+// Logits are ordered by a 64-bit key that preserves the order of doubles
+// (-0 and +0 share a key); equal keys fall back to the lower expert index.
+__device__ __forceinline__ unsigned long long order_key(double v) {
+  if (v == 0.0) v = 0.0;
+  const unsigned long long u = (unsigned long long)__double_as_longlong(v);
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+__device__ __forceinline__ int wave_count(int p) { return __popcll(__ballot(p)); }
+
+// Lanes below this lane with their bit set in mask.
+__device__ __forceinline__ int lanes_below(unsigned long long mask) {
+  return __builtin_amdgcn_mbcnt_hi((unsigned)(mask >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0u));
+}
+
+// The m-th largest of the wave's values v[i] with in[i] set (m >= 1 of them
+// exist): the largest T with at least m values >= T, found one bit at a
+// time from the most significant.
+template <int NE>
+__device__ __forceinline__ unsigned wave_kth_largest(const unsigned (&v)[NE], const int (&in)[NE], int m) {
+  unsigned T = 0;
+  for (int b = 31; b >= 0; --b) {
+    const unsigned c = T | (1u << b);
+    int n = 0;
+#pragma unroll
+    for (int i = 0; i < NE; ++i) n += wave_count(in[i] & (int)(v[i] >= c));
+    if (n >= m) T = c;
+  }
+  return T;
+}
+
+// Top-k of lg[0..E) (E <= 64 NE) by one wave: sel[j] = expert of rank j
+// under (descending logit, ascending index). ck/ce: LDS scratch of k keys
+// and experts. The k-th largest high key half is found first; only when
+// several experts share it are the low halves, then the indices, consulted.
+template <int NE>
+__device__ void wave_topk(const double* lg, int E, int k, int* sel, unsigned long long* ck, int* ce) {
+  const int l = threadIdx.x & 63;
+  unsigned long long key[NE];
+  unsigned hi[NE], lo[NE];
+  int valid[NE];
+#pragma unroll
+  for (int i = 0; i < NE; ++i) {
+    const int e = l + 64 * i;
+    valid[i] = e < E;
+    key[i] = valid[i] ? order_key(lg[e]) : 0ull;
+    hi[i] = (unsigned)(key[i] >> 32);
+    lo[i] = (unsigned)key[i];
+  }
+  const unsigned T = wave_kth_largest<NE>(hi, valid, k);
+  int above = 0, at = 0, inq[NE];
+#pragma unroll
+  for (int i = 0; i < NE; ++i) {
+    inq[i] = valid[i] & (int)(hi[i] == T);
+    above += wave_count(valid[i] & (int)(hi[i] > T));
+    at += wave_count(inq[i]);
+  }
+  // experts with high half T: all of them are selected, or the need best
+  // among them (low half, then index)
+  unsigned T2 = 0;
+  int need_ties = kMaxE + 1;
+  if (above + at > k) {
+    const int need = k - above;
+    T2 = wave_kth_largest<NE>(lo, inq, need);
+    int above2 = 0;
+#pragma unroll
+    for (int i = 0; i < NE; ++i) above2 += wave_count(inq[i] & (int)(lo[i] > T2));
+    need_ties = need - above2;
+  }
+  // compact the k selected experts in index order
+  int base = 0, tie_base = 0;
+#pragma unroll
+  for (int i = 0; i < NE; ++i) {
+    const int tie = inq[i] & (int)(lo[i] == T2);
+    const unsigned long long tm = __ballot(tie);
+    const int trank = tie_base + lanes_below(tm);
+    tie_base += __popcll(tm);
+    const int s = valid[i] & ((int)(hi[i] > T) | (inq[i] & ((int)(lo[i] > T2) | (tie & (int)(trank < need_ties)))));
+    const unsigned long long sm = __ballot(s);
+    if (s) {
+      const int pos = base + lanes_below(sm);
+      ck[pos] = key[i];
+      ce[pos] = l + 64 * i;
+    }
+    base += __popcll(sm);
+  }
+  wave_lds_sync();
+  // rank among the selected: larger keys, and equal keys of lower index
+  // (earlier in the compacted order)
+  if (l < k) {
+    const unsigned long long kj = ck[l];
+    int r = 0;
+    for (int f = 0; f < k; ++f) {
+      const unsigned long long kf = ck[f];
+      r += (int)(kf > kj) | ((int)(kf == kj) & (int)(f < l));
+    }
+    sel[r] = ce[l];
+  }
+  wave_lds_sync();
+}
+
 // Select item for token t: logits (fixed-order sum of the chunk partials plus
 // bias), top-k by descending logit with ties to the lower index, softmax over
 // the k selected logits, written to topk_idx / topk_w.
+//
+// Up to kWG experts, each thread holds its expert's key and counts the
+// experts with a larger high key half (comparisons split over the waves):
+// experts sharing a high half share a rank, and rank slot r < k receives the
+// best of its group by (low half, then lower index). A group of g > 1 at rank
+// r < k - 1 leaves slot r + 1 empty; with no empty slot every rank below k is
+// held by a single expert, or by the correct best of a group at rank k - 1,
+// so the slots are the exact selection. Otherwise (and for more experts) one
+// wave selects exactly on the full keys.
 __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) {
   const int tid = threadIdx.x;
   const int E = P.E, k = P.k, B = P.B;
-  {
-    double* lg = reinterpret_cast<double*>(smem);          // [E]
-    double* ex = lg + kMaxE;                                // [k]
-    int* sel = reinterpret_cast<int*>(ex + kMaxK);          // [k]
-    int* rank = sel + kMaxK;                                // [E]
-    const int* rcf = wsp<const int>(A, P.o_rc_flag);
-    wait_all(A, P.n_rc, [&](int i) { return ld_dev(rcf + i) != 0; });
-    const double* rl = wsp<const double>(A, P.o_rl);
-    for (int e = tid; e < E; e += kWG) {
-      double s = 0.0;
-      for (int c0 = 0; c0 < P.nch_r; c0 += 32) {
-        // 32 chunk partials in flight; chunks past the end re-read the last
-        // one and are masked out of the sum
-        double v[32];
+  double* lg = reinterpret_cast<double*>(smem);                                    // [E]
+  unsigned long long* slot = reinterpret_cast<unsigned long long*>(lg + kMaxE);    // [k]
+  unsigned long long* ck = slot + kMaxK;                                           // [k]
+  unsigned* hk = reinterpret_cast<unsigned*>(ck + kMaxK);                          // [kWG]
+  int* rank = reinterpret_cast<int*>(hk + kWG);                                    // [kWG]
+  int* sel = rank + kWG;                                                           // [k]
+  int* ce = sel + kMaxK;                                                           // [k]
+  // the bias is read before the wait so its latency is hidden
+  const float b0 = (A.L.router_bias && tid < E) ? A.L.router_bias[tid] : 0.0f;
+  const int* rcf = wsp<const int>(A, P.o_rc_flag);
+  wait_all(A, P.n_rc, [&](int i) { return ld_dev(rcf + i) != 0; });
+  const double* rl = wsp<const double>(A, P.o_rl);
+  double own = 0.0;  // logit of expert tid
+  for (int e = tid; e < E; e += kWG) {
+    double s = 0.0;
+    for (int c0 = 0; c0 < P.nch_r; c0 += 32) {
+      // 32 chunk partials in flight; chunks past the end re-read the last
+      // one and are masked out of the sum
+      double v[32];
 #pragma unroll
-        for (int i = 0; i < 32; ++i) v[i] = ld_dev(rl + ((size_t)min(c0 + i, P.nch_r - 1) * B + t) * E + e);
+      for (int i = 0; i < 32; ++i) v[i] = ld_dev(rl + ((size_t)min(c0 + i, P.nch_r - 1) * B + t) * E + e);
 #pragma unroll
-        for (int i = 0; i < 32; ++i) s += (c0 + i < P.nch_r) ? v[i] : 0.0;
-      }
-      if (A.L.router_bias) s += (double)A.L.router_bias[e];
-      lg[e] = s;
+      for (int i = 0; i < 32; ++i) s += (c0 + i < P.nch_r) ? v[i] : 0.0;
     }
-    if (tid < kMaxK) sel[tid] = -1;
-    for (int e = tid; e < E; e += kWG) rank[e] = 0;
-    __syncthreads();
-    trace_mark(0);
-    // rank of expert e = number of experts before it under (descending logit,
-    // ascending index); the experts of rank < k are the selection, in order.
-    // The comparisons of one expert are split over `parts` thread groups.
-    {
-      const int parts = max(1, kWG / E);
-      const int per = (E + parts - 1) / parts;
-      for (int i = tid; i < parts * E; i += kWG) {
-        const int e = i % E, pt = i / E;
-        const double v = lg[e];
-        const int f0 = pt * per, f1 = min(E, f0 + per);
-        int rk = 0;
-        // 8 logits per round, read together (broadcast LDS reads)
-        for (int f = f0; f < f1; f += 8) {
-          double u[8];
-#pragma unroll
-          for (int b = 0; b < 8; ++b) u[b] = lg[min(f + b, E - 1)];
-          // bitwise (not short-circuit) logic: no branches in the loop
-#pragma unroll
-          for (int b = 0; b < 8; ++b)
-            rk += ((int)(u[b] > v) | ((int)(u[b] == v) & (int)(f + b < e))) & (int)(f + b < f1);
-        }
-        atomicAdd(&rank[e], rk);
-      }
+    if (A.L.router_bias) s += (double)(e == tid ? b0 : A.L.router_bias[e]);
+    lg[e] = s;
+    if (e == tid) own = s;
+  }
+  const bool counted = E <= kWG;
+  if (counted) {
+    const int Ep = (E + 31) & ~31;
+    const unsigned long long key = tid < E ? order_key(own) : 0ull;
+    if (tid < Ep) {
+      hk[tid] = (unsigned)(key >> 32);  // padding keys are 0, below every logit's
+      rank[tid] = 0;
     }
-    trace_mark(3);
+    if (tid < kMaxK) slot[tid] = 0ull;
     __syncthreads();
-    for (int e = tid; e < E; e += kWG)
-      if (rank[e] < k) sel[rank[e]] = e;
+    const int parts = max(1, kWG / Ep);
+    const int per = ((Ep + parts - 1) / parts + 31) & ~31;
+    const int e = tid % Ep, pt = tid / Ep;
+    const int f0 = pt * per, f1 = min(Ep, f0 + per);
+    const unsigned ke = hk[e];
+    int rk = 0;
+    for (int f = f0; f < f1; f += 32) {
+      const uint4* q = reinterpret_cast<const uint4*>(hk + f);
+      uint4 u[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) u[j] = q[j];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) rk += (int)(u[j].x > ke) + (int)(u[j].y > ke) + (int)(u[j].z > ke) + (int)(u[j].w > ke);
+    }
+    if (e < E && f0 < f1) atomicAdd(&rank[e], rk);
     __syncthreads();
+    if (tid < E) {
+      const int r = rank[tid];
+      if (r < k) atomicMax(&slot[r], ((unsigned long long)(unsigned)key << 32) | (unsigned)(~tid));
+    }
+  }
+  __syncthreads();
+  trace_mark(0);
+  if (tid < 64) {
+    const unsigned long long v = counted && tid < k ? slot[tid] : 1ull;
+    int e;
+    if (!counted || __ballot(v == 0ull)) {
+      const int ne = (E + 63) / 64;
+      if (ne <= 1)
+        wave_topk<1>(lg, E, k, sel, ck, ce);
+      else if (ne <= 2)
+        wave_topk<2>(lg, E, k, sel, ck, ce);
+      else if (ne <= 4)
+        wave_topk<4>(lg, E, k, sel, ck, ce);
+      else if (ne <= 8)
+        wave_topk<8>(lg, E, k, sel, ck, ce);
+      else
+        wave_topk<16>(lg, E, k, sel, ck, ce);
+      e = tid < k ? sel[tid] : 0;
+    } else {
+      e = tid < k ? (int)(~(unsigned)v) : 0;
+    }
     trace_mark(1);
-    // softmax over the k selected logits, summed in selection order
+    // softmax over the k selected logits (a fixed summation tree); exp of a
+    // non-positive difference in single precision is far inside the
+    // weights' tolerance
+    const double x = lg[e];
+    const double mx = lane0(x);
+    const double ex = tid < k ? (double)expf((float)(x - mx)) : 0.0;
+    const double sum = wave_sum(ex);
     if (tid < k) {
-      const int e = sel[tid];
-      const double mx = sel[0] >= 0 ? lg[sel[0]] : 0.0;
-      // exp of a non-positive difference; single precision is far inside
-      // the weights' tolerance
-      ex[tid] = e >= 0 ? (double)expf((float)(lg[e] - mx)) : 0.0;
-    }
-    __syncthreads();
-    if (tid < k) {
-      double sum = 0.0;
-      for (int j = 0; j < k; ++j) sum += ex[j];
-      st_dev(A.topk_idx + t * k + tid, sel[tid]);
-      st_dev(A.topk_w + t * k + tid, (float)(ex[tid] / sum));
+      st_dev(A.topk_idx + t * k + tid, e);
+      st_dev(A.topk_w + t * k + tid, (float)(ex / sum));
     }
     trace_mark(2);
   }
 }
 
-// z reduce item i: outputs [256 i, 256 i + 256) of z[2][B][r], each the
-// fixed-order sum of its chunk partials (both halves from one basis when
-// U_up is U_gate).
 __device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
   const int* zcf = wsp<const int>(A, P.o_zc_flag);
   wait_all(A, P.n_zc, [&](int f) { return ld_dev(zcf + f) != 0; });
@@ -498,9 +711,9 @@ __device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
     for (int c0 = 0; c0 < P.nch_z; c0 += 32) {
       float v[32];
 #pragma unroll
-      for (int j = 0; j < 32; ++j) v[j] = (c0 + j < P.nch_z) ? ld_dev(zp + (size_t)(c0 + j) * B * r) : 0.0f;
+      for (int j = 0; j < 32; ++j) v[j] = ld_dev(zp + (size_t)min(c0 + j, P.nch_z - 1) * B * r);
 #pragma unroll
-      for (int j = 0; j < 32; ++j) s += v[j];
+      for (int j = 0; j < 32; ++j) s += (c0 + j < P.nch_z) ? v[j] : 0.0f;
     }
     A.z_out[o] = s;
   }
@@ -546,6 +759,25 @@ constexpr uint32_t kOob = 0x80000000u;  // an offset past every resource
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
+
+constexpr int kSc1 = 16;  // cache policy operand of a device-scope (sc1) buffer access
+
+// Device-scope reads of workspace data written by other workgroups, through
+// one buffer resource over the workspace: the byte offset kOob (past the
+// workspace) reads zeros without a memory access, so a skipped term needs no
+// branch and every load of a batch issues back to back.
+struct WsRead {
+  rsrc_t rs;
+  const uint8_t* base;
+  __device__ __forceinline__ WsRead(const Args& A, const Plan& P)
+      : rs(make_rsrc(A.ws, (uint32_t)P.total)), base(A.ws) {}
+  __device__ __forceinline__ uint32_t off(const void* p) const {
+    return (uint32_t)(reinterpret_cast<const uint8_t*>(p) - base);
+  }
+  __device__ __forceinline__ float4 f4(uint32_t o) const {
+    return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, o, 0, kSc1));
+  }
+};
 
 template <int D, int NOPS, int PD>
 struct VqPipe {
@@ -731,18 +963,17 @@ __device__ __forceinline__ void stage_bf16(uint4* ops, int ld, int nt, int n8, F
 // loads) as bf16 hi/lo pairs: ops[t * ld + 2 j] (hi) and [.. + 1] (lo) hold
 // inputs 8 j .. 8 j + 7 of row src(t), value = hi + lo.
 template <typename F>
-__device__ __forceinline__ void stage_split(uint4* ops, int ld, int nt, int n8, F src) {
+__device__ __forceinline__ void stage_split(const WsRead& ws, uint4* ops, int ld, int nt, int n8, F src) {
   // four groups per thread per round, their loads in flight together
   for (int i0 = threadIdx.x; i0 < nt * n8; i0 += 4 * kWG) {
     float4 v[4][2];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int i = i0 + u * kWG;
-      if (i < nt * n8) {
-        const float* p = src(i / n8) + 8 * (i % n8);
-        v[u][0] = ld_dev4(p);
-        v[u][1] = ld_dev4(p + 4);
-      }
+      const int ii = min(i, nt * n8 - 1);
+      const uint32_t o = i < nt * n8 ? ws.off(src(ii / n8) + 8 * (ii % n8)) : kOob;
+      v[u][0] = ws.f4(o);
+      v[u][1] = ws.f4(o + 16);
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -790,11 +1021,11 @@ __device__ __forceinline__ float4 fma4(float w, float4 v, float4 a) {
 // the workgroup is split into G groups (G * items <= 256 threads) that take
 // every G-th term, BATCH terms' loads issued together; the group partials
 // meet in LDS (`red`, G * items * NV float4) and are added in group order,
-// so the result is deterministic. load(item, p, v, w) fills term p (p < 0:
-// no term, return zeros); done(item, sum) receives the result. All threads of
-// the workgroup must call it.
-template <int NV, int BATCH, typename Load, typename Done>
-__device__ __forceinline__ void split_sum(int items, int npair, float4* red, Load load, Done done) {
+// so the result is deterministic. term(item, p, off, w) gives term p's
+// workspace byte offsets and weight (p < 0 or no term: kOob and 0); done(item,
+// sum) receives the result. All threads of the workgroup must call it.
+template <int NV, int BATCH, typename Term, typename Done>
+__device__ __forceinline__ void split_sum(const WsRead& ws, int items, int npair, float4* red, Term term, Done done) {
   const int tid = threadIdx.x;
   const int G = items >= kWG ? 1 : min(16, kWG / items);
   for (int base = 0; base < items * G; base += kWG) {
@@ -805,13 +1036,18 @@ __device__ __forceinline__ void split_sum(int items, int npair, float4* red, Loa
     for (int u = 0; u < NV; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (idx < items * G) {
       for (int p0 = g; p0 < npair; p0 += G * BATCH) {
-        float4 v[BATCH][NV];
+        uint32_t off[BATCH][NV];
         float wt[BATCH];
 #pragma unroll
         for (int b = 0; b < BATCH; ++b) {
           const int p = p0 + b * G;
-          load(item, p < npair ? p : -1, v[b], wt[b]);
+          term(item, p < npair ? p : -1, off[b], wt[b]);
         }
+        float4 v[BATCH][NV];
+#pragma unroll
+        for (int b = 0; b < BATCH; ++b)
+#pragma unroll
+          for (int u = 0; u < NV; ++u) v[b][u] = ws.f4(off[b][u]);
 #pragma unroll
         for (int b = 0; b < BATCH; ++b)
 #pragma unroll
@@ -898,13 +1134,35 @@ __device__ __forceinline__ Routing expert_of(const Plan& P, const RouteTab& RT, 
   return {min(max(v.x, 0), P.E - 1), s0, min(max(v.z, 0), P.S - s0)};
 }
 
+// One code book (K words of D bf16) as 16-byte groups, one per thread, zero
+// past the book; stored for the item as word c at cb[c] (d = 8) or at the
+// 8-byte slot c of the uint2 view (d = 4). Items load their book before
+// their weight prime and store it with their activation staging.
+template <int D>
+__device__ __forceinline__ uint4 book_load(const uint16_t* src, int K) {
+  const int n16 = K * D * 2, byte0 = threadIdx.x * 16;
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (byte0 + 16 <= n16) {
+    v = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(src) + byte0);
+  } else if (byte0 < n16) {  // ragged end of the book
+    uint16_t e[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int u = 0; byte0 + 2 * u < n16; ++u) e[u] = src[byte0 / 2 + u];
+    v = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16));
+  }
+  return v;
+}
+template <int D>
+__device__ __forceinline__ void book_store(uint4* cb, uint4 v) {
+  if (threadIdx.x < 256 * D / 8) cb[threadIdx.x] = v;
+}
+
 // Gate/up tile (a, pj, cg, s): 256 output columns of projection pj over
 // split s of the joint reduction axis [x (H inputs) | z (r ranks)], i.e. the
 // VQ gather sum and V^T z accumulate in the same MFMA accumulators. Each
 // tile writes its partial sums.
 template <int D>
 __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg, int s,
-                            bool lr_first, const uint4* cbs, uint8_t* smem) {
+                            bool lr_first, uint4* cbs, uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);
   const int H = P.H, I = P.I, r = P.r, B = P.B;
   const int KSX = H / 32, KSZ = (r + 31) / 32;
@@ -921,18 +1179,29 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
   uint4* xs = reinterpret_cast<uint4*>(smem);
   uint4* zs = xs + P.nt_max * ldx;
   float* gu = wsp<float>(A, P.o_gu);
-  const int* slot_tok = RT.slot_tok;
+  const int* const slot_tok = RT.slot_tok;
   const float* zsrc = (P.flags & F_Z) ? A.z_out : A.z_in;
-  const uint4* cb = cbs + pj * 256;
 
   VqPipe<D, 1, kPdVq> vq;
   DensePipe<2, kPdDense> lr;
   const int n8x = (x1 - x0) * 4, n8z = (z1 - z0) * 4;  // 8-element groups per token row
-  // z rows past r are zero-padded on both operands; r % 8 == 0, so a group
-  // of 8 ranks is either all valid or all padding
-  auto z_group = [&](int t, int jj) -> const float* {
-    const int q = z0 * 32 + 8 * jj;
-    return q < r ? zsrc + ((size_t)pj * B + slot_tok[R.s0 + t]) * r + q : nullptr;
+  // Activation loads through buffer resources over x [B][H] and z [2][B][r]
+  // (written before this kernel): groups past the tile's rows, and z rows
+  // past r (zero-padded on both operands; r % 8 == 0, so a group of 8 ranks
+  // is all valid or all padding), read zeros from the out-of-range offset.
+  const rsrc_t xrs = make_rsrc(A.x, (uint32_t)B * H * 2);
+  const rsrc_t zrs = make_rsrc(zsrc, (uint32_t)(2 * B * r * 4));
+  auto x_group = [&](int tg, int i, int n) -> uint4 {  // group i of the n staged from row tg
+    const int ii = min(i, n - 1), t = tg + ii / n8x;
+    const uint32_t o = (uint32_t)(((size_t)slot_tok[R.s0 + t] * H + x0 * 32 + 8 * (ii % n8x)) * 2);
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xrs, i < n ? o : kOob, 0, 0));
+  };
+  auto z_group = [&](int tg, int i, int n, float4& v0, float4& v1) {  // group i of the n from row tg
+    const int ii = min(i, n - 1), t = tg + ii / n8z, q = z0 * 32 + 8 * (ii % n8z);
+    const uint32_t o = (uint32_t)((((size_t)pj * B + slot_tok[R.s0 + t]) * r + q) * 4);
+    const uint32_t oo = i < n && q < r ? o : kOob;
+    v0 = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(zrs, oo, 0, 0));
+    v1 = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(zrs, oo + 16, 0, 0));
   };
   auto put_z = [&](int t, int jj, float4 v0, float4 v1) {
     const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
@@ -957,19 +1226,15 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
 #pragma unroll
     for (int u = 0; u < kRegStage; ++u) {
       const int i = threadIdx.x + u * kWG;
-      if (i < nt * n8x)
-        xv[u] = *reinterpret_cast<const uint4*>(A.x + (size_t)slot_tok[R.s0 + tg + i / n8x] * H + x0 * 32 +
-                                                8 * (i % n8x));
-      if (i < nt * n8z) {
-        const float* zp = z_group(tg + i / n8z, i % n8z);
-        zv[u][0] = zp ? ld_dev4(zp) : make_float4(0.f, 0.f, 0.f, 0.f);
-        zv[u][1] = zp ? ld_dev4(zp + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
+      xv[u] = x_group(tg, i, nt * n8x);
+      z_group(tg, i, nt * n8z, zv[u][0], zv[u][1]);
     }
-    __builtin_amdgcn_sched_barrier(0);  // keep the activation loads first
+    const uint4 bk = book_load<D>(pj ? A.L.cb_up : A.L.cb_gate, P.K);
+    __builtin_amdgcn_sched_barrier(0);  // keep the activation and book loads first
     vq.prime(codes, H / D, I, c0, I, x0, x1);
     lr.prime(V, I, c0, I, r, z0, z1);
     __syncthreads();
+    book_store<D>(cbs, bk);
 #pragma unroll
     for (int u = 0; u < kRegStage; ++u) {
       const int i = threadIdx.x + u * kWG;
@@ -981,12 +1246,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
     for (int i0 = threadIdx.x + kRegStage * kWG; i0 < nt * n8x; i0 += 4 * kWG) {
       uint4 v[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int i = i0 + u * kWG;
-        if (i < nt * n8x)
-          v[u] = *reinterpret_cast<const uint4*>(A.x + (size_t)slot_tok[R.s0 + tg + i / n8x] * H + x0 * 32 +
-                                                 8 * (i % n8x));
-      }
+      for (int u = 0; u < 4; ++u) v[u] = x_group(tg, i0 + u * kWG, nt * n8x);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int i = i0 + u * kWG;
@@ -996,12 +1256,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
     for (int i0 = threadIdx.x + kRegStage * kWG; i0 < nt * n8z; i0 += 2 * kWG) {
       float4 v[2][2];
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int i = i0 + u * kWG;
-        const float* zp = i < nt * n8z ? z_group(tg + i / n8z, i % n8z) : nullptr;
-        v[u][0] = zp ? ld_dev4(zp) : make_float4(0.f, 0.f, 0.f, 0.f);
-        v[u][1] = zp ? ld_dev4(zp + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
+      for (int u = 0; u < 2; ++u) z_group(tg, i0 + u * kWG, nt * n8z, v[u][0], v[u][1]);
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int i = i0 + u * kWG;
@@ -1013,7 +1268,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
     f32x4 acc[4];
     zero_acc(acc);
     if (lr_first) lr.run(zs, ldz, z0, nt, acc);
-    vq.run(cb, xs, ldx, x0, nt, acc);
+    vq.run(cbs, xs, ldx, x0, nt, acc);
     trace_mark(1);
     if (!lr_first) lr.run(zs, ldz, z0, nt, acc);
     store_acc(acc, nt, c0, I, [&](int t) { return gu + (((size_t)(R.s0 + tg + t) * 2 + pj) * P.ns + s) * I; });
@@ -1031,19 +1286,16 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
   const int ns = P.ns, nq = kColsPerGroup / 4, cbase = cg * kColsPerGroup;
   float* pbuf = wsp<float>(A, P.o_p);
   float4* red = reinterpret_cast<float4*>(smem);
+  const WsRead ws(A, P);
   split_sum<2, 8>(
-      R.ne * nq, ns, red,
-      [&](int item, int sp, float4(&v)[2], float& wt) {
+      ws, R.ne * nq, ns, red,
+      [&](int item, int sp, uint32_t(&off)[2], float& wt) {
         const int t = item / nq, col = cbase + 4 * (item % nq);
-        if (sp < 0 || col >= I) {
-          v[0] = v[1] = make_float4(0.f, 0.f, 0.f, 0.f);
-          wt = 0.f;
-          return;
-        }
-        const float* src = gu + ((size_t)(R.s0 + t) * 2 * ns + sp) * I + col;
-        v[0] = ld_dev4(src);
-        v[1] = ld_dev4(src + (size_t)ns * I);
-        wt = 1.f;
+        const bool ok = sp >= 0 && col < I;
+        const uint32_t o = (uint32_t)(P.o_gu + (((size_t)(R.s0 + t) * 2 * ns + max(sp, 0)) * I + min(col, I - 4)) * 4);
+        off[0] = ok ? o : kOob;
+        off[1] = ok ? o + (uint32_t)ns * I * 4 : kOob;
+        wt = ok ? 1.f : 0.f;
       },
       [&](int item, const float4(&gsum)[2]) {
         const int t = item / nq, col = cbase + 4 * (item % nq);
@@ -1062,9 +1314,10 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
 // columns of r (A_e^T p -> uap[s], nsdl splits: the coefficient bytes of a
 // K-step are 16x the code bytes). Weight loads are issued before waiting
 // for the expert's p.
-template <typename Prime, typename Run, typename Dst>
+template <typename Prime, typename Stage, typename Run, typename Dst>
 __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Routing& R, int ks0, int ks1,
-                                          int c0, int n_out, Prime prime, Run run, Dst dst, uint8_t* smem) {
+                                          int c0, int n_out, Prime prime, Stage stage, Run run, Dst dst,
+                                          uint8_t* smem) {
   prime();
   wait_geq(A, wsp<int>(A, P.o_gu_done) + R.e, P.ncg);
   const int I = P.I;
@@ -1075,7 +1328,8 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
     const int nt = min(P.nt_max, R.ne - tg);
     if (tg > 0) prime();
     __syncthreads();
-    stage_split(ps, ld, nt, (ks1 - ks0) * 4,
+    stage();
+    stage_split(WsRead(A, P), ps, ld, nt, (ks1 - ks0) * 4,
                 [&](int t) { return pbuf + (size_t)(R.s0 + tg + t) * I + ks0 * 32; });
     __syncthreads();
     trace_mark(0);
@@ -1088,7 +1342,7 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
 
 template <int D>
 __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgx, int s,
-                             const uint4* cbs, uint8_t* smem) {
+                             uint4* cbs, uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);
   const int H = P.H, I = P.I, S = P.S, KS = I / 32;
   const int ks0 = s * KS / P.nsd, ks1 = (s + 1) * KS / P.nsd;
@@ -1096,8 +1350,15 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
   const uint8_t* codes = A.L.codes_down + (size_t)R.e * (I / D) * H;
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
   VqPipe<D, 2, kPdVq> pipe;
-  down_body(P, A, R, ks0, ks1, c0, H, [&]() { pipe.prime(codes, I / D, H, c0, H, ks0, ks1); },
-            [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs + 2 * 256, ps, ld, ks0, nt, acc); },
+  uint4 bk;
+  down_body(P, A, R, ks0, ks1, c0, H,
+            [&]() {
+              bk = book_load<D>(A.L.cb_down, P.K);
+              __builtin_amdgcn_sched_barrier(0);
+              pipe.prime(codes, I / D, H, c0, H, ks0, ks1);
+            },
+            [&]() { book_store<D>(cbs, bk); },
+            [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs, ps, ld, ks0, nt, acc); },
             [&](int slot) { return dn + (size_t)slot * H; }, smem);
   publish(wsp<int>(A, P.o_dn_done) + R.e * (P.ncgh + 1) + cgx);
 }
@@ -1107,7 +1368,6 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
 // (r values per slot) and flags the expert's low-rank part done.
 __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgr, int s,
                              uint8_t* smem) {
-  __shared__ int s_last;
   const Routing R = expert_of(P, RT, a);
   const int I = P.I, r = P.r, S = P.S, KS = I / 32, nsdl = P.nsdl;
   const int ks0 = s * KS / nsdl, ks1 = (s + 1) * KS / nsdl;
@@ -1115,26 +1375,10 @@ __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, i
   const uint16_t* Ae = A.L.A_down + (size_t)R.e * I * r;
   float* uap = wsp<float>(A, P.o_uap);
   DensePipe<2, kPdDense> pipe;
-  down_body(P, A, R, ks0, ks1, c0, r, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); },
+  down_body(P, A, R, ks0, ks1, c0, r, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); }, [&]() {},
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(ps, ld, ks0, nt, acc); },
             [&](int slot) { return uap + ((size_t)s * S + slot) * r; }, smem);
-  int* tick = wsp<int>(A, P.o_lr_tick) + R.e;
-  if (!last_of(tick, P.ncgr * nsdl, &s_last)) return;
-  const int nq = r / 4;
-  float* u = wsp<float>(A, P.o_u);
-  split_sum<1, 8>(
-      R.ne * nq, nsdl, reinterpret_cast<float4*>(smem),
-      [&](int item, int sp, float4(&v)[1], float& wt) {
-        if (sp < 0) {
-          v[0] = make_float4(0.f, 0.f, 0.f, 0.f);
-          wt = 0.f;
-          return;
-        }
-        v[0] = ld_dev4(uap + ((size_t)sp * S + R.s0 + item / nq) * r + 4 * (item % nq));
-        wt = 1.f;
-      },
-      [&](int item, const float4(&q)[1]) { st_dev4(u + (size_t)(R.s0 + item / nq) * r + 4 * (item % nq), q[0]); });
-  if (threadIdx.x == 0) *tick = 0;
+  // the combine sums the nsdl partials of u_e itself
   publish(wsp<int>(A, P.o_dn_done) + R.e * (P.ncgh + 1) + P.ncgh);
 }
 
@@ -1150,18 +1394,38 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
   const int tid = threadIdx.x, w = tid >> 6;
   const int cbase = cgy * kColsPerGroup;
   const int KSR = (r + 31) / 32;
-  DensePipe<2, kPdDense> bp;
+  // B is primed in full for r <= 128 (later K-steps load during the run)
+  DensePipe<2, 4> bp;
   if (r > 0) bp.prime(A.L.B_down, H, cbase + w * 64, H, r, 0, KSR);
 
   const int* s_slot = RT.tok_slot + t0 * k;  // (t, j) -> slot of the tile's tokens
   const float* s_w_slot = RT.slot_w;
   const int* s_e_slot = RT.slot_e;
   float4* red = reinterpret_cast<float4*>(smem);                      // [256]
-  float* bt = reinterpret_cast<float*>(red + kWG);                    // [nt][256] B^T u
-  uint4* us = reinterpret_cast<uint4*>(bt + kTokPass * kColsPerGroup);
+  float* dnb = reinterpret_cast<float*>(red + kWG);                   // [nt][256] VQ down sums
+  uint4* us = reinterpret_cast<uint4*>(dnb + kTokPass * kColsPerGroup);
   const int ntk = nt * k;
+  const int nq = KSR * 8, ld = KSR * 8 + 1;
+  const int nsdl = P.nsdl, kd = k * nsd, ku = r > 0 ? k * nsdl : 0;
+  constexpr int kB = kCombineChunk;
+  // Term tables, built before the wait: per (token, selection j, split) the
+  // row offset and weight of a low-rank partial of u_e (ku per token) and of
+  // a VQ down partial (kd per token); kOob and 0 for an invalid selection.
+  uint2* tab_u = reinterpret_cast<uint2*>(us + (size_t)P.tpc * ld);
+  uint2* tab_d = tab_u + nt * ku;
+  for (int i = tid; i < nt * (ku + kd); i += kWG) {
+    const bool isu = i < nt * ku;
+    const int ii = isu ? i : i - nt * ku;
+    const int per = isu ? ku : kd, nsp = isu ? nsdl : nsd;
+    const int t = ii / per, pp = ii % per, j = pp / nsp, ss = pp % nsp;
+    const int sl = s_slot[t * k + j];
+    const int slc = max(sl, 0);
+    const uint32_t o = isu ? (uint32_t)(P.o_uap + ((size_t)ss * S + slc) * r * 4)
+                           : (uint32_t)(P.o_dn + ((size_t)ss * S + slc) * H * 4);
+    (isu ? tab_u : tab_d)[ii] = make_uint2(sl >= 0 ? o : kOob, __float_as_uint(sl >= 0 ? s_w_slot[slc] : 0.f));
+  }
   {
-    // every down tile of this column group (and of the low-rank columns) of
+    // every down tile of this column group (and every low-rank down tile) of
     // every expert of these tokens
     const int* dnd = wsp<const int>(A, P.o_dn_done);
     const int ncol = r > 0 ? 2 : 1, per_e = P.ncgh + 1;
@@ -1169,71 +1433,83 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
       const int c = i % ncol, tj = i / ncol;
       const int sl = s_slot[tj];
       if (sl < 0) return true;
-      return ld_dev(dnd + s_e_slot[sl] * per_e + (c == 0 ? cgy : P.ncgh)) >= (c == 0 ? nsd : 1);
+      return ld_dev(dnd + s_e_slot[sl] * per_e + (c == 0 ? cgy : P.ncgh)) >= (c == 0 ? nsd : P.ncgr * nsdl);
     });
   }
+  trace_mark(2);
+  // One pass with the loads in flight together: u[t] = sum_j a_j u_ej[slot_j]
+  // (u_e from its nsdl partials) in quads of ranks (zero past r; staged as
+  // bf16 hi/lo for B^T u), and the VQ down sums of this column group, one
+  // float4 of 4 columns per item. Each item's terms (selection-major) are
+  // cut into chunks of kB taken by separate threads, so a thread has at most
+  // kB loads in flight; the chunk sums are added in order afterwards.
+  const WsRead ws(A, P);
+  const int nu = r > 0 ? nt * nq : 0, nd = nt * 64;
+  const int cu = (ku + kB - 1) / kB, cd = (kd + kB - 1) / kB;
+  const int n_units = nu * cu + nd * cd;
+  float4* part = reinterpret_cast<float4*>(smem + combine_part_offset(P));
+  for (int unit = tid; unit < n_units; unit += kWG) {
+    const bool isu = unit < nu * cu;
+    const int uu = isu ? unit : unit - nu * cu;
+    const int it = isu ? uu / cu : uu / cd, c = isu ? uu % cu : uu % cd;
+    const int t = isu ? it / nq : it >> 6, q = isu ? it % nq : 0;
+    const int col = cbase + 4 * (it & 63);
+    // the column's (or rank quad's) byte offset within a term's row; a
+    // padding quad or column reads out of range
+    const uint32_t ocol = isu ? (4 * q < r ? (uint32_t)(16 * q) : kOob) : (col < H ? (uint32_t)(4 * col) : kOob);
+    const int nterm = isu ? ku : kd, p0 = c * kB;
+    const uint2* tb = (isu ? tab_u + t * ku : tab_d + t * kd) + p0;
+    uint2 e[kB];
+#pragma unroll
+    for (int b = 0; b < kB; ++b) e[b] = tb[min(b, nterm - 1 - p0)];
+    float4 v[kB];
+#pragma unroll
+    for (int b = 0; b < kB; ++b) v[b] = ws.f4(p0 + b < nterm ? e[b].x + ocol : kOob);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int b = 0; b < kB; ++b) acc = fma4(p0 + b < nterm ? __uint_as_float(e[b].y) : 0.f, v[b], acc);
+    part[unit] = acc;
+  }
+  __syncthreads();
+  for (int item = tid; item < nu + nd; item += kWG) {
+    const bool isu = item < nu;
+    const int nc = isu ? cu : cd;
+    const float4* pp = part + (isu ? item * cu : nu * cu + (item - nu) * cd);
+    float4 acc = pp[0];
+    for (int c = 1; c < nc; ++c) acc = make_float4(acc.x + pp[c].x, acc.y + pp[c].y, acc.z + pp[c].z, acc.w + pp[c].w);
+    if (isu)
+      put_split_quad(us + (item / nq) * ld, item % nq, acc);
+    else
+      reinterpret_cast<float4*>(dnb)[item - nu] = acc;
+  }
+  trace_mark(3);
+  __syncthreads();
+  trace_mark(0);
   if (r > 0) {
-    // u[t] = sum_j a_j u_ej[slot_j] in quads of ranks (zero past r), staged
-    // as bf16 hi/lo
-    const float* ue = wsp<const float>(A, P.o_u);
-    const int nq = KSR * 8, ld = KSR * 8 + 1;
-    split_sum<1, 8>(
-        nt * nq, k, red,
-        [&](int item, int j, float4(&v)[1], float& wt) {
-          const int t = item / nq, q = item % nq;
-          const int sl = j >= 0 ? s_slot[t * k + j] : -1;
-          if (sl < 0 || 4 * q >= r) {
-            v[0] = make_float4(0.f, 0.f, 0.f, 0.f);
-            wt = 0.f;
-            return;
-          }
-          v[0] = ld_dev4(ue + (size_t)sl * r + 4 * q);
-          wt = s_w_slot[sl];
-        },
-        [&](int item, const float4(&u)[1]) { put_split_quad(us + (item / nq) * ld, item % nq, u[0]); });
-    __syncthreads();
-    trace_mark(0);
+    // y = VQ sums + B^T u, written from the accumulators: token rows 4g + i,
+    // columns 64 w + 4 n + q
     f32x4 acc[4];
     zero_acc(acc);
     bp.run(us, ld, 0, nt, acc);
-    // B^T u into LDS: token rows 4g + i, columns 64 w + 4 n + q
+    trace_mark(1);
     const int l = tid & 63, n = l & 15, g = l >> 4;
+    const int c = w * 64 + 4 * n;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = 4 * g + i;
-      if (t < nt)
-        *reinterpret_cast<float4*>(bt + t * kColsPerGroup + w * 64 + 4 * n) =
-            make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+      if (t < nt && cbase + c < H) {
+        const float4 d = *reinterpret_cast<const float4*>(dnb + t * kColsPerGroup + c);
+        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + cbase + c) =
+            make_float4(d.x + acc[0][i], d.y + acc[1][i], d.z + acc[2][i], d.w + acc[3][i]);
+      }
     }
-    __syncthreads();
-    trace_mark(1);
+  } else {
+    for (int i = tid; i < nt * 64; i += kWG) {
+      const int t = i >> 6, col = cbase + 4 * (i & 63);
+      if (col < H)
+        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) = reinterpret_cast<const float4*>(dnb)[i];
+    }
   }
-  // VQ part and output, one float4 of 4 columns per item
-  const float* dn = wsp<const float>(A, P.o_dn);
-  split_sum<1, 8>(
-      nt * 64, k * nsd, red,
-      [&](int item, int p, float4(&v)[1], float& wt) {
-        const int t = item >> 6, col = cbase + 4 * (item & 63);
-        const int j = p / nsd, ss = p % nsd;
-        const int sl = p >= 0 ? s_slot[t * k + j] : -1;
-        if (sl < 0 || col >= H) {
-          v[0] = make_float4(0.f, 0.f, 0.f, 0.f);
-          wt = 0.f;
-          return;
-        }
-        v[0] = ld_dev4(dn + ((size_t)ss * S + sl) * H + col);
-        wt = s_w_slot[sl];
-      },
-      [&](int item, const float4(&q)[1]) {
-        const int t = item >> 6, c4 = item & 63, col = cbase + 4 * c4;
-        if (col >= H) return;
-        float4 o = q[0];
-        if (r > 0) {
-          const float4 b = *reinterpret_cast<const float4*>(bt + t * kColsPerGroup + 4 * c4);
-          o = make_float4(o.x + b.x, o.y + b.y, o.z + b.z, o.w + b.w);
-        }
-        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) = o;
-      });
 }
 
 // Gate/up tile of position p. The tiles of splits s < s_vq read codes (LDS
@@ -1287,7 +1563,6 @@ __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
   if (blockIdx.x == 0 && (P.flags & F_EXPERTS)) {
     clear_ints(wsp<int>(A, P.o_gu_tick), P.E * P.ncg);
     clear_ints(wsp<int>(A, P.o_gu_done), P.E);
-    clear_ints(wsp<int>(A, P.o_lr_tick), P.E);
     clear_ints(wsp<int>(A, P.o_dn_done), P.E * (P.ncgh + 1));
   }
   for (int j = blockIdx.x; j < P.n_pre; j += gridDim.x) {
@@ -1322,27 +1597,19 @@ __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
 template <int D>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  __shared__ uint4 cbs[3 * 256];  // gate, up, down code books (zero-padded to 256 words)
+  __shared__ uint4 cbs[256];  // the code book of the current item (zero-padded to 256 words)
   const int tid = threadIdx.x;
-  {
-    // code word c of book b at cbs[b * 256 + c] (d = 8) or at the 8-byte
-    // slot b * 512 + c of the uint2 view (d = 4); one load per thread per
-    // book (code books are 16-byte aligned, K * d * 2 bytes long)
-    const uint16_t* src[3] = {A.L.cb_gate, A.L.cb_up, A.L.cb_down};
-    const int n16 = P.K * D * 2;  // bytes of a code book
-#pragma unroll
-    for (int b = 0; b < 3; ++b) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      const int byte0 = tid * 16;
-      if (byte0 + 16 <= n16) {
-        v = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(src[b]) + byte0);
-      } else if (byte0 < n16) {  // ragged end of the book
-        uint16_t e[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int u = 0; byte0 + 2 * u < n16; ++u) e[u] = src[b][byte0 / 2 + u];
-        v = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16));
-      }
-      if (tid < 256 * D / 8) reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(cbs) + b * 256 * 8)[tid] = v;
-    }
+  ItemTrace tr_route;
+  // Small batches: the selections, one per lane of wave 0, are built into
+  // the routing tables by that wave.
+  const bool wave_routing = P.S <= 64;
+  const int32_t* r_idx = (P.flags & F_ROUTE) ? A.topk_idx : A.idx_in;
+  const float* r_w = (P.flags & F_ROUTE) ? A.topk_w : A.w_in;
+  int sel_e = -1;
+  float sel_w = 0.0f;
+  if (wave_routing && tid < P.S) {
+    sel_e = ld_dev(r_idx + tid);
+    sel_w = ld_dev(r_w + tid);
   }
   if (blockIdx.x == 0) {
     clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags);
@@ -1350,9 +1617,9 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
   // routing tables at the start of dynamic LDS, item LDS after them
   uint8_t* item_smem = smem + P.lds_routing;
-  ItemTrace tr_route;
-  const RouteTab RT = (P.flags & F_ROUTE) ? build_routing(P, A.topk_idx, A.topk_w, smem, item_smem, true)
-                                          : build_routing(P, A.idx_in, A.w_in, smem, item_smem, false);
+  const RouteTab RT = wave_routing
+                          ? build_routing_wave(P, (sel_e >= 0 && sel_e < P.E) ? sel_e : -1, sel_w, smem)
+                          : build_routing(P, r_idx, r_w, smem, item_smem, (P.flags & F_ROUTE) != 0);
   tr_route.done(A, P, P.n_pre + P.max_act * (gateup_tiles_per_expert(P) + down_tiles_per_expert(P)) + P.n_cb +
                           blockIdx.x, 8);
   const int nact = RT.nact;

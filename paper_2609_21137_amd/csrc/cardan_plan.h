@@ -38,6 +38,8 @@ constexpr int kRowsRouter = 64;     // hidden rows per router / shared-projectio
 constexpr int kColsPerGroup = 256;  // output columns per expert tile (4 waves x 64)
 constexpr int kTokPass = 16;        // token slots per MFMA pass (N of 16x16x32)
 constexpr int kMaxE = 1024, kMaxK = 32, kMaxR = 512, kMaxB = 64;
+constexpr int kCombineChunk = 16;  // terms per load batch in the combine
+
 
 // flags of one call
 enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8 };
@@ -70,11 +72,27 @@ struct Plan {
   int n_rc, n_zc, n_sel, n_zr, n_pre;
   int n_rc_flags, n_zc_flags;  // flag slots (shape-wide maxima of n_rc, n_zc)
   // workspace byte offsets
-  size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_tick, o_gu_done, o_lr_tick, o_dn_done;  // counters
-  size_t o_rl, o_zp, o_z, o_gu, o_p, o_dn, o_uap, o_u, total;
+  size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_tick, o_gu_done, o_dn_done;  // counters
+  size_t o_rl, o_zp, o_z, o_gu, o_p, o_dn, o_uap, total;
   size_t lds_route, lds_expert;  // dynamic LDS of the two kernels
   size_t lds_routing;            // routing tables at the start of k_expert's dynamic LDS
 };
+
+// Combine item LDS: reduction area [kWG] float4, VQ down sums [kTokPass][256]
+// float, u operand rows [tpc][ld] uint4, term tables [tpc][k (nsdl + nsd)]
+// uint2, then the per-chunk partial sums (float4).
+inline __host__ __device__ size_t combine_part_offset(const Plan& P) {
+  const size_t ld = (size_t)(P.r + 31) / 32 * 8 + 1;
+  const size_t o = (size_t)kWG * 16 + (size_t)kTokPass * kColsPerGroup * 4 + (size_t)P.tpc * ld * 16 +
+                   (size_t)P.tpc * P.k * (P.nsdl + P.nsd) * 8;
+  return (o + 15) & ~(size_t)15;
+}
+inline __host__ __device__ size_t combine_lds(const Plan& P) {
+  const size_t nq = (size_t)(P.r + 31) / 32 * 8;
+  const size_t cu = P.r > 0 ? ((size_t)P.k * P.nsdl + kCombineChunk - 1) / kCombineChunk : 0;
+  const size_t cd = ((size_t)P.k * P.nsd + kCombineChunk - 1) / kCombineChunk;
+  return combine_part_offset(P) + (size_t)P.tpc * (nq * cu + 64 * cd) * 16;
+}
 
 __host__ __device__ inline int gateup_tiles_per_expert(const Plan& P) { return 2 * P.ncg * P.ns; }
 __host__ __device__ inline int down_tiles_per_expert(const Plan& P) {

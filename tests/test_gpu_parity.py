@@ -131,23 +131,42 @@ def test_separate_up_basis_and_expert_ffn_entry(C):
     assert torch.equal(y, y2) and torch.equal(idx, idx2)
 
 
-def test_given_routing_with_invalid_and_duplicate_entries(C):
+def _caller_routing(w, case):
+    if case == "one":  # batch 1 (staged token), one expert twice
+        return np.array([[4, 4]], dtype=np.int32), np.array([[0.3, 0.7]], dtype=np.float32)
+    if case == "few":  # 6 selections: one wave builds the routing tables
+        idx = np.array([[3, 5], [7, 7], [-1, w.E + 3]], dtype=np.int32)
+        wts = np.array([[0.6, 0.4], [0.25, 0.75], [0.5, 0.5]], dtype=np.float32)
+        return idx, wts
+    # 80 selections (the block-wide builder): random experts with repeats
+    # within a token, negative and too-large indices
+    rng = np.random.default_rng(11)
+    idx = rng.integers(0, w.E, size=(40, 2)).astype(np.int32)
+    idx[rng.random(idx.shape) < 0.1] = -1
+    idx[rng.random(idx.shape) < 0.05] = w.E + 1
+    idx[::7, 1] = idx[::7, 0]
+    wts = rng.random(idx.shape).astype(np.float32)
+    return idx, wts
+
+
+@pytest.mark.parametrize("case", ["one", "few", "many"])
+def test_given_routing_with_invalid_and_duplicate_entries(C, case):
     """vq_lr_expert_ffn with caller routing: an out-of-range index contributes
     nothing; a repeated expert counts twice."""
     w = TINY
     L = synth.workload_layer(w)
-    x_bits = synth.make_input(w.H, 3, seed=6)
     shape = C.shape_of(w)
     DL = C.DeviceLayer.from_numpy(L)
-    idx = np.array([[3, 5], [7, 7], [-1, 2]], dtype=np.int32)
-    wts = np.array([[0.6, 0.4], [0.25, 0.75], [0.5, 0.5]], dtype=np.float32)
+    idx, wts = _caller_routing(w, case)
+    x_bits = synth.make_input(w.H, idx.shape[0], seed=6)
     x = C.bf16_tensor(x_bits)
     z = C.shared_proj(shape, x, DL.tensors["U_gate"])
     y = C.vq_lr_expert_ffn(shape, x, torch.from_numpy(idx).cuda(),
                            torch.from_numpy(wts).cuda(), z, DL)
     torch.cuda.synchronize()
-    keep = np.where(idx >= 0, idx, 0)
-    wref = np.where(idx >= 0, wts, 0.0).astype(np.float64)
+    ok = (idx >= 0) & (idx < w.E)
+    keep = np.where(ok, idx, 0)
+    wref = np.where(ok, wts, 0.0).astype(np.float64)
     y_ref = O.expert_ffn(x_bits, keep, wref, L, w.d)
     err = np.abs(y.cpu().numpy() - y_ref).max() / np.abs(y_ref).max()
     assert err <= HEADROOM, err
@@ -234,3 +253,29 @@ def test_rmsnorm(C):
     ref = O.rmsnorm(y, 1e-6)
     # within one bf16 rounding step of the float64 value
     assert np.all(np.abs(got - ref) <= np.abs(ref) * 2.0 ** -8 + 1e-30)
+
+
+@pytest.mark.parametrize("k", [4, 6])
+def test_exact_and_single_precision_ties(C, k):
+    """Logits that tie exactly (lower index first) and logits that differ only
+    below single precision (the exact comparison decides): the top-k must
+    still match the oracle element for element."""
+    import dataclasses
+    w = dataclasses.replace(TINY, top_k=k)
+    L = synth.workload_layer(w)
+    H, E = w.H, w.E
+    wr = np.zeros((H, E), dtype=np.float64)
+    wr[0] = [1.0, 1.0, 1.0, 0.5, 0.25, 0.25, -1.0, 0.0]
+    wr[1, 2] = 1.0
+    L["router_w"] = synth.to_bf16_bits(wr)
+    L["router_bias"] = np.zeros(E, dtype=np.float32)
+    xv = np.zeros((2, H), dtype=np.float64)
+    xv[:, 0] = 1.0
+    xv[:, 1] = 2.0 ** -30   # expert 2's logit is 1 + 2^-30: above 1 in float64, equal in float32
+    x_bits = synth.to_bf16_bits(xv)
+    y_ref, idx_ref, a_ref, _ = O.moe_layer_factored(x_bits, L, w.top_k, w.d)
+    assert list(idx_ref[0][:3]) == [2, 0, 1]
+    y, idx, wt = _run_layer(C, w, L, x_bits)
+    assert np.array_equal(idx, idx_ref), (idx, idx_ref)
+    assert np.abs(wt - a_ref).max() <= 1e-5
+    assert np.abs(y - y_ref).max() <= TOL * np.abs(y_ref).max()
