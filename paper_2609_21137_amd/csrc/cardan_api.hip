@@ -194,14 +194,12 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);
   P.o_rc_flag = o; o = align256(o + (size_t)P.n_rc_flags * 4);
   P.o_zc_flag = o; o = align256(o + (size_t)P.n_zc_flags * 4);
-  P.o_gu_tick = o; o = align256(o + (size_t)P.E * ceil_div(P.I, kColsPerGroup) * 4);
-  P.o_gu_done = o; o = align256(o + (size_t)P.E * 4);
-  P.o_dn_done = o; o = align256(o + (size_t)P.E * (ceil_div(P.H, kColsPerGroup) + 1) * 4);
+  P.o_gu_tick = o; o = align256(o + (size_t)P.E * ceil_div(P.I, kColsPerGroup) * kTickPad * 4);
+  P.o_dn_done = o; o = align256(o + (size_t)P.E * (ceil_div(P.H, kColsPerGroup) + 1) * kTickPad * 4);
   P.o_rl = o; o = align256(o + (size_t)P.nch_r * B * P.E * 8);
   P.o_zp = o; o = align256(o + (size_t)2 * P.nch_z * B * P.r * 4);
   P.o_z = o; o = align256(o + (size_t)2 * B * P.r * 4);
   P.o_gu = o; o = align256(o + (size_t)P.S * 2 * P.ns * P.I * 4);
-  P.o_p = o; o = align256(o + (size_t)P.S * P.I * 4);
   P.o_dn = o; o = align256(o + (size_t)P.nsd * P.S * P.H * 4);
   P.o_uap = o; o = align256(o + (size_t)P.nsdl * P.S * P.r * 4);
   P.total = o;

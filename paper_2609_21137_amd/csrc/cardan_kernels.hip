@@ -959,45 +959,10 @@ __device__ __forceinline__ void stage_bf16(uint4* ops, int ld, int nt, int n8, F
   }
 }
 
-// Stages float32 activation rows (produced in this kernel: device-scope
-// loads) as bf16 hi/lo pairs: ops[t * ld + 2 j] (hi) and [.. + 1] (lo) hold
-// inputs 8 j .. 8 j + 7 of row src(t), value = hi + lo.
-template <typename F>
-__device__ __forceinline__ void stage_split(const WsRead& ws, uint4* ops, int ld, int nt, int n8, F src) {
-  // four groups per thread per round, their loads in flight together
-  for (int i0 = threadIdx.x; i0 < nt * n8; i0 += 4 * kWG) {
-    float4 v[4][2];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u * kWG;
-      const int ii = min(i, nt * n8 - 1);
-      const uint32_t o = i < nt * n8 ? ws.off(src(ii / n8) + 8 * (ii % n8)) : kOob;
-      v[u][0] = ws.f4(o);
-      v[u][1] = ws.f4(o + 16);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u * kWG;
-      if (i >= nt * n8) continue;
-      const int t = i / n8, j = i % n8;
-      const float f[8] = {v[u][0].x, v[u][0].y, v[u][0].z, v[u][0].w, v[u][1].x, v[u][1].y, v[u][1].z, v[u][1].w};
-      uint32_t h[8], lw[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        h[e] = rne_bf16(f[e]);
-        lw[e] = rne_bf16(f[e] - bf(h[e]));
-      }
-      ops[t * ld + 2 * j] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                                       h[6] | (h[7] << 16));
-      ops[t * ld + 2 * j + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
-                                           lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
-    }
-  }
-}
-
 // Writes 4 consecutive fp32 values as bf16 hi/lo halves of an LDS operand
-// row laid out as stage_split does: quad q of a row is half (q & 1) of the
-// uint4 pair at [2 (q >> 1)] (hi) and [2 (q >> 1) + 1] (lo).
+// row of float32 activations (value = hi + lo): inputs 8 j .. 8 j + 7 sit in
+// the uint4 pair [2 j] (hi) and [2 j + 1] (lo), so quad q is half (q & 1) of
+// the pair at [2 (q >> 1)].
 __device__ __forceinline__ void put_split_quad(uint4* row, int q, float4 v) {
   const float f[4] = {v.x, v.y, v.z, v.w};
   uint32_t h[4], lw[4];
@@ -1011,6 +976,57 @@ __device__ __forceinline__ void put_split_quad(uint4* row, int q, float4 v) {
   *hi = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
   *lo = make_uint2(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16));
 }
+
+// Down operand rows from the gate/up partial sums: p = silu(g) * u for token
+// rows [0, nt) (slots slot0 + t) on I columns col0 + [0, 4 nquad), each sum
+// over the ns splits in split order, staged as bf16 hi/lo quads. U units
+// (token, quad) per thread per round and NSC splits per load batch keep 16
+// loads in flight.
+template <int U, int NSC>
+__device__ __forceinline__ void stage_silu(const WsRead& ws, const Plan& P, uint4* ops, int ld, int nt, int nquad,
+                                           int slot0, int col0) {
+  const int ns = P.ns, I = P.I, n = nt * nquad;
+  for (int i0 = threadIdx.x; i0 < n; i0 += U * kWG) {
+    float4 g[U], u[U];
+    uint32_t base[U];
+#pragma unroll
+    for (int uu = 0; uu < U; ++uu) {
+      const int i = i0 + uu * kWG, ii = min(i, n - 1);
+      base[uu] = i < n ? (uint32_t)(P.o_gu + ((size_t)(slot0 + ii / nquad) * 2 * ns * I + col0 + 4 * (ii % nquad)) * 4)
+                       : kOob;
+      g[uu] = u[uu] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    for (int s0 = 0; s0 < ns; s0 += NSC) {
+      float4 v[U][2][NSC];
+#pragma unroll
+      for (int uu = 0; uu < U; ++uu)
+#pragma unroll
+        for (int pj = 0; pj < 2; ++pj)
+#pragma unroll
+          for (int sc = 0; sc < NSC; ++sc)
+            v[uu][pj][sc] = ws.f4(s0 + sc < ns ? base[uu] + (uint32_t)((pj * ns + s0 + sc) * I * 4) : kOob);
+#pragma unroll
+      for (int uu = 0; uu < U; ++uu)
+#pragma unroll
+        for (int sc = 0; sc < NSC; ++sc) {
+          g[uu] = make_float4(g[uu].x + v[uu][0][sc].x, g[uu].y + v[uu][0][sc].y, g[uu].z + v[uu][0][sc].z,
+                              g[uu].w + v[uu][0][sc].w);
+          u[uu] = make_float4(u[uu].x + v[uu][1][sc].x, u[uu].y + v[uu][1][sc].y, u[uu].z + v[uu][1][sc].z,
+                              u[uu].w + v[uu][1][sc].w);
+        }
+    }
+#pragma unroll
+    for (int uu = 0; uu < U; ++uu) {
+      const int i = i0 + uu * kWG;
+      if (i >= n) continue;
+      const float4 x = g[uu], y = u[uu];
+      put_split_quad(ops + (i / nquad) * ld, i % nquad,
+                     make_float4(x.x / (1.0f + expf(-x.x)) * y.x, x.y / (1.0f + expf(-x.y)) * y.y,
+                                 x.z / (1.0f + expf(-x.z)) * y.z, x.w / (1.0f + expf(-x.w)) * y.w));
+    }
+  }
+}
+
 
 __device__ __forceinline__ float4 fma4(float w, float4 v, float4 a) {
   return make_float4(fmaf(w, v.x, a.x), fmaf(w, v.y, a.y), fmaf(w, v.z, a.z), fmaf(w, v.w, a.w));
@@ -1275,38 +1291,9 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
     trace_mark(2);
   }
 
-  // The last of the 2 ns tiles of (a, cg) forms p = silu(g) * u for the
-  // expert's tokens on these 256 columns from all partial sums, once, and
-  // counts the column group done for the expert.
-  __shared__ int s_last;
-  int* tick = wsp<int>(A, P.o_gu_tick) + a * P.ncg + cg;
-  const bool last = last_of(tick, 2 * P.ns, &s_last);
-  trace_mark(3);
-  if (!last) return;
-  const int ns = P.ns, nq = kColsPerGroup / 4, cbase = cg * kColsPerGroup;
-  float* pbuf = wsp<float>(A, P.o_p);
-  float4* red = reinterpret_cast<float4*>(smem);
-  const WsRead ws(A, P);
-  split_sum<2, 8>(
-      ws, R.ne * nq, ns, red,
-      [&](int item, int sp, uint32_t(&off)[2], float& wt) {
-        const int t = item / nq, col = cbase + 4 * (item % nq);
-        const bool ok = sp >= 0 && col < I;
-        const uint32_t o = (uint32_t)(P.o_gu + (((size_t)(R.s0 + t) * 2 * ns + max(sp, 0)) * I + min(col, I - 4)) * 4);
-        off[0] = ok ? o : kOob;
-        off[1] = ok ? o + (uint32_t)ns * I * 4 : kOob;
-        wt = ok ? 1.f : 0.f;
-      },
-      [&](int item, const float4(&gsum)[2]) {
-        const int t = item / nq, col = cbase + 4 * (item % nq);
-        if (col >= I) return;
-        const float4 g = gsum[0], u = gsum[1];
-        st_dev4(pbuf + (size_t)(R.s0 + t) * I + col,
-                make_float4(g.x / (1.0f + expf(-g.x)) * u.x, g.y / (1.0f + expf(-g.y)) * u.y,
-                            g.z / (1.0f + expf(-g.z)) * u.z, g.w / (1.0f + expf(-g.w)) * u.w));
-      });
-  if (threadIdx.x == 0) *tick = 0;
-  publish(wsp<int>(A, P.o_gu_done) + R.e);
+  // counts the tile done for (a, cg); the down tiles form p = silu(g) * u
+  // from the 2 ns partial sums of their columns
+  publish(wsp<int>(A, P.o_gu_tick) + (a * P.ncg + cg) * kTickPad);
 }
 
 // Down tile (a, cgx, s) over split s of I, 256 output columns: for cgx <
@@ -1315,22 +1302,31 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
 // K-step are 16x the code bytes). Weight loads are issued before waiting
 // for the expert's p.
 template <typename Prime, typename Stage, typename Run, typename Dst>
-__device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Routing& R, int ks0, int ks1,
+__device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Routing& R, int a, int ks0, int ks1,
                                           int c0, int n_out, Prime prime, Stage stage, Run run, Dst dst,
                                           uint8_t* smem) {
   prime();
-  wait_geq(A, wsp<int>(A, P.o_gu_done) + R.e, P.ncg);
-  const int I = P.I;
+  // every gate/up tile of the column groups holding inputs [32 ks0, 32 ks1)
+  const int cg0 = ks0 * 32 / kColsPerGroup, ncgw = (ks1 * 32 - 1) / kColsPerGroup - cg0 + 1;
+  const int* tick = wsp<const int>(A, P.o_gu_tick) + (a * P.ncg + cg0) * kTickPad;
+  wait_all(A, ncgw, [&](int i) { return ld_dev(tick + i * kTickPad) >= 2 * P.ns; });
   const int ld = (ks1 - ks0) * 8 + 1;
   uint4* ps = reinterpret_cast<uint4*>(smem);
-  const float* pbuf = wsp<const float>(A, P.o_p);
+  const WsRead ws(A, P);
   for (int tg = 0; tg < R.ne; tg += P.nt_max) {
     const int nt = min(P.nt_max, R.ne - tg);
     if (tg > 0) prime();
     __syncthreads();
     stage();
-    stage_split(WsRead(A, P), ps, ld, nt, (ks1 - ks0) * 4,
-                [&](int t) { return pbuf + (size_t)(R.s0 + tg + t) * I + ks0 * 32; });
+    const int nquad = (ks1 - ks0) * 8, slot0 = R.s0 + tg, col0 = ks0 * 32;
+    if (P.ns <= 1)
+      stage_silu<8, 1>(ws, P, ps, ld, nt, nquad, slot0, col0);
+    else if (P.ns <= 2)
+      stage_silu<4, 2>(ws, P, ps, ld, nt, nquad, slot0, col0);
+    else if (P.ns <= 4)
+      stage_silu<2, 4>(ws, P, ps, ld, nt, nquad, slot0, col0);
+    else
+      stage_silu<1, 8>(ws, P, ps, ld, nt, nquad, slot0, col0);
     __syncthreads();
     trace_mark(0);
     f32x4 acc[4];
@@ -1351,7 +1347,7 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
   VqPipe<D, 2, kPdVq> pipe;
   uint4 bk;
-  down_body(P, A, R, ks0, ks1, c0, H,
+  down_body(P, A, R, a, ks0, ks1, c0, H,
             [&]() {
               bk = book_load<D>(A.L.cb_down, P.K);
               __builtin_amdgcn_sched_barrier(0);
@@ -1360,7 +1356,7 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
             [&]() { book_store<D>(cbs, bk); },
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs, ps, ld, ks0, nt, acc); },
             [&](int slot) { return dn + (size_t)slot * H; }, smem);
-  publish(wsp<int>(A, P.o_dn_done) + R.e * (P.ncgh + 1) + cgx);
+  publish(wsp<int>(A, P.o_dn_done) + (R.e * (P.ncgh + 1) + cgx) * kTickPad);
 }
 
 // Low-rank down tile (a, cgr, s): partial A_e^T p over split s of I. The
@@ -1375,11 +1371,11 @@ __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, i
   const uint16_t* Ae = A.L.A_down + (size_t)R.e * I * r;
   float* uap = wsp<float>(A, P.o_uap);
   DensePipe<2, kPdDense> pipe;
-  down_body(P, A, R, ks0, ks1, c0, r, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); }, [&]() {},
+  down_body(P, A, R, a, ks0, ks1, c0, r, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); }, [&]() {},
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(ps, ld, ks0, nt, acc); },
             [&](int slot) { return uap + ((size_t)s * S + slot) * r; }, smem);
   // the combine sums the nsdl partials of u_e itself
-  publish(wsp<int>(A, P.o_dn_done) + R.e * (P.ncgh + 1) + P.ncgh);
+  publish(wsp<int>(A, P.o_dn_done) + (R.e * (P.ncgh + 1) + P.ncgh) * kTickPad);
 }
 
 // Combine tile (cgy, tq): output columns [256 cgy, +256) of tokens
@@ -1433,7 +1429,7 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
       const int c = i % ncol, tj = i / ncol;
       const int sl = s_slot[tj];
       if (sl < 0) return true;
-      return ld_dev(dnd + s_e_slot[sl] * per_e + (c == 0 ? cgy : P.ncgh)) >= (c == 0 ? nsd : P.ncgr * nsdl);
+      return ld_dev(dnd + (s_e_slot[sl] * per_e + (c == 0 ? cgy : P.ncgh)) * kTickPad) >= (c == 0 ? nsd : P.ncgr * nsdl);
     });
   }
   trace_mark(2);
@@ -1552,8 +1548,8 @@ __device__ __forceinline__ GateUpTile gateup_at(const Plan& P, int p, int nact, 
 // ===========================================================================
 // Each kernel clears the counters of the other kernel of the call before
 // any of them is used again (the stream orders the two kernels).
-__device__ __forceinline__ void clear_ints(int* p, int n) {
-  for (int i = threadIdx.x; i < n; i += kWG) p[i] = 0;
+__device__ __forceinline__ void clear_ints(int* p, int n, int stride = 1) {
+  for (int i = threadIdx.x; i < n; i += kWG) p[i * stride] = 0;
 }
 
 // Routing-independent work and the routing itself: router chunks, z units,
@@ -1561,9 +1557,8 @@ __device__ __forceinline__ void clear_ints(int* p, int n) {
 __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   if (blockIdx.x == 0 && (P.flags & F_EXPERTS)) {
-    clear_ints(wsp<int>(A, P.o_gu_tick), P.E * P.ncg);
-    clear_ints(wsp<int>(A, P.o_gu_done), P.E);
-    clear_ints(wsp<int>(A, P.o_dn_done), P.E * (P.ncgh + 1));
+    clear_ints(wsp<int>(A, P.o_gu_tick), P.E * P.ncg, kTickPad);
+    clear_ints(wsp<int>(A, P.o_dn_done), P.E * (P.ncgh + 1), kTickPad);
   }
   for (int j = blockIdx.x; j < P.n_pre; j += gridDim.x) {
     __syncthreads();

@@ -48,6 +48,7 @@ enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8 };
 // count of timed-out waits
 enum { C_ERR = 0, C_NUM };
 constexpr int kCtrStride = 16;      // ints between counters
+constexpr int kTickPad = 32;        // ints between the tile counters (one 128-byte line each)
 
 struct Plan {
   int H, I, E, k, d, K, r, B;
@@ -72,8 +73,8 @@ struct Plan {
   int n_rc, n_zc, n_sel, n_zr, n_pre;
   int n_rc_flags, n_zc_flags;  // flag slots (shape-wide maxima of n_rc, n_zc)
   // workspace byte offsets
-  size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_tick, o_gu_done, o_dn_done;  // counters
-  size_t o_rl, o_zp, o_z, o_gu, o_p, o_dn, o_uap, total;
+  size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_tick, o_dn_done;  // counters
+  size_t o_rl, o_zp, o_z, o_gu, o_dn, o_uap, total;
   size_t lds_route, lds_expert;  // dynamic LDS of the two kernels
   size_t lds_routing;            // routing tables at the start of k_expert's dynamic LDS
 };
