@@ -192,8 +192,8 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.n_zc_flags = ceil_div(2 * ceil_div(P.r, 64) * P.nch_z, 4);
   size_t o = 0;
   P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);
-  P.o_rc_flag = o; o = align256(o + (size_t)P.n_rc_flags * 4);
-  P.o_zc_flag = o; o = align256(o + (size_t)P.n_zc_flags * 4);
+  P.o_rc_flag = o; o = align256(o + (size_t)P.n_rc_flags * kTickPad * 4);
+  P.o_zc_flag = o; o = align256(o + (size_t)P.n_zc_flags * kTickPad * 4);
   P.o_gu_tick = o; o = align256(o + (size_t)P.E * ceil_div(P.I, kColsPerGroup) * kTickPad * 4);
   P.o_dn_done = o; o = align256(o + (size_t)P.E * (ceil_div(P.H, kColsPerGroup) + 1) * kTickPad * 4);
   P.o_rl = o; o = align256(o + (size_t)P.nch_r * B * P.E * 8);

@@ -336,7 +336,7 @@ __device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c,
     __syncthreads();
   }
   trace_mark(2);
-  set_flag(wsp<int>(A, P.o_rc_flag) + item);
+  set_flag(wsp<int>(A, P.o_rc_flag) + item * kTickPad);
 }
 
 // Routing tables of a call in LDS. Every workgroup of k_expert rebuilds them
@@ -612,7 +612,7 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
   // the bias is read before the wait so its latency is hidden
   const float b0 = (A.L.router_bias && tid < E) ? A.L.router_bias[tid] : 0.0f;
   const int* rcf = wsp<const int>(A, P.o_rc_flag);
-  wait_all(A, P.n_rc, [&](int i) { return ld_dev(rcf + i) != 0; });
+  wait_all(A, P.n_rc, [&](int i) { return ld_dev(rcf + i * kTickPad) != 0; });
   const double* rl = wsp<const double>(A, P.o_rl);
   double own = 0.0;  // logit of expert tid
   for (int e = tid; e < E; e += kWG) {
@@ -700,7 +700,7 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
 
 __device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
   const int* zcf = wsp<const int>(A, P.o_zc_flag);
-  wait_all(A, P.n_zc, [&](int f) { return ld_dev(zcf + f) != 0; });
+  wait_all(A, P.n_zc, [&](int f) { return ld_dev(zcf + f * kTickPad) != 0; });
   const int o = i * kWG + threadIdx.x;
   const int B = P.B, r = P.r;
   if (o < 2 * B * r) {
@@ -1132,7 +1132,7 @@ __device__ void item_z(const Plan& P, const Args& A, int j, uint8_t* smem) {
       store_acc(acc, nt, c0, r, [&](int t) { return zp + (((size_t)pj * P.nch_z + s) * B + tg + t) * r; });
     }
   }
-  set_flag(wsp<int>(A, P.o_zc_flag) + j);
+  set_flag(wsp<int>(A, P.o_zc_flag) + j * kTickPad);
 }
 
 // ===========================================================================
@@ -1582,8 +1582,8 @@ __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
 
 // Clears the routing kernel's counters (after calls that run k_route alone).
 __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
-  clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags);
-  clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags);
+  clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags, kTickPad);
+  clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags, kTickPad);
 }
 
 // Expert work of the active experts (count published by k_route): gate/up
@@ -1607,8 +1607,8 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     sel_w = ld_dev(r_w + tid);
   }
   if (blockIdx.x == 0) {
-    clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags);
-    clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags);
+    clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags, kTickPad);
+    clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags, kTickPad);
   }
   // routing tables at the start of dynamic LDS, item LDS after them
   uint8_t* item_smem = smem + P.lds_routing;
