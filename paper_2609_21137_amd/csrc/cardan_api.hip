@@ -176,6 +176,9 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   auto down_fits = [&](int n) {
     return (size_t)P.nt_max * (ks_max(KSD, n) * 8 + 1) * 16 + kWG * 2 * 16 <= kLdsBudget;
   };
+  // low-rank down tiles cover at least kLrDownSteps K-steps (their weights
+  // load while they wait): fewer partials of u_e for the combine to sum
+  P.nsdl = std::min(P.nsdl, ceil_div(KSD, kLrDownSteps));
   while (P.nsd < KSD && !down_fits(P.nsd)) ++P.nsd;
   while (P.nsdl < KSD && !down_fits(P.nsdl)) ++P.nsdl;
   P.n_cb = P.ncgh * ceil_div(B, P.tpc);

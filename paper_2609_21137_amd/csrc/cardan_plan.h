@@ -39,6 +39,7 @@ constexpr int kColsPerGroup = 256;  // output columns per expert tile (4 waves x
 constexpr int kTokPass = 16;        // token slots per MFMA pass (N of 16x16x32)
 constexpr int kMaxE = 1024, kMaxK = 32, kMaxR = 512, kMaxB = 64;
 constexpr int kCombineChunk = 16;  // terms per load batch in the combine
+constexpr int kLrDownSteps = 4;    // K-steps of a low-rank down tile when the plan would cut finer
 
 
 // flags of one call
