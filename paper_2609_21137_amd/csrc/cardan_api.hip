@@ -161,6 +161,17 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
     if (items <= 512.0 || tile >= 128.0 * 1024) break;
     tile *= 1.05;
   }
+  // Latency shape: if the item count still fits the nominal grid, code
+  // splits of at most one pipeline prime (kPdVq K-steps) and low-rank splits
+  // of kPdDense steps, so no tile streams refills after its prime.
+  if (P.ns > 1) {
+    const int nv = std::max(P.ns_v, ceil_div(KSX, kPdVq)), nl = KSZ > 0 ? ceil_div(KSZ, kPdDense) : 0;
+    const double items = exp_act * (2.0 * P.ncg * (nv + nl) + P.ncgh * P.nsd + P.ncgr * P.nsdl);
+    if (items <= 512.0) {
+      P.ns_v = nv;
+      P.ns = nv + nl;
+    }
+  }
   // token rows staged per pass: halve (down to 4) before splitting K further
   // to fit the operand staging into LDS; experts with more tokens than one
   // pass stream their weights again per pass (rare at these sizes)

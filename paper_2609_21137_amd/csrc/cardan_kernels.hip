@@ -838,6 +838,14 @@ struct VqPipe {
   }
   __device__ __forceinline__ void run(const uint4* cb_s, const uint4* ops, int ops_ld, int ops_ks0,
                                       int nt, f32x4 acc[4]) {
+    if (nks <= PD) {  // every step was primed: no refills
+#pragma unroll
+      for (int u = 0; u < PD; ++u) {
+        if (u < nks) step(ks0 + u, buf[u], cb_s, ops, ops_ld, ops_ks0, nt, acc);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      return;
+    }
     for (int i0 = 0; i0 < nks; i0 += PD) {
 #pragma unroll
       for (int u = 0; u < PD; ++u) {
@@ -913,6 +921,12 @@ struct DensePipe {
     sched_step<NOPS, 4 * NOPS>();
   }
   __device__ __forceinline__ void run(const uint4* ops, int ops_ld, int ops_ks0, int nt, f32x4 acc[4]) {
+    if (nks <= PD) {  // every step was primed: no refills
+#pragma unroll
+      for (int u = 0; u < PD; ++u)
+        if (u < nks) step(ks0 + u, buf[u], ops, ops_ld, ops_ks0, nt, acc);
+      return;
+    }
     for (int i0 = 0; i0 < nks; i0 += PD) {
 #pragma unroll
       for (int u = 0; u < PD; ++u) {
@@ -925,8 +939,6 @@ struct DensePipe {
   }
 };
 
-constexpr int kPdVq = 16;    // code K-steps in flight per wave (256 B each)
-constexpr int kPdDense = 2;  // dense K-steps in flight per wave (4 KB each)
 
 __device__ __forceinline__ void zero_acc(f32x4 acc[4]) {
 #pragma unroll
@@ -1546,6 +1558,27 @@ __device__ __forceinline__ GateUpTile gateup_at(const Plan& P, int p, int nact, 
 // ===========================================================================
 // the two persistent kernels of a layer call
 // ===========================================================================
+// Brings the 7 64-byte lines of the kernel arguments (Plan, then Args) into
+// the scalar cache with loads issued back to back and one wait, so the
+// fields read later hit instead of missing one line at a time. One asm
+// statement: the loads' destinations are clobbered until the wait.
+static_assert(sizeof(Plan) + sizeof(Args) > 6 * 64 && sizeof(Plan) + sizeof(Args) <= 7 * 64,
+              "kernel arguments span 7 lines; update warm_kernargs");
+__device__ __forceinline__ void warm_kernargs() {
+#if __HIP_DEVICE_COMPILE__
+  asm volatile(
+      "s_load_dword s90, %0, 0x0\n\t"
+      "s_load_dword s91, %0, 0x40\n\t"
+      "s_load_dword s92, %0, 0x80\n\t"
+      "s_load_dword s93, %0, 0xc0\n\t"
+      "s_load_dword s94, %0, 0x100\n\t"
+      "s_load_dword s95, %0, 0x140\n\t"
+      "s_load_dword s96, %0, 0x180\n\t"
+      "s_waitcnt lgkmcnt(0)" ::"s"(__builtin_amdgcn_kernarg_segment_ptr())
+      : "s90", "s91", "s92", "s93", "s94", "s95", "s96", "memory");
+#endif
+}
+
 // Each kernel clears the counters of the other kernel of the call before
 // any of them is used again (the stream orders the two kernels).
 __device__ __forceinline__ void clear_ints(int* p, int n, int stride = 1) {
@@ -1556,6 +1589,7 @@ __device__ __forceinline__ void clear_ints(int* p, int n, int stride = 1) {
 // per-token select (the last one groups the slots), z reduce.
 __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  warm_kernargs();
   if (blockIdx.x == 0 && (P.flags & F_EXPERTS)) {
     clear_ints(wsp<int>(A, P.o_gu_tick), P.E * P.ncg, kTickPad);
     clear_ints(wsp<int>(A, P.o_dn_done), P.E * (P.ncgh + 1), kTickPad);
@@ -1593,6 +1627,7 @@ template <int D>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ uint4 cbs[256];  // the code book of the current item (zero-padded to 256 words)
+  warm_kernargs();
   const int tid = threadIdx.x;
   ItemTrace tr_route;
   // Small batches: the selections, one per lane of wave 0, are built into
@@ -1620,32 +1655,38 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   const int nact = RT.nact;
   const int tgu = gateup_tiles_per_expert(P), tdn = down_tiles_per_expert(P);
   const int s_vq = P.ns_v;  // first gate/up split without code steps
-  const int n_items = nact * (tgu + tdn) + P.n_cb;
-  for (int jp = blockIdx.x; jp < n_items; jp += gridDim.x) {
+  const int n_gu = nact * tgu, n_dn = nact * tdn, n_items = n_gu + n_dn + P.n_cb;
+  // Items in index order, one loop per kind (the kinds are contiguous ranges):
+  // each loop's invariant set-up is computed only by workgroups that enter it.
+  int jp = blockIdx.x;
+  for (; jp < n_gu; jp += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
-    int j = jp, kind = 4;
-    if (j < nact * tgu) {
-      const GateUpTile t = gateup_at(P, j, nact, s_vq, gridDim.x);
-      // a tile holding both code and low-rank steps runs the low-rank part
-      // first in the second half of the grid, so the two workgroups sharing
-      // a CU overlap LDS-bound and HBM-bound phases
-      const bool lr_first = (int)(jp % gridDim.x) >= (int)(gridDim.x >> 1);
-      item_gateup<D>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem);
-    } else if ((j -= nact * tgu) < nact * tdn) {
-      const int a = j / tdn, rem = j % tdn, nvq = P.ncgh * P.nsd;
-      if (rem < nvq) {
-        kind = 5;
-        item_down_vq<D>(P, A, RT, a, rem / P.nsd, rem % P.nsd, cbs, item_smem);
-      } else {
-        kind = 6;
-        item_down_lr(P, A, RT, a, (rem - nvq) / P.nsdl, (rem - nvq) % P.nsdl, item_smem);
-      }
+    const GateUpTile t = gateup_at(P, jp, nact, s_vq, gridDim.x);
+    // a tile holding both code and low-rank steps runs the low-rank part
+    // first in the second half of the grid, so the two workgroups sharing a
+    // CU overlap LDS-bound and HBM-bound phases
+    const bool lr_first = (int)(jp % gridDim.x) >= (int)(gridDim.x >> 1);
+    item_gateup<D>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem);
+    tr.done(A, P, P.n_pre + jp, 4);
+  }
+  for (; jp < n_gu + n_dn; jp += gridDim.x) {
+    __syncthreads();
+    ItemTrace tr;
+    const int j = jp - n_gu, a = j / tdn, rem = j % tdn, nvq = P.ncgh * P.nsd;
+    if (rem < nvq) {
+      item_down_vq<D>(P, A, RT, a, rem / P.nsd, rem % P.nsd, cbs, item_smem);
+      tr.done(A, P, P.n_pre + jp, 5);
     } else {
-      kind = 7;
-      item_combine(P, A, RT, j - nact * tdn, item_smem);
+      item_down_lr(P, A, RT, a, (rem - nvq) / P.nsdl, (rem - nvq) % P.nsdl, item_smem);
+      tr.done(A, P, P.n_pre + jp, 6);
     }
-    tr.done(A, P, P.n_pre + jp, kind);
+  }
+  for (; jp < n_items; jp += gridDim.x) {
+    __syncthreads();
+    ItemTrace tr;
+    item_combine(P, A, RT, jp - n_gu - n_dn, item_smem);
+    tr.done(A, P, P.n_pre + jp, 7);
   }
 }
 

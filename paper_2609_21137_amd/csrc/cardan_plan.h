@@ -38,6 +38,8 @@ constexpr int kRowsRouter = 64;     // hidden rows per router / shared-projectio
 constexpr int kColsPerGroup = 256;  // output columns per expert tile (4 waves x 64)
 constexpr int kTokPass = 16;        // token slots per MFMA pass (N of 16x16x32)
 constexpr int kMaxE = 1024, kMaxK = 32, kMaxR = 512, kMaxB = 64;
+constexpr int kPdVq = 16;     // code K-steps in flight per wave (4 B per lane each)
+constexpr int kPdDense = 2;   // dense K-steps in flight per wave (4 KB each)
 constexpr int kCombineChunk = 16;  // terms per load batch in the combine
 constexpr int kLrDownSteps = 4;    // K-steps of a low-rank down tile when the plan would cut finer
 
