@@ -1594,27 +1594,36 @@ __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
     clear_ints(wsp<int>(A, P.o_gu_tick), P.E * P.ncg, kTickPad);
     clear_ints(wsp<int>(A, P.o_dn_done), P.E * (P.ncgh + 1), kTickPad);
   }
-  for (int j = blockIdx.x; j < P.n_pre; j += gridDim.x) {
+  // items in index order, one loop per kind (contiguous ranges)
+  const int e_rc = P.n_rc, e_zc = e_rc + P.n_zc, e_sel = e_zc + P.n_sel;
+  int j = blockIdx.x;
+  for (; j < e_rc; j += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
-    int jj = j, kind = 0;
-    if (jj < P.n_rc) {
-      item_router_chunk(P, A, jj, jj % P.nch_r, jj / P.nch_r, smem);
-    } else if ((jj -= P.n_rc) < P.n_zc) {
-      kind = 1;
-      item_z(P, A, jj, smem);
-    } else if ((jj -= P.n_zc) < P.n_sel) {
-      kind = 2;
-      item_select(P, A, jj, smem);
-    } else {
-      kind = 3;
-      item_z_reduce(P, A, jj - P.n_sel);
-    }
-    tr.done(A, P, j, kind);
+    item_router_chunk(P, A, j, j % P.nch_r, j / P.nch_r, smem);
+    tr.done(A, P, j, 0);
+  }
+  for (; j < e_zc; j += gridDim.x) {
+    __syncthreads();
+    ItemTrace tr;
+    item_z(P, A, j - e_rc, smem);
+    tr.done(A, P, j, 1);
+  }
+  for (; j < e_sel; j += gridDim.x) {
+    __syncthreads();
+    ItemTrace tr;
+    item_select(P, A, j - e_zc, smem);
+    tr.done(A, P, j, 2);
+  }
+  for (; j < P.n_pre; j += gridDim.x) {
+    __syncthreads();
+    ItemTrace tr;
+    item_z_reduce(P, A, j - e_sel);
+    tr.done(A, P, j, 3);
   }
 }
 
-// Clears the routing kernel's counters (after calls that run k_route alone).
+// Clears the routing kernel's flags (after calls that run k_route alone).
 __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
   clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags, kTickPad);
   clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags, kTickPad);
