@@ -762,20 +762,25 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
 
 constexpr int kSc1 = 16;  // cache policy operand of a device-scope (sc1) buffer access
 
-// Device-scope reads of workspace data written by other workgroups, through
-// one buffer resource over the workspace: the byte offset kOob (past the
-// workspace) reads zeros without a memory access, so a skipped term needs no
-// branch and every load of a batch issues back to back.
-struct WsRead {
+// Device-scope reads (and 16-byte writes) of workspace data handed between
+// workgroups, through one buffer resource over the workspace: the byte
+// offset kOob (past the workspace) reads zeros without a memory access, so a
+// skipped term needs no branch and every load of a batch issues back to back.
+struct WsAccess {
   rsrc_t rs;
   const uint8_t* base;
-  __device__ __forceinline__ WsRead(const Args& A, const Plan& P)
+  __device__ __forceinline__ WsAccess(const Args& A, const Plan& P)
       : rs(make_rsrc(A.ws, (uint32_t)P.total)), base(A.ws) {}
   __device__ __forceinline__ uint32_t off(const void* p) const {
     return (uint32_t)(reinterpret_cast<const uint8_t*>(p) - base);
   }
   __device__ __forceinline__ float4 f4(uint32_t o) const {
     return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, o, 0, kSc1));
+  }
+  // one 16-byte device-scope store (the producers' side of the hand-offs)
+  __device__ __forceinline__ void st4(uint32_t o, float4 v) const {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, o, 0, kSc1);
   }
 };
 
@@ -948,14 +953,14 @@ __device__ __forceinline__ void zero_acc(f32x4 acc[4]) {
 // Stores token rows 4g + i < nt of the wave's accumulators with device-scope
 // stores: row t goes to dst(t) + c0 + 4n (the 4 MFMAs' columns).
 template <typename F>
-__device__ __forceinline__ void store_acc(const f32x4 acc[4], int nt, int c0, int n_out, F dst) {
+__device__ __forceinline__ void store_acc(const WsAccess& ws, const f32x4 acc[4], int nt, int c0, int n_out, F dst) {
   const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
   const int col = c0 + 4 * n;
   if (col >= n_out) return;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int t = 4 * g + i;
-    if (t < nt) st_dev4(dst(t) + col, make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]));
+    if (t < nt) ws.st4(ws.off(dst(t) + col), make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]));
   }
 }
 
@@ -995,7 +1000,7 @@ __device__ __forceinline__ void put_split_quad(uint4* row, int q, float4 v) {
 // (token, quad) per thread per round and NSC splits per load batch keep 16
 // loads in flight.
 template <int U, int NSC>
-__device__ __forceinline__ void stage_silu(const WsRead& ws, const Plan& P, uint4* ops, int ld, int nt, int nquad,
+__device__ __forceinline__ void stage_silu(const WsAccess& ws, const Plan& P, uint4* ops, int ld, int nt, int nquad,
                                            int slot0, int col0) {
   const int ns = P.ns, I = P.I, n = nt * nquad;
   for (int i0 = threadIdx.x; i0 < n; i0 += U * kWG) {
@@ -1053,7 +1058,7 @@ __device__ __forceinline__ float4 fma4(float w, float4 v, float4 a) {
 // workspace byte offsets and weight (p < 0 or no term: kOob and 0); done(item,
 // sum) receives the result. All threads of the workgroup must call it.
 template <int NV, int BATCH, typename Term, typename Done>
-__device__ __forceinline__ void split_sum(const WsRead& ws, int items, int npair, float4* red, Term term, Done done) {
+__device__ __forceinline__ void split_sum(const WsAccess& ws, int items, int npair, float4* red, Term term, Done done) {
   const int tid = threadIdx.x;
   const int G = items >= kWG ? 1 : min(16, kWG / items);
   for (int base = 0; base < items * G; base += kWG) {
@@ -1141,7 +1146,7 @@ __device__ void item_z(const Plan& P, const Args& A, int j, uint8_t* smem) {
       f32x4 acc[4];
       zero_acc(acc);
       pipe.run(ops, ld, ks0, nt, acc);
-      store_acc(acc, nt, c0, r, [&](int t) { return zp + (((size_t)pj * P.nch_z + s) * B + tg + t) * r; });
+      store_acc(WsAccess(A, P), acc, nt, c0, r, [&](int t) { return zp + (((size_t)pj * P.nch_z + s) * B + tg + t) * r; });
     }
   }
   set_flag(wsp<int>(A, P.o_zc_flag) + j * kTickPad);
@@ -1299,7 +1304,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
     vq.run(cbs, xs, ldx, x0, nt, acc);
     trace_mark(1);
     if (!lr_first) lr.run(zs, ldz, z0, nt, acc);
-    store_acc(acc, nt, c0, I, [&](int t) { return gu + (((size_t)(R.s0 + tg + t) * 2 + pj) * P.ns + s) * I; });
+    store_acc(WsAccess(A, P), acc, nt, c0, I, [&](int t) { return gu + (((size_t)(R.s0 + tg + t) * 2 + pj) * P.ns + s) * I; });
     trace_mark(2);
   }
 
@@ -1324,7 +1329,7 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
   wait_all(A, ncgw, [&](int i) { return ld_dev(tick + i * kTickPad) >= 2 * P.ns; });
   const int ld = (ks1 - ks0) * 8 + 1;
   uint4* ps = reinterpret_cast<uint4*>(smem);
-  const WsRead ws(A, P);
+  const WsAccess ws(A, P);
   for (int tg = 0; tg < R.ne; tg += P.nt_max) {
     const int nt = min(P.nt_max, R.ne - tg);
     if (tg > 0) prime();
@@ -1344,7 +1349,7 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
     f32x4 acc[4];
     zero_acc(acc);
     run(ps, ld, nt, acc);
-    store_acc(acc, nt, c0, n_out, [&](int t) { return dst(R.s0 + tg + t); });
+    store_acc(ws, acc, nt, c0, n_out, [&](int t) { return dst(R.s0 + tg + t); });
   }
 }
 
@@ -1451,7 +1456,7 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
   // float4 of 4 columns per item. Each item's terms (selection-major) are
   // cut into chunks of kB taken by separate threads, so a thread has at most
   // kB loads in flight; the chunk sums are added in order afterwards.
-  const WsRead ws(A, P);
+  const WsAccess ws(A, P);
   const int nu = r > 0 ? nt * nq : 0, nd = nt * 64;
   const int cu = (ku + kB - 1) / kB, cd = (kd + kB - 1) / kB;
   const int n_units = nu * cu + nd * cd;
@@ -1459,7 +1464,8 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
   for (int unit = tid; unit < n_units; unit += kWG) {
     const bool isu = unit < nu * cu;
     const int uu = isu ? unit : unit - nu * cu;
-    const int it = isu ? uu / cu : uu / cd, c = isu ? uu % cu : uu % cd;
+    // chunk-major: neighbouring threads read neighbouring quads of one row
+    const int it = isu ? uu % nu : uu % nd, c = isu ? uu / nu : uu / nd;
     const int t = isu ? it / nq : it >> 6, q = isu ? it % nq : 0;
     const int col = cbase + 4 * (it & 63);
     // the column's (or rank quad's) byte offset within a term's row; a
@@ -1481,10 +1487,13 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
   __syncthreads();
   for (int item = tid; item < nu + nd; item += kWG) {
     const bool isu = item < nu;
-    const int nc = isu ? cu : cd;
-    const float4* pp = part + (isu ? item * cu : nu * cu + (item - nu) * cd);
+    const int nc = isu ? cu : cd, stride = isu ? nu : nd;
+    const float4* pp = part + (isu ? item : nu * cu + (item - nu));
     float4 acc = pp[0];
-    for (int c = 1; c < nc; ++c) acc = make_float4(acc.x + pp[c].x, acc.y + pp[c].y, acc.z + pp[c].z, acc.w + pp[c].w);
+    for (int c = 1; c < nc; ++c) {
+      const float4 q = pp[c * stride];
+      acc = make_float4(acc.x + q.x, acc.y + q.y, acc.z + q.z, acc.w + q.w);
+    }
     if (isu)
       put_split_quad(us + (item / nq) * ld, item % nq, acc);
     else
