@@ -201,6 +201,14 @@ EDGE_SHAPES = [
     ("max_batch_64", 256, 128, 16, 4, 8, 64, 8, 64),
     ("rank_512", 1024, 256, 8, 2, 8, 256, 512, 3),
     ("k32_wide", 512, 288, 40, 32, 4, 256, 40, 2),
+    # more than 256 experts: exact one-wave radix top-k (5 and 16 keys a lane)
+    ("e300_k8", 256, 64, 300, 8, 8, 64, 8, 3),
+    ("e1024_k32", 128, 32, 1024, 32, 4, 16, 8, 2),
+    # deep inputs: 16 code splits (SiLU staged from 34 partials in 3 rounds),
+    # 128 router chunks
+    ("deep_h8192", 8192, 64, 8, 2, 8, 64, 16, 1),
+    # 512 selections: block-wide routing tables, 16-token combine tiles
+    ("b64_e128_k8", 256, 128, 128, 8, 8, 64, 16, 64),
 ]
 
 
@@ -275,6 +283,33 @@ def test_exact_and_single_precision_ties(C, k):
     x_bits = synth.to_bf16_bits(xv)
     y_ref, idx_ref, a_ref, _ = O.moe_layer_factored(x_bits, L, w.top_k, w.d)
     assert list(idx_ref[0][:3]) == [2, 0, 1]
+    y, idx, wt = _run_layer(C, w, L, x_bits)
+    assert np.array_equal(idx, idx_ref), (idx, idx_ref)
+    assert np.abs(wt - a_ref).max() <= 1e-5
+    assert np.abs(y - y_ref).max() <= TOL * np.abs(y_ref).max()
+
+
+def test_ties_beyond_256_experts(C):
+    """300 experts (the exact one-wave radix top-k): a group of exact ties
+    across the lanes and key rounds, a near tie below single precision, and
+    a tie group straddling the k-th place — indices must match the oracle."""
+    H, I, E, k, d, K, r, B = 256, 64, 300, 8, 8, 64, 8, 2
+    L = synth.make_layer(H, I, E, d, K, r, seed=31)
+    wr = np.zeros((H, E), dtype=np.float64)
+    for e in (5, 77, 150, 260, 299):      # exact ties at the top
+        wr[0, e] = 1.0
+    wr[0, 123] = wr[1, 123] = 1.0           # 1 + 2^-30: above them only in float64
+    for e in (3, 64, 128, 192, 256, 298):  # six-way tie around the k-th place
+        wr[0, e] = 0.5
+    L["router_w"] = synth.to_bf16_bits(wr)
+    L["router_bias"] = np.zeros(E, dtype=np.float32)
+    xv = np.zeros((B, H), dtype=np.float64)
+    xv[:, 0] = 1.0
+    xv[:, 1] = 2.0 ** -30
+    x_bits = synth.to_bf16_bits(xv)
+    y_ref, idx_ref, a_ref, _ = O.moe_layer_factored(x_bits, L, k, d)
+    assert list(idx_ref[0]) == [123, 5, 77, 150, 260, 299, 3, 64]
+    w = TINY.__class__("ties_e300", H=H, I=I, E=E, top_k=k, d=d, K=K, r=r, B=B, seed=0)
     y, idx, wt = _run_layer(C, w, L, x_bits)
     assert np.array_equal(idx, idx_ref), (idx, idx_ref)
     assert np.abs(wt - a_ref).max() <= 1e-5
