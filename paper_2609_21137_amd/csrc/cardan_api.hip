@@ -124,7 +124,9 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.n_eg = ceil_div(P.E, 64);
   P.z_sep = z_sep;
   P.nt_max = std::min(B, kTokPass);
-  P.tpc = std::min(kTokPass, ceil_div(B, 4));
+  // combine tiles of up to B/8 tokens: eight per column group at large
+  // batches, so the final gather is spread over more workgroups
+  P.tpc = std::min(kTokPass, ceil_div(B, 8));
   const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KSD = P.I / 32;
   P.nch_z = std::max(1, KSX / 2);                  // two K-steps of U per z unit
   // Tile sizes: the expected active experts' weight bytes spread over a
