@@ -197,14 +197,14 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.n_cb = P.ncgh * ceil_div(B, P.tpc);
 
   const int z_units = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nch_z;
-  P.n_rc = (flags & F_ROUTE) ? P.nch_r * P.n_eg : 0;
+  P.n_rc = (flags & F_ROUTE) ? P.nch_r * P.n_eg * ceil_div(B, kRouterTok) : 0;
   P.n_zc = (flags & F_Z) ? ceil_div(z_units, 4) : 0;
   P.n_sel = (flags & F_ROUTE) ? B : 0;
   P.n_zr = (flags & F_Z) ? ceil_div(2 * B * P.r, kWG) : 0;
   P.n_pre = P.n_rc + P.n_zc + P.n_sel + P.n_zr;
 
   // counters first, at offsets that depend only on the shape
-  P.n_rc_flags = P.nch_r * P.n_eg;
+  P.n_rc_flags = P.nch_r * P.n_eg * ceil_div(B, kRouterTok);
   P.n_zc_flags = ceil_div(2 * ceil_div(P.r, 64) * P.nch_z, 4);
   size_t o = 0;
   P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);

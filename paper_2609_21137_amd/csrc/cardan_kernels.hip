@@ -273,12 +273,12 @@ __device__ int block_exclusive_scan(int* arr, int n, int* tmp4) {
   return total;
 }
 
-// Router chunk (c, g): partial logits over hidden rows [64c, 64c + 64) for
-// experts [64g, 64g + 64). Lane l of wave w owns expert 64g + l and rows
-// 64c + 16w .. + 16; float64 FMAs of exact bf16 products, four independent
-// chains per token, then the four waves' partials are added in wave order
-// through LDS.
-__device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c, int g, uint8_t* smem) {
+// Router chunk (c, g, tb): partial logits over hidden rows [64c, 64c + 64)
+// for experts [64g, 64g + 64) of tokens [4tb, 4tb + 4). Lane l of wave w
+// owns expert 64g + l and rows 64c + 16w .. + 16; float64 FMAs of exact bf16
+// products, four independent chains per token, then the four waves'
+// partials are added in wave order through LDS.
+__device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c, int g, int tb, uint8_t* smem) {
   float* xs = reinterpret_cast<float*>(smem);                          // [16][64]
   double* part = reinterpret_cast<double*>(smem + kTokPass * kRowsRouter * 4);  // [4][16][64]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -289,8 +289,8 @@ __device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c,
 #pragma unroll
   for (int i = 0; i < 16; ++i) wv[i] = Wr[(size_t)i * E];
   double* rl = wsp<double>(A, P.o_rl);
-  for (int tg = 0; tg < B; tg += kTokPass) {
-    const int nt = min(kTokPass, B - tg);
+  {
+    const int tg = tb * kRouterTok, nt = min(kRouterTok, B - tg);
     for (int i = tid; i < nt * kRowsRouter; i += kWG) {
       const int t = i / kRowsRouter, h = i % kRowsRouter;
       xs[i] = bf(A.x[(size_t)(tg + t) * H + h0 + h]);
@@ -612,7 +612,9 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
   // the bias is read before the wait so its latency is hidden
   const float b0 = (A.L.router_bias && tid < E) ? A.L.router_bias[tid] : 0.0f;
   const int* rcf = wsp<const int>(A, P.o_rc_flag);
-  wait_all(A, P.n_rc, [&](int i) { return ld_dev(rcf + i * kTickPad) != 0; });
+  const int nrt = P.nch_r * P.n_eg;  // router chunks of this token's block
+  rcf += (t / kRouterTok) * nrt * kTickPad;
+  wait_all(A, nrt, [&](int i) { return ld_dev(rcf + i * kTickPad) != 0; });
   const double* rl = wsp<const double>(A, P.o_rl);
   double own = 0.0;  // logit of expert tid
   for (int e = tid; e < E; e += kWG) {
@@ -1609,7 +1611,8 @@ __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
   for (; j < e_rc; j += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
-    item_router_chunk(P, A, j, j % P.nch_r, j / P.nch_r, smem);
+    const int nrt = P.nch_r * P.n_eg, jr = j % nrt;
+    item_router_chunk(P, A, j, jr % P.nch_r, jr / P.nch_r, j / nrt, smem);
     tr.done(A, P, j, 0);
   }
   for (; j < e_zc; j += gridDim.x) {

@@ -35,6 +35,7 @@ namespace cardan {
 
 constexpr int kWG = 256;            // threads per workgroup (4 wave64)
 constexpr int kRowsRouter = 64;     // hidden rows per router / shared-projection chunk
+constexpr int kRouterTok = 4;       // tokens per router chunk item
 constexpr int kColsPerGroup = 256;  // output columns per expert tile (4 waves x 64)
 constexpr int kTokPass = 16;        // token slots per MFMA pass (N of 16x16x32)
 constexpr int kMaxE = 1024, kMaxK = 32, kMaxR = 512, kMaxB = 64;
