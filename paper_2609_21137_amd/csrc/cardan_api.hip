@@ -164,8 +164,8 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
     tile *= 1.05;
   }
   // Latency shape: if the item count still fits the nominal grid, code
-  // splits of at most one pipeline prime (kPdVq K-steps) and low-rank splits
-  // of kPdDense steps, so no tile streams refills after its prime.
+  // splits of at most kPdVq K-steps and low-rank splits of kPdDense steps
+  // (at most two pipeline fills of a gate/up tile).
   if (P.ns > 1) {
     const int nv = std::max(P.ns_v, ceil_div(KSX, kPdVq)), nl = KSZ > 0 ? ceil_div(KSZ, kPdDense) : 0;
     const double items = exp_act * (2.0 * P.ncg * (nv + nl) + P.ncgh * P.nsd + P.ncgr * P.nsdl);

@@ -1217,7 +1217,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
   const int* const slot_tok = RT.slot_tok;
   const float* zsrc = (P.flags & F_Z) ? A.z_out : A.z_in;
 
-  VqPipe<D, 1, kPdVq> vq;
+  VqPipe<D, 1, kPdGateUp> vq;
   DensePipe<2, kPdDense> lr;
   const int n8x = (x1 - x0) * 4, n8z = (z1 - z0) * 4;  // 8-element groups per token row
   // Activation loads through buffer resources over x [B][H] and z [2][B][r]

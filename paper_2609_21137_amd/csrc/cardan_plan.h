@@ -40,6 +40,8 @@ constexpr int kColsPerGroup = 256;  // output columns per expert tile (4 waves x
 constexpr int kTokPass = 16;        // token slots per MFMA pass (N of 16x16x32)
 constexpr int kMaxE = 1024, kMaxK = 32, kMaxR = 512, kMaxB = 64;
 constexpr int kPdVq = 16;     // code K-steps in flight per wave (4 B per lane each)
+constexpr int kPdGateUp = 8;  // the same for gate/up tiles: half the bytes requested at once when
+                              // every tile starts together, the rest as the first steps complete
 constexpr int kPdDense = 2;   // dense K-steps in flight per wave (4 KB each)
 constexpr int kCombineChunk = 16;  // terms per load batch in the combine
 constexpr int kLrDownSteps = 4;    // K-steps of a low-rank down tile when the plan would cut finer
