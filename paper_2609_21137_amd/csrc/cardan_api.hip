@@ -204,7 +204,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.n_pre = P.n_rc + P.n_zc + P.n_sel + P.n_zr;
 
   // counters first, at offsets that depend only on the shape
-  P.n_rc_flags = P.nch_r * P.n_eg * ceil_div(B, kRouterTok);
+  P.n_rc_flags = P.nch_r * P.n_eg * ceil_div(kMaxB, kRouterTok);
   P.n_zc_flags = ceil_div(2 * ceil_div(P.r, 64) * P.nch_z, 4);
   size_t o = 0;
   P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);

@@ -1591,7 +1591,10 @@ __device__ __forceinline__ void warm_kernargs() {
 }
 
 // Each kernel clears the counters of the other kernel of the call before
-// any of them is used again (the stream orders the two kernels).
+// any of them is used again (the stream orders the two kernels): the flags
+// this call's routing items set, and every expert tick of the shape (a call
+// leaves no flag set, so calls of different batch sizes can share a
+// workspace).
 __device__ __forceinline__ void clear_ints(int* p, int n, int stride = 1) {
   for (int i = threadIdx.x; i < n; i += kWG) p[i * stride] = 0;
 }
@@ -1637,8 +1640,8 @@ __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
 
 // Clears the routing kernel's flags (after calls that run k_route alone).
 __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
-  clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags, kTickPad);
-  clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags, kTickPad);
+  clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc, kTickPad);
+  clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc, kTickPad);
 }
 
 // Expert work of the active experts (count published by k_route): gate/up
@@ -1663,8 +1666,8 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     sel_w = ld_dev(r_w + tid);
   }
   if (blockIdx.x == 0) {
-    clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc_flags, kTickPad);
-    clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc_flags, kTickPad);
+    clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc, kTickPad);
+    clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc, kTickPad);
   }
   // routing tables at the start of dynamic LDS, item LDS after them
   uint8_t* item_smem = smem + P.lds_routing;

@@ -252,6 +252,28 @@ def test_batch_rows_independent_and_repeatable(C):
         assert np.abs(y1[0] - y16[t]).max() <= 1e-5 * np.abs(y16[t]).max()
 
 
+def test_workspace_reused_across_batch_sizes(C):
+    """One workspace serves calls of different batch sizes in turn. Every
+    call must find the synchronisation counters cleared whatever batch ran
+    before it (their offsets depend on the layer shape only), so each result
+    equals that of a fresh workspace bit for bit."""
+    w = QWEN3_B16
+    L = synth.workload_layer(w)
+    x = synth.workload_input(w)
+    shape = C.make_shape(w.H, w.I, w.E, w.top_k, w.d, w.K, w.r)
+    DL = C.DeviceLayer.from_numpy(L)
+    ws = C.new_workspace(shape, x.shape[0])
+    for B in (16, 1, 16, 3, 1, 8, 16):
+        _say(f"workspace reuse: batch {B}")
+        y, idx, wt = C.moe_layer(shape, C.bf16_tensor(x[:B]), DL, ws=ws)
+        torch.cuda.synchronize()
+        assert C.workspace_status(ws) == 0, "an in-kernel wait timed out"
+        y_f, idx_f, wt_f = _run_layer(C, w, L, x[:B])
+        assert np.array_equal(idx.cpu().numpy(), idx_f)
+        assert np.array_equal(wt.cpu().numpy(), wt_f)
+        assert np.array_equal(y.cpu().numpy().astype(np.float64), y_f)
+
+
 def test_rmsnorm(C):
     rng = np.random.default_rng(0)
     y = rng.standard_normal((16, 2048)).astype(np.float32) * 0.3
