@@ -15,7 +15,7 @@
 
 namespace cardan {
 const void* route_kernel();
-const void* expert_kernel(int d);
+const void* expert_kernel(int d, int dnw);
 hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t);
@@ -194,6 +194,11 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.nsdl = std::min(P.nsdl, ceil_div(KSD, kLrDownSteps));
   while (P.nsd < KSD && !down_fits(P.nsd)) ++P.nsd;
   while (P.nsdl < KSD && !down_fits(P.nsdl)) ++P.nsdl;
+  // Many items: VQ down tiles over two column groups, so that each K-step's
+  // activation reads serve twice the columns and the down tiles take half
+  // the workgroup slots
+  const double items_all = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
+  if (items_all > 512.0 && P.ncgh > 1 && P.d == 8) P.flags |= F_DN_WIDE;
   P.n_cb = P.ncgh * ceil_div(B, P.tpc);
 
   const int z_units = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nch_z;
@@ -352,7 +357,7 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
     }
   }
   if (P.flags & F_EXPERTS) {
-    const int cap = resident_grid(expert_kernel(P.d), P.lds_expert, &err);
+    const int cap = resident_grid(expert_kernel(P.d, dn_width(P)), P.lds_expert, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_EXPERT);
     err = launch_expert(P, A, cap, P.lds_expert, stream, tm.ev0, tm.ev1);

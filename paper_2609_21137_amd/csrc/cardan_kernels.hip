@@ -867,6 +867,94 @@ struct VqPipe {
   }
 };
 
+// Two 64-column sub-tiles per wave, kColsPerGroup columns apart (a down tile
+// of two column groups, float32 activations as bf16 hi + lo): each K-step's
+// activation reads serve both sub-tiles. A second sub-tile past n_out reads
+// zeros (its results are never stored).
+template <int D, int PD>
+struct VqPipe2 {
+  static constexpr int W = D == 8 ? 1 : 2;
+  uint32_t buf[PD][2 * W];
+  rsrc_t rs;
+  uint32_t lane_off, lane_off2, step_bytes, row_len;
+  int ks0, nks;
+  bool has2;
+
+  __device__ __forceinline__ void load(int i, uint32_t (&b)[2 * W]) {
+    const uint32_t st = (uint32_t)(ks0 + i) * step_bytes;
+    const uint32_t o = i < nks ? lane_off + st : kOob, o2 = i < nks && has2 ? lane_off2 + st : kOob;
+    b[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, o, 0, 0);
+    if constexpr (D == 4) b[1] = __builtin_amdgcn_raw_buffer_load_b32(rs, o + row_len, 0, 0);
+    b[W] = __builtin_amdgcn_raw_buffer_load_b32(rs, o2, 0, 0);
+    if constexpr (D == 4) b[W + 1] = __builtin_amdgcn_raw_buffer_load_b32(rs, o2 + row_len, 0, 0);
+  }
+  __device__ __forceinline__ void prime(const uint8_t* c, int n_rows, int rl, int c0, int n_out, int k0,
+                                        int k1) {
+    rs = make_rsrc(c, (uint32_t)n_rows * rl);
+    row_len = rl;
+    const int g = (threadIdx.x & 63) >> 4;
+    const int col = min(c0 + 4 * (threadIdx.x & 15), n_out - 4);
+    const int col2 = min(c0 + kColsPerGroup + 4 * (threadIdx.x & 15), n_out - 4);
+    has2 = c0 + kColsPerGroup < n_out;
+    step_bytes = (uint32_t)(32 / D) * rl;
+    lane_off = (uint32_t)(g * (8 / D)) * rl + col;
+    lane_off2 = (uint32_t)(g * (8 / D)) * rl + col2;
+    ks0 = k0;
+    nks = k1 - k0;
+#pragma unroll
+    for (int u = 0; u < PD; ++u) load(u, buf[u]);
+  }
+  __device__ __forceinline__ uint4 word(const uint4* __restrict__ cb_s, const uint32_t* b, int q) const {
+    if constexpr (D == 8) {
+      return cb_s[(b[0] >> (8 * q)) & 255u];
+    } else {
+      const uint2* cb2 = reinterpret_cast<const uint2*>(cb_s);
+      const uint2 lo = cb2[(b[0] >> (8 * q)) & 255u];
+      const uint2 hi = cb2[(b[1] >> (8 * q)) & 255u];
+      return make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+  }
+  __device__ __forceinline__ void step(int ks, const uint32_t (&b)[2 * W], const uint4* __restrict__ cb_s,
+                                       const uint4* __restrict__ ops, int ops_ld, int ops_ks0, int nt,
+                                       f32x4 acc[8]) {
+    const int l = threadIdx.x & 63, n = l & 15, g = l >> 4;
+    const int oi = a_row(n, nt) * ops_ld + ((ks - ops_ks0) * 4 + g) * 2;
+    const uint4 a0 = ops[oi], a1 = ops[oi + 1];
+    uint4 w[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      w[q] = word(cb_s, b, q);
+      w[4 + q] = word(cb_s, b + W, q);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      acc[q] = mfma_bf16(a0, w[q], acc[q]);
+      acc[q] = mfma_bf16(a1, w[q], acc[q]);
+    }
+    sched_step<2 + (D == 8 ? 8 : 16), 16>();
+  }
+  __device__ __forceinline__ void run(const uint4* cb_s, const uint4* ops, int ops_ld, int ops_ks0, int nt,
+                                      f32x4 acc[8]) {
+    if (nks <= PD) {  // every step was primed: no refills
+#pragma unroll
+      for (int u = 0; u < PD; ++u) {
+        if (u < nks) step(ks0 + u, buf[u], cb_s, ops, ops_ld, ops_ks0, nt, acc);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      return;
+    }
+    for (int i0 = 0; i0 < nks; i0 += PD) {
+#pragma unroll
+      for (int u = 0; u < PD; ++u) {
+        const int i = i0 + u;
+        if (i < nks) step(ks0 + i, buf[u], cb_s, ops, ops_ld, ops_ks0, nt, acc);
+        load(i + PD, buf[u]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+};
+
 template <int Q>
 __device__ __forceinline__ uint4 dense_w(const uint2 (&b)[8]) {
   constexpr uint32_t sel = (Q & 1) ? 0x07060302u : 0x05040100u;
@@ -1355,6 +1443,41 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
   }
 }
 
+template <int NACC, typename Prime, typename Stage, typename Run, typename Finish>
+__device__ __forceinline__ void down_body_wide(const Plan& P, const Args& A, const Routing& R, int a, int ks0, int ks1,
+                                          Prime prime, Stage stage, Run run, Finish finish, uint8_t* smem) {
+  prime();
+  // every gate/up tile of the column groups holding inputs [32 ks0, 32 ks1)
+  const int cg0 = ks0 * 32 / kColsPerGroup, ncgw = (ks1 * 32 - 1) / kColsPerGroup - cg0 + 1;
+  const int* tick = wsp<const int>(A, P.o_gu_tick) + (a * P.ncg + cg0) * kTickPad;
+  wait_all(A, ncgw, [&](int i) { return ld_dev(tick + i * kTickPad) >= 2 * P.ns; });
+  const int ld = (ks1 - ks0) * 8 + 1;
+  uint4* ps = reinterpret_cast<uint4*>(smem);
+  const WsAccess ws(A, P);
+  for (int tg = 0; tg < R.ne; tg += P.nt_max) {
+    const int nt = min(P.nt_max, R.ne - tg);
+    if (tg > 0) prime();
+    __syncthreads();
+    stage();
+    const int nquad = (ks1 - ks0) * 8, slot0 = R.s0 + tg, col0 = ks0 * 32;
+    if (P.ns <= 1)
+      stage_silu<8, 1>(ws, P, ps, ld, nt, nquad, slot0, col0);
+    else if (P.ns <= 2)
+      stage_silu<4, 2>(ws, P, ps, ld, nt, nquad, slot0, col0);
+    else if (P.ns <= 4)
+      stage_silu<2, 4>(ws, P, ps, ld, nt, nquad, slot0, col0);
+    else
+      stage_silu<1, 8>(ws, P, ps, ld, nt, nquad, slot0, col0);
+    __syncthreads();
+    trace_mark(0);
+    f32x4 acc[NACC];
+#pragma unroll
+    for (int q = 0; q < NACC; q += 4) zero_acc(acc + q);
+    run(ps, ld, nt, acc);
+    finish(ws, acc, nt, R.s0 + tg);
+  }
+}
+
 template <int D>
 __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgx, int s,
                              uint4* cbs, uint8_t* smem) {
@@ -1376,6 +1499,42 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs, ps, ld, ks0, nt, acc); },
             [&](int slot) { return dn + (size_t)slot * H; }, smem);
   publish(wsp<int>(A, P.o_dn_done) + (R.e * (P.ncgh + 1) + cgx) * kTickPad);
+}
+
+// VQ down tile over two column groups (cgx, cgx + 1): as item_down_vq, each
+// wave on 64 columns of both groups.
+template <int D>
+__device__ void item_down_vq2(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgx, int s,
+                              uint4* cbs, uint8_t* smem) {
+  const Routing R = expert_of(P, RT, a);
+  const int H = P.H, I = P.I, S = P.S, KS = I / 32;
+  const int ks0 = s * KS / P.nsd, ks1 = (s + 1) * KS / P.nsd;
+  const int c0 = cgx * kColsPerGroup + (threadIdx.x >> 6) * 64;
+  const uint8_t* codes = A.L.codes_down + (size_t)R.e * (I / D) * H;
+  float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
+  VqPipe2<D, kPdVq> pipe;
+  uint4 bk;
+  down_body_wide<8>(P, A, R, a, ks0, ks1,
+               [&]() {
+                 bk = book_load<D>(A.L.cb_down, P.K);
+                 __builtin_amdgcn_sched_barrier(0);
+                 pipe.prime(codes, I / D, H, c0, H, ks0, ks1);
+               },
+               [&]() { book_store<D>(cbs, bk); },
+               [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs, ps, ld, ks0, nt, acc); },
+               [&](const WsAccess& ws, const f32x4* acc, int nt, int slot0) {
+                 store_acc(ws, acc, nt, c0, H, [&](int t) { return dn + (size_t)(slot0 + t) * H; });
+                 store_acc(ws, acc + 4, nt, c0 + kColsPerGroup, H,
+                           [&](int t) { return dn + (size_t)(slot0 + t) * H; });
+               },
+               smem);
+  int* done = wsp<int>(A, P.o_dn_done) + (R.e * (P.ncgh + 1) + cgx) * kTickPad;
+  drain_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(done, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (cgx + 1 < P.ncgh) __hip_atomic_fetch_add(done + kTickPad, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 // Low-rank down tile (a, cgr, s): partial A_e^T p over split s of I. The
@@ -1646,8 +1805,9 @@ __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
 
 // Expert work of the active experts (count published by k_route): gate/up
 // tiles, down tiles (waiting per expert for p), combine tiles (waiting for
-// every down tile).
-template <int D>
+// every down tile). DNW: column groups per VQ down tile; a separate
+// instantiation keeps the wide tiles' registers out of the narrow one.
+template <int D, int DNW>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ uint4 cbs[256];  // the code book of the current item (zero-padded to 256 words)
@@ -1677,7 +1837,8 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   tr_route.done(A, P, P.n_pre + P.max_act * (gateup_tiles_per_expert(P) + down_tiles_per_expert(P)) + P.n_cb +
                           blockIdx.x, 8);
   const int nact = RT.nact;
-  const int tgu = gateup_tiles_per_expert(P), tdn = down_tiles_per_expert(P);
+  const int nvq = (P.ncgh + DNW - 1) / DNW * P.nsd;  // VQ down tiles per expert
+  const int tgu = gateup_tiles_per_expert(P), tdn = nvq + P.ncgr * P.nsdl;
   const int s_vq = P.ns_v;  // first gate/up split without code steps
   const int n_gu = nact * tgu, n_dn = nact * tdn, n_items = n_gu + n_dn + P.n_cb;
   // Items in index order, one loop per kind (the kinds are contiguous ranges):
@@ -1697,9 +1858,12 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   for (; jp < n_gu + n_dn; jp += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
-    const int j = jp - n_gu, a = j / tdn, rem = j % tdn, nvq = P.ncgh * P.nsd;
+    const int j = jp - n_gu, a = j / tdn, rem = j % tdn;
     if (rem < nvq) {
-      item_down_vq<D>(P, A, RT, a, rem / P.nsd, rem % P.nsd, cbs, item_smem);
+      if constexpr (DNW == 2)
+        item_down_vq2<D>(P, A, RT, a, rem / P.nsd * 2, rem % P.nsd, cbs, item_smem);
+      else
+        item_down_vq<D>(P, A, RT, a, rem / P.nsd, rem % P.nsd, cbs, item_smem);
       tr.done(A, P, P.n_pre + jp, 5);
     } else {
       item_down_lr(P, A, RT, a, (rem - nvq) / P.nsdl, (rem - nvq) % P.nsdl, item_smem);
@@ -1736,9 +1900,10 @@ __global__ __launch_bounds__(kWG) void k_rmsnorm(int H, const float* __restrict_
 // ---------------------------------------------------------------------------
 const void* route_kernel() { return reinterpret_cast<const void*>(&k_route); }
 
-const void* expert_kernel(int d) {
-  return d == 8 ? reinterpret_cast<const void*>(&k_expert<8>)
-                : reinterpret_cast<const void*>(&k_expert<4>);
+const void* expert_kernel(int d, int dnw) {
+  return d == 8 ? (dnw == 2 ? reinterpret_cast<const void*>(&k_expert<8, 2>)
+                            : reinterpret_cast<const void*>(&k_expert<8, 1>))
+                : reinterpret_cast<const void*>(&k_expert<4, 1>);
 }
 
 // With a start/stop event pair the launch records them as part of the
@@ -1765,10 +1930,12 @@ hipError_t launch_route_reset(const Plan& P, const Args& A, hipStream_t st) {
 
 hipError_t launch_expert(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st, hipEvent_t ev0,
                          hipEvent_t ev1) {
-  if (P.d == 8)
-    CARDAN_LAUNCH(k_expert<8>, grid, lds, st, ev0, ev1, P, A);
+  if (P.d == 8 && dn_width(P) == 2)
+    CARDAN_LAUNCH((k_expert<8, 2>), grid, lds, st, ev0, ev1, P, A);
+  else if (P.d == 8)
+    CARDAN_LAUNCH((k_expert<8, 1>), grid, lds, st, ev0, ev1, P, A);
   else
-    CARDAN_LAUNCH(k_expert<4>, grid, lds, st, ev0, ev1, P, A);
+    CARDAN_LAUNCH((k_expert<4, 1>), grid, lds, st, ev0, ev1, P, A);
   return hipGetLastError();
 }
 

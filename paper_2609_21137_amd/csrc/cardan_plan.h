@@ -48,7 +48,8 @@ constexpr int kLrDownSteps = 4;    // K-steps of a low-rank down tile when the p
 
 
 // flags of one call
-enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8 };
+enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8,
+       F_DN_WIDE = 16 };  // set by the plan: VQ down tiles over two column groups
 
 // counters at the start of the workspace, one per 64-byte slot: the status
 // count of timed-out waits
@@ -102,8 +103,9 @@ inline __host__ __device__ size_t combine_lds(const Plan& P) {
 }
 
 __host__ __device__ inline int gateup_tiles_per_expert(const Plan& P) { return 2 * P.ncg * P.ns; }
+__host__ __device__ inline int dn_width(const Plan& P) { return (P.flags & F_DN_WIDE) ? 2 : 1; }
 __host__ __device__ inline int down_tiles_per_expert(const Plan& P) {
-  return P.ncgh * P.nsd + P.ncgr * P.nsdl;
+  return (P.ncgh + dn_width(P) - 1) / dn_width(P) * P.nsd + P.ncgr * P.nsdl;
 }
 
 // K-steps [k0, k1) of gate/up split s over the joint axis of KSX code steps
