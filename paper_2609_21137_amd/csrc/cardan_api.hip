@@ -230,6 +230,10 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // item LDS, also the grouping scratch at the start of the kernel
   const size_t group_scratch = round256((size_t)2 * P.S * 4 + (size_t)4 * P.E * 4 + 32);
   P.lds_expert = P.lds_routing + std::max(lds_expert(P), group_scratch);
+  // the large-batch kernel holds kBookCopies code books in static LDS: only
+  // where two workgroups still fit a CU (80 KB each)
+  if ((P.flags & F_DN_WIDE) && P.lds_expert + (size_t)256 * kBookCopies * 16 + 512 > 80 * 1024)
+    P.flags &= ~F_DN_WIDE;
   return P;
 }
 

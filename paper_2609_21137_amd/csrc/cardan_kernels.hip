@@ -786,7 +786,9 @@ struct WsAccess {
   }
 };
 
-template <int D, int NOPS, int PD>
+// NC: copies of the code book in LDS (d = 8): lane l reads copy l % NC, so
+// lanes of one LDS pass collide less on the random code-word rows.
+template <int D, int NOPS, int PD, int NC = 1>
 struct VqPipe {
   static constexpr int W = D == 8 ? 1 : 2;
   uint32_t buf[PD][W];
@@ -829,7 +831,7 @@ struct VqPipe {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if constexpr (D == 8) {
-        w[q] = cb_s[(b[0] >> (8 * q)) & 255u];
+        w[q] = cb_s[((b[0] >> (8 * q)) & 255u) * NC + (l & (NC - 1))];
       } else {
         const uint2 lo = cb2[(b[0] >> (8 * q)) & 255u];
         const uint2 hi = cb2[(b[1] >> (8 * q)) & 255u];
@@ -845,7 +847,15 @@ struct VqPipe {
   }
   __device__ __forceinline__ void run(const uint4* cb_s, const uint4* ops, int ops_ld, int ops_ks0,
                                       int nt, f32x4 acc[4]) {
+    run(cb_s, ops, ops_ld, ops_ks0, nt, acc, []() {});
+  }
+  // late() runs once when at most PD steps remain (loads for what follows
+  // the run go out then, not before the run starts)
+  template <typename Late>
+  __device__ __forceinline__ void run(const uint4* cb_s, const uint4* ops, int ops_ld, int ops_ks0,
+                                      int nt, f32x4 acc[4], Late late) {
     if (nks <= PD) {  // every step was primed: no refills
+      late();
 #pragma unroll
       for (int u = 0; u < PD; ++u) {
         if (u < nks) step(ks0 + u, buf[u], cb_s, ops, ops_ld, ops_ks0, nt, acc);
@@ -854,6 +864,7 @@ struct VqPipe {
       return;
     }
     for (int i0 = 0; i0 < nks; i0 += PD) {
+      if (i0 + PD >= nks) late();
 #pragma unroll
       for (int u = 0; u < PD; ++u) {
         const int i = i0 + u;
@@ -871,7 +882,7 @@ struct VqPipe {
 // of two column groups, float32 activations as bf16 hi + lo): each K-step's
 // activation reads serve both sub-tiles. A second sub-tile past n_out reads
 // zeros (its results are never stored).
-template <int D, int PD>
+template <int D, int PD, int NC = 1>
 struct VqPipe2 {
   static constexpr int W = D == 8 ? 1 : 2;
   uint32_t buf[PD][2 * W];
@@ -906,7 +917,7 @@ struct VqPipe2 {
   }
   __device__ __forceinline__ uint4 word(const uint4* __restrict__ cb_s, const uint32_t* b, int q) const {
     if constexpr (D == 8) {
-      return cb_s[(b[0] >> (8 * q)) & 255u];
+      return cb_s[((b[0] >> (8 * q)) & 255u) * NC + ((threadIdx.x & 63) & (NC - 1))];
     } else {
       const uint2* cb2 = reinterpret_cast<const uint2*>(cb_s);
       const uint2 lo = cb2[(b[0] >> (8 * q)) & 255u];
@@ -1278,12 +1289,21 @@ template <int D>
 __device__ __forceinline__ void book_store(uint4* cb, uint4 v) {
   if (threadIdx.x < 256 * D / 8) cb[threadIdx.x] = v;
 }
+// NC interleaved copies (d = 8): word w of copy c at w * NC + c
+template <int NC>
+__device__ __forceinline__ void book_store_copies(uint4* cb, uint4 v) {
+#pragma unroll
+  for (int c = 0; c < NC; ++c) cb[threadIdx.x * NC + c] = v;
+}
 
 // Gate/up tile (a, pj, cg, s): 256 output columns of projection pj over
 // split s of the joint reduction axis [x (H inputs) | z (r ranks)], i.e. the
 // VQ gather sum and V^T z accumulate in the same MFMA accumulators. Each
 // tile writes its partial sums.
-template <int D>
+// LATE: a tile that runs more code steps than its pipeline holds, code
+// steps first, loads its coefficients during the last of them (fewer bytes
+// requested at once when every tile starts; large batches).
+template <int D, bool LATE, int NC>
 __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg, int s,
                             bool lr_first, uint4* cbs, uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);
@@ -1305,7 +1325,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
   const int* const slot_tok = RT.slot_tok;
   const float* zsrc = (P.flags & F_Z) ? A.z_out : A.z_in;
 
-  VqPipe<D, 1, kPdGateUp> vq;
+  VqPipe<D, 1, kPdGateUp, NC> vq;
   DensePipe<2, kPdDense> lr;
   const int n8x = (x1 - x0) * 4, n8z = (z1 - z0) * 4;  // 8-element groups per token row
   // Activation loads through buffer resources over x [B][H] and z [2][B][r]
@@ -1340,6 +1360,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
                                           lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
   };
   constexpr int kRegStage = 2;  // activation groups per thread loaded ahead of the weights
+  const bool lr_late = LATE && !lr_first && x1 - x0 > kPdGateUp;
   for (int tg = 0; tg < R.ne; tg += P.nt_max) {
     const int nt = min(P.nt_max, R.ne - tg);
     // Activation loads go out before the weight prime: loads complete in
@@ -1355,9 +1376,12 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
     const uint4 bk = book_load<D>(pj ? A.L.cb_up : A.L.cb_gate, P.K);
     __builtin_amdgcn_sched_barrier(0);  // keep the activation and book loads first
     vq.prime(codes, H / D, I, c0, I, x0, x1);
-    lr.prime(V, I, c0, I, r, z0, z1);
+    if (!lr_late) lr.prime(V, I, c0, I, r, z0, z1);
     __syncthreads();
-    book_store<D>(cbs, bk);
+    if constexpr (NC > 1)
+      book_store_copies<NC>(cbs, bk);
+    else
+      book_store<D>(cbs, bk);
 #pragma unroll
     for (int u = 0; u < kRegStage; ++u) {
       const int i = threadIdx.x + u * kWG;
@@ -1391,7 +1415,12 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
     f32x4 acc[4];
     zero_acc(acc);
     if (lr_first) lr.run(zs, ldz, z0, nt, acc);
-    vq.run(cbs, xs, ldx, x0, nt, acc);
+    if constexpr (LATE)
+      vq.run(cbs, xs, ldx, x0, nt, acc, [&]() {
+        if (lr_late) lr.prime(V, I, c0, I, r, z0, z1);
+      });
+    else
+      vq.run(cbs, xs, ldx, x0, nt, acc);
     trace_mark(1);
     if (!lr_first) lr.run(zs, ldz, z0, nt, acc);
     store_acc(WsAccess(A, P), acc, nt, c0, I, [&](int t) { return gu + (((size_t)(R.s0 + tg + t) * 2 + pj) * P.ns + s) * I; });
@@ -1512,7 +1541,7 @@ __device__ void item_down_vq2(const Plan& P, const Args& A, const RouteTab& RT, 
   const int c0 = cgx * kColsPerGroup + (threadIdx.x >> 6) * 64;
   const uint8_t* codes = A.L.codes_down + (size_t)R.e * (I / D) * H;
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
-  VqPipe2<D, kPdVq> pipe;
+  VqPipe2<D, kPdVq, kBookCopies> pipe;
   uint4 bk;
   down_body_wide<8>(P, A, R, a, ks0, ks1,
                [&]() {
@@ -1520,7 +1549,7 @@ __device__ void item_down_vq2(const Plan& P, const Args& A, const RouteTab& RT, 
                  __builtin_amdgcn_sched_barrier(0);
                  pipe.prime(codes, I / D, H, c0, H, ks0, ks1);
                },
-               [&]() { book_store<D>(cbs, bk); },
+               [&]() { book_store_copies<kBookCopies>(cbs, bk); },
                [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(cbs, ps, ld, ks0, nt, acc); },
                [&](const WsAccess& ws, const f32x4* acc, int nt, int slot0) {
                  store_acc(ws, acc, nt, c0, H, [&](int t) { return dn + (size_t)(slot0 + t) * H; });
@@ -1810,7 +1839,10 @@ __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
 template <int D, int DNW>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  __shared__ uint4 cbs[256];  // the code book of the current item (zero-padded to 256 words)
+  // the code book of the current item (zero-padded to 256 words), in
+  // kBookCopies copies in the large-batch kernel
+  constexpr int NC = DNW == 2 ? kBookCopies : 1;
+  __shared__ uint4 cbs[256 * NC];
   warm_kernargs();
   const int tid = threadIdx.x;
   ItemTrace tr_route;
@@ -1852,7 +1884,7 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     // first in the second half of the grid, so the two workgroups sharing a
     // CU overlap LDS-bound and HBM-bound phases
     const bool lr_first = (int)(jp % gridDim.x) >= (int)(gridDim.x >> 1);
-    item_gateup<D>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem);
+    item_gateup<D, DNW == 2, NC>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem);
     tr.done(A, P, P.n_pre + jp, 4);
   }
   for (; jp < n_gu + n_dn; jp += gridDim.x) {

@@ -44,6 +44,7 @@ constexpr int kPdGateUp = 8;  // the same for gate/up tiles: half the bytes requ
                               // every tile starts together, the rest as the first steps complete
 constexpr int kPdDense = 2;   // dense K-steps in flight per wave (4 KB each)
 constexpr int kCombineChunk = 16;  // terms per load batch in the combine
+constexpr int kBookCopies = 4;     // code book copies in LDS of the large-batch expert kernel (d = 8)
 constexpr int kLrDownSteps = 4;    // K-steps of a low-rank down tile when the plan would cut finer
 
 
