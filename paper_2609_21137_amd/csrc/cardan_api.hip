@@ -194,11 +194,12 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.nsdl = std::min(P.nsdl, ceil_div(KSD, kLrDownSteps));
   while (P.nsd < KSD && !down_fits(P.nsd)) ++P.nsd;
   while (P.nsdl < KSD && !down_fits(P.nsdl)) ++P.nsdl;
-  // Many items: VQ down tiles over two column groups, so that each K-step's
-  // activation reads serve twice the columns and the down tiles take half
-  // the workgroup slots
+  // Items for more than two rounds of the nominal grid (throughput-bound):
+  // VQ down tiles over two column groups, so that each K-step's activation
+  // reads serve twice the columns and the down tiles take half the
+  // workgroup slots (fewer rounds, longer tiles)
   const double items_all = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
-  if (items_all > 512.0 && P.ncgh > 1 && P.d == 8) P.flags |= F_DN_WIDE;
+  if (items_all > 2 * 512.0 && P.ncgh > 1 && P.d == 8) P.flags |= F_DN_WIDE;
   P.n_cb = P.ncgh * ceil_div(B, P.tpc);
 
   const int z_units = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nch_z;
