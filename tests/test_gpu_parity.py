@@ -209,6 +209,9 @@ EDGE_SHAPES = [
     ("deep_h8192", 8192, 64, 8, 2, 8, 64, 16, 1),
     # 512 selections: block-wide routing tables, 16-token combine tiles
     ("b64_e128_k8", 256, 128, 128, 8, 8, 64, 16, 64),
+    # large-batch kernel (down tiles over two column groups) with an odd
+    # number of column groups, the last one ragged (704 = 2 x 256 + 192)
+    ("wide_tiles_ragged", 704, 768, 128, 8, 8, 256, 128, 32),
 ]
 
 
