@@ -103,7 +103,7 @@ size_t lds_route(const Plan& P) {
 size_t lds_expert(const Plan& P) {
   const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KSD = P.I / 32;
   size_t need = (size_t)P.nt_max * gateup_ld(KSX, KSZ, P.ns, P.ns_v) * 16;
-  // down: p operand rows + split_sum reduction (2 float4 per thread)
+  // down: p operand rows + a reduction area of 2 float4 per thread
   const int ksd = std::max(ks_max(KSD, P.nsd), ks_max(KSD, P.nsdl));
   need = std::max(need, (size_t)P.nt_max * (ksd * 8 + 1) * 16 + kWG * 2 * 16);
   need = std::max(need, combine_lds(P));

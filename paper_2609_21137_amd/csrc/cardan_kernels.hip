@@ -121,15 +121,6 @@ __device__ __forceinline__ double ld_dev(const double* p) {
 __device__ __forceinline__ int ld_dev(const int* p) {
   return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_dev4(float* p, float4 v) {
-  st_dev(p, v.x);
-  st_dev(p + 1, v.y);
-  st_dev(p + 2, v.z);
-  st_dev(p + 3, v.w);
-}
-__device__ __forceinline__ float4 ld_dev4(const float* p) {
-  return make_float4(ld_dev(p), ld_dev(p + 1), ld_dev(p + 2), ld_dev(p + 3));
-}
 
 // Orders this wave's LDS writes before its later LDS reads by other lanes
 // (a wave executes its LDS operations in order; this keeps the compiler from
@@ -157,24 +148,9 @@ __device__ __forceinline__ void set_flag(int* f) {
   if (threadIdx.x == 0) st_dev(f, 1);
 }
 
-// Waits until *c >= target (thread 0 polls). Bounded: on timeout the status
-// counter is raised and the caller proceeds, so the grid always drains.
-__device__ __forceinline__ void wait_geq(const Args& A, const int* c, int target) {
-  if (threadIdx.x == 0) {
-    unsigned it = 0;
-    while (ld_dev(c) < target) {
-      __builtin_amdgcn_s_sleep(4);
-      if (++it > kSpinLimit) {
-        atomicAdd(ctr(A, C_ERR), 1);
-        break;
-      }
-    }
-    trace_wait_done();
-  }
-  __syncthreads();
-}
-
 // Waits until cond(i) holds for every i in [0, n) (threads test in parallel).
+// Bounded: on timeout the status counter is raised and the caller proceeds,
+// so the grid always drains.
 template <typename F>
 __device__ __forceinline__ void wait_all(const Args& A, int n, F cond) {
   unsigned it = 0;
@@ -191,17 +167,6 @@ __device__ __forceinline__ void wait_all(const Args& A, int n, F cond) {
       break;
     }
   }
-}
-
-// Ticket: true in the one workgroup that arrives last of `total`; every
-// workgroup drains its stores first, so the last one may read them all.
-__device__ __forceinline__ bool last_of(int* tick, int total, int* s_flag) {
-  drain_stores();
-  __syncthreads();
-  if (threadIdx.x == 0)
-    *s_flag = (__hip_atomic_fetch_add(tick, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == total - 1);
-  __syncthreads();
-  return *s_flag;
 }
 
 // Inclusive prefix sum across a wave64 with DPP row shifts and row
@@ -1150,66 +1115,6 @@ __device__ __forceinline__ float4 fma4(float w, float4 v, float4 a) {
   return make_float4(fmaf(w, v.x, a.x), fmaf(w, v.y, a.y), fmaf(w, v.z, a.z), fmaf(w, v.w, a.w));
 }
 
-// Sums of many partials with every load in flight at once. For each of
-// `items` outputs (NV float4 values each) it adds `npair` weighted terms:
-// the workgroup is split into G groups (G * items <= 256 threads) that take
-// every G-th term, BATCH terms' loads issued together; the group partials
-// meet in LDS (`red`, G * items * NV float4) and are added in group order,
-// so the result is deterministic. term(item, p, off, w) gives term p's
-// workspace byte offsets and weight (p < 0 or no term: kOob and 0); done(item,
-// sum) receives the result. All threads of the workgroup must call it.
-template <int NV, int BATCH, typename Term, typename Done>
-__device__ __forceinline__ void split_sum(const WsAccess& ws, int items, int npair, float4* red, Term term, Done done) {
-  const int tid = threadIdx.x;
-  const int G = items >= kWG ? 1 : min(16, kWG / items);
-  for (int base = 0; base < items * G; base += kWG) {
-    const int idx = base + tid;
-    const int item = idx % items, g = idx / items;
-    float4 acc[NV];
-#pragma unroll
-    for (int u = 0; u < NV; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (idx < items * G) {
-      for (int p0 = g; p0 < npair; p0 += G * BATCH) {
-        uint32_t off[BATCH][NV];
-        float wt[BATCH];
-#pragma unroll
-        for (int b = 0; b < BATCH; ++b) {
-          const int p = p0 + b * G;
-          term(item, p < npair ? p : -1, off[b], wt[b]);
-        }
-        float4 v[BATCH][NV];
-#pragma unroll
-        for (int b = 0; b < BATCH; ++b)
-#pragma unroll
-          for (int u = 0; u < NV; ++u) v[b][u] = ws.f4(off[b][u]);
-#pragma unroll
-        for (int b = 0; b < BATCH; ++b)
-#pragma unroll
-          for (int u = 0; u < NV; ++u) acc[u] = fma4(wt[b], v[b][u], acc[u]);
-      }
-    }
-    if (G == 1) {
-      if (idx < items) done(item, acc);
-    } else {
-#pragma unroll
-      for (int u = 0; u < NV; ++u) red[(g * items + item) * NV + u] = acc[u];
-      __syncthreads();
-      if (tid < items) {
-        float4 sum[NV];
-#pragma unroll
-        for (int u = 0; u < NV; ++u) sum[u] = red[tid * NV + u];
-        for (int gg = 1; gg < G; ++gg)
-#pragma unroll
-          for (int u = 0; u < NV; ++u) {
-            const float4 q = red[(gg * items + tid) * NV + u];
-            sum[u] = make_float4(sum[u].x + q.x, sum[u].y + q.y, sum[u].z + q.z, sum[u].w + q.w);
-          }
-        done(tid, sum);
-      }
-      __syncthreads();
-    }
-  }
-}
 
 // ===========================================================================
 // shared projections on MFMA
@@ -1588,8 +1493,8 @@ __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, i
 // Combine tile (cgy, tq): output columns [256 cgy, +256) of tokens
 // [tpc tq, tpc tq + tpc): y[t] = sum_j a_j sum_s dn[s][slot_j] + B^T u[t]
 // with u[t] = sum_j a_j u_e[slot_j]. B rows are loaded before the
-// wait; B^T u runs on MFMA with u as bf16 hi/lo. Every partial sum keeps all
-// its loads in flight (split_sum).
+// wait; B^T u runs on MFMA with u as bf16 hi/lo. The partial sums are
+// gathered in chunks of kCombineChunk loads in flight per thread.
 __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, int jc, uint8_t* smem) {
   const int cgy = jc % P.ncgh, tq = jc / P.ncgh;
   const int H = P.H, r = P.r, k = P.k, S = P.S, nsd = P.nsd;
