@@ -40,6 +40,11 @@ Functions:
                               ``Q^T x + V^T (U^T x)`` (gate/up) and
                               ``Q^T p + B^T (A^T p)`` (down).
 * ``moe_layer_scalar``     -- O2: pure-Python scalar loops for tiny shapes.
+* ``moe_layer_dense``      -- the uncompressed baseline: the same MoE block
+                              (Sec. 2.1) with dense bf16 expert matrices.
+* ``moe_layer_dense_down`` -- compressed gate/up (Eq. (1)) with the down
+                              projection kept as a dense bf16 matrix, the
+                              paper's own setting (Sec. 3.1).
 
 All bf16 inputs arrive as raw uint16 bit patterns and are widened exactly.
 """
@@ -299,6 +304,54 @@ def expert_outputs_sampled(x, idx, a, layer: dict, d: int, cols) -> np.ndarray:
                 ye = ye + Bd.T @ (_f(layer["A_down"][e]).T @ p)
             out[t] += a[t, j] * ye
     return out
+
+
+# --------------------------------------------------------------------------
+# dense-weight baselines
+# --------------------------------------------------------------------------
+def expert_ffn_dense(x, idx, a, W_gate, W_up, W_down) -> np.ndarray:
+    """Expert computation for fixed routing with dense expert matrices
+    ``W_gate[e]``, ``W_up[e]`` [H, I] and ``W_down[e]`` [I, H] (Sec. 2.1):
+    ``y_t = sum_j a[t, j] * W_down[e]^T (silu(W_gate[e]^T x_t) * W_up[e]^T x_t)``
+    in selection order."""
+    xf = _f(x)
+    idx = np.asarray(idx)
+    a = np.asarray(a, dtype=np.float64)
+    y = np.zeros((xf.shape[0], xf.shape[1]))
+    for t in range(xf.shape[0]):
+        for j in range(idx.shape[1]):
+            e = int(idx[t, j])
+            g = _f(W_gate[e]).T @ xf[t]
+            u = _f(W_up[e]).T @ xf[t]
+            p = silu(g) * u
+            y[t] += a[t, j] * (_f(W_down[e]).T @ p)
+    return y
+
+
+def moe_layer_dense(x, router_w, router_bias, W_gate, W_up, W_down, k: int):
+    """The uncompressed baseline layer: route, then dense experts.
+    Returns ``(y [B, H] f64, idx [B, k], a [B, k], margin [B])``."""
+    idx, a, margin, _ = route(x, router_w, router_bias, k)
+    return expert_ffn_dense(x, idx, a, W_gate, W_up, W_down), idx, a, margin
+
+
+def moe_layer_dense_down(x, layer: dict, W_down, k: int, d: int):
+    """Gate and up from Eq. (1) (VQ plus shared-basis low rank), down a dense
+    bf16 matrix ``W_down[e]`` [I, H]. Same return as ``moe_layer``."""
+    idx, a, margin, _ = route(x, layer["router_w"], layer.get("router_bias"), k)
+    xf = _f(x)
+    y = np.zeros((xf.shape[0], xf.shape[1]))
+    cache = {}
+    for t in range(xf.shape[0]):
+        for j in range(idx.shape[1]):
+            e = int(idx[t, j])
+            if e not in cache:
+                Wg, Wu, _ = expert_matrices(layer, e, d)
+                cache[e] = (Wg, Wu)
+            Wg, Wu = cache[e]
+            p = silu(Wg.T @ xf[t]) * (Wu.T @ xf[t])
+            y[t] += a[t, j] * (_f(W_down[e]).T @ p)
+    return y, idx, a, margin
 
 
 # --------------------------------------------------------------------------

@@ -17,6 +17,9 @@ Recipe (one independent PCG64 stream per tensor, keyed by
   gate and up; private ``V_e[r, I] ~ N(0, 0.01)`` (std).
 * Down: private ``A_e[I, r] ~ N(0, 0.01)`` (std), shared ``B[r, H] ~ N(0, 1/H)``
   (variance).
+* Dense bf16 expert matrices (the uncompressed baseline and the dense-down
+  variant): ``W_gate, W_up [E, H, I]`` and ``W_down [E, I, H] ~ N(0, 0.02)``
+  (std, the scale of a code-book entry).
 
 Normals are drawn in float64, rounded to float32 (round to nearest even) and
 then to bf16 (round to nearest even).
@@ -32,6 +35,7 @@ from .configs import Workload
 _T_X, _T_WR, _T_CBG, _T_CBU, _T_CBD = 1, 2, 3, 4, 5
 _T_JG, _T_JU, _T_JD, _T_U, _T_UU = 6, 7, 8, 9, 10
 _T_VG, _T_VU, _T_A, _T_B = 11, 12, 13, 14
+_T_WG, _T_WU, _T_WD = 15, 16, 17
 
 
 def _rng(seed: int, layer: int, tensor_id: int, extra: int = 0) -> np.random.Generator:
@@ -93,6 +97,19 @@ def make_layer(H: int, I: int, E: int, d: int, K: int, r: int, seed: int, layer:
         for key in ("U_gate", "U_up", "V_gate", "V_up", "A_down", "B_down"):
             L[key] = None
     return L
+
+
+def make_dense_weights(H: int, I: int, E: int, seed: int, layer: int = 0, which=("gate", "up", "down")) -> dict:
+    """Dense bf16 expert matrices ``W_gate``/``W_up`` [E, H, I] and
+    ``W_down`` [E, I, H] (those named in ``which``), as bf16 bits."""
+    out = {}
+    if "gate" in which:
+        out["W_gate"] = _normal_bf16(_rng(seed, layer, _T_WG), (E, H, I), 0.02)
+    if "up" in which:
+        out["W_up"] = _normal_bf16(_rng(seed, layer, _T_WU), (E, H, I), 0.02)
+    if "down" in which:
+        out["W_down"] = _normal_bf16(_rng(seed, layer, _T_WD), (E, I, H), 0.02)
+    return out
 
 
 def make_input(H: int, B: int, seed: int, layer: int = 0, step: int = 0) -> np.ndarray:

@@ -308,12 +308,48 @@ def pin_storage_rate_tables():
         assert round(bits, 2) == row["bits"], (name, bits)
 
 
+def pin_dense_baseline_against_torch():
+    """The dense-weight baseline layer against the independent torch float64
+    dense MoE on random bf16 matrices."""
+    H, I, E, k, B = 24, 16, 6, 2, 3
+    L = _rand_layer(H, I, E, 8, 16, 0, seed=11)  # only the router is used
+    W = {key: _bf(O.bf16_to_f64(v) * 10.0) for key, v in synth.make_dense_weights(H, I, E, seed=11).items()}
+    x = synth.make_input(H, B, seed=11)
+    y_ref, idx_ref, a_ref = dense_moe_torch(O.bf16_to_f64(x), O.bf16_to_f64(L["router_w"]),
+                                            L["router_bias"].astype(np.float64), O.bf16_to_f64(W["W_gate"]),
+                                            O.bf16_to_f64(W["W_up"]), O.bf16_to_f64(W["W_down"]), k)
+    y, idx, a, _ = O.moe_layer_dense(x, L["router_w"], L["router_bias"], W["W_gate"], W["W_up"], W["W_down"], k)
+    assert np.array_equal(idx, idx_ref)
+    assert np.allclose(a, a_ref, rtol=0, atol=1e-14)
+    assert np.allclose(y, y_ref, rtol=1e-12, atol=1e-12)
+
+
+def pin_dense_down_reduces_to_compressed():
+    """With r = 0 the decoded matrices are exact bf16 values: setting the
+    dense down matrix to the decoded down codes gives O1 bit for bit, and
+    setting dense gate/up matrices to the decoded gate/up codes as well gives
+    the dense baseline bit for bit."""
+    H, I, E, k, d, K, B = 16, 16, 5, 2, 4, 16, 3
+    L = _scale_codebooks(_rand_layer(H, I, E, d, K, 0, seed=12), 10.0)
+    x = synth.make_input(H, B, seed=12)
+    dec = lambda key, cb: np.stack([_bf(O.decode_vq(L[key][e], L[cb], d)) for e in range(E)])
+    Wg, Wu, Wd = dec("codes_gate", "cb_gate"), dec("codes_up", "cb_up"), dec("codes_down", "cb_down")
+    y1, idx1, a1, _ = O.moe_layer(x, L, k, d)
+    y2, idx2, a2, _ = O.moe_layer_dense_down(x, L, Wd, k, d)
+    y3, idx3, a3, _ = O.moe_layer_dense(x, L["router_w"], L["router_bias"], Wg, Wu, Wd, k)
+    assert np.array_equal(idx1, idx2) and np.array_equal(idx1, idx3)
+    assert np.array_equal(a1, a2) and np.array_equal(a1, a3)
+    assert np.array_equal(y1, y2) and np.array_equal(y2, y3)
+    assert np.abs(y1).max() > 1e-3  # a non-trivial output
+
+
 PINS = [
     pin_worked_example, pin_o1_equals_scalar_bruteforce, pin_o1_equals_factored,
     pin_onehot_codebook_is_dense_moe, pin_value_table_d1_is_dense_moe,
     pin_zero_codebooks_is_lowrank_moe, pin_expert_permutation_invariance,
     pin_batch_rows_independent, pin_topk_rules, pin_decode_layout, pin_silu_and_rmsnorm,
-    pin_bf16_widening, pin_storage_rate_tables,
+    pin_bf16_widening, pin_storage_rate_tables, pin_dense_baseline_against_torch,
+    pin_dense_down_reduces_to_compressed,
 ]
 
 
@@ -394,9 +430,25 @@ def _mut_storage_no_basis(d, K, r, H, I, E, b_index=None, b_coef=16, b_codebook=
     return _ORIG["storage_bits_per_weight"](d, K, r, H, I, E, b_index, b_coef, b_codebook, 0)
 
 
+def _mut_dense_no_silu(x, idx, a, W_gate, W_up, W_down):
+    xf = O.bf16_to_f64(x)
+    y = np.zeros_like(xf)
+    for t in range(xf.shape[0]):
+        for j in range(np.asarray(idx).shape[1]):
+            e = int(idx[t, j])
+            p = (O.bf16_to_f64(W_gate[e]).T @ xf[t]) * (O.bf16_to_f64(W_up[e]).T @ xf[t])
+            y[t] += a[t, j] * (O.bf16_to_f64(W_down[e]).T @ p)
+    return y
+
+
+def _mut_dense_down_transposed(x, layer, W_down, k, d):
+    Wt = np.ascontiguousarray(np.swapaxes(np.asarray(W_down), 1, 2))
+    return _ORIG["moe_layer_dense_down"](x, layer, Wt, k, d)
+
+
 _ORIG = {name: getattr(O, name) for name in
          ("decode_vq", "expert_matrices", "silu", "gating", "select_topk", "router_logits",
-          "expert_ffn", "storage_bits_per_weight")}
+          "expert_ffn", "storage_bits_per_weight", "moe_layer_dense_down")}
 
 MUTATIONS = {
     "decode_element_order_reversed": ("decode_vq", _mut_decode_reversed),
@@ -410,6 +462,8 @@ MUTATIONS = {
     "router_bias_dropped": ("router_logits", _mut_no_bias),
     "affinity_not_applied": ("expert_ffn", _mut_unweighted),
     "shared_basis_not_amortised": ("storage_bits_per_weight", _mut_storage_no_basis),
+    "dense_baseline_silu_dropped": ("expert_ffn_dense", _mut_dense_no_silu),
+    "dense_down_transposed": ("moe_layer_dense_down", _mut_dense_down_transposed),
 }
 
 
