@@ -105,7 +105,8 @@ int cardan_abi_version(void);
 const char* cardan_last_error(void);
 
 /* Workspace size in bytes needed by every ws-taking entry point for this
- * shape and any batch up to B. Host-only; no device is touched. */
+ * shape and any batch up to B (the dense-weight entry points included).
+ * Host-only; no device is touched. */
 int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out);
 
 /* Router and gating (paper Sec. 2.1): logits l[t][e] = sum_h x[t][h] *
@@ -146,6 +147,38 @@ int cardan_vq_lr_expert_ffn(const cardan_shape* shape, int32_t B, const cardan_b
 int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
                      const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
                      void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Dense bf16 expert weights of an uncompressed layer (device pointers). */
+typedef struct {
+  const cardan_bf16* router_w;    /* [H][E]                                  */
+  const float*       router_bias; /* [E] added to the logits, or NULL        */
+  const cardan_bf16* W_gate;      /* [E][H][I]                               */
+  const cardan_bf16* W_up;        /* [E][H][I]                               */
+  const cardan_bf16* W_down;      /* [E][I][H]                               */
+} cardan_dense_layer;
+
+/* The layer with compressed gate and up projections (Eq. (1)) and a dense
+ * bf16 down projection W_down [E][I][H], the form whose down matrices the
+ * paper leaves uncompressed (Sec. 3.2): routing as cardan_route_topk, g and
+ * u as in cardan_vq_lr_expert_ffn, then y[t] = sum_j topk_w[t][j] *
+ * W_down[e_j]^T p_j. The layer's cb_down, codes_down, A_down and B_down are
+ * not read (may be NULL). Outputs as cardan_moe_layer. H * I * 2 must stay
+ * below 2^31 (CARDAN_ERR_UNSUPPORTED otherwise). */
+int cardan_moe_layer_dense_down(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                                const cardan_layer* layer, const cardan_bf16* W_down, float* y,
+                                int32_t* topk_idx, float* topk_w,
+                                void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The uncompressed MoE layer (paper Sec. 2.1), the baseline the compressed
+ * form is measured against: routing as cardan_route_topk, then for every
+ * (token, selected expert) p = silu(W_gate[e]^T x) * (W_up[e]^T x) and
+ * y[t] = sum_j topk_w[t][j] * W_down[e_j]^T p_j, float32 accumulation.
+ * Only H, I, E and top_k of `shape` are read; the workspace size is
+ * cardan_workspace_bytes() of any valid shape with those four fields.
+ * H * I * 2 must stay below 2^31. Outputs as cardan_moe_layer. */
+int cardan_dense_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                           const cardan_dense_layer* layer, float* y, int32_t* topk_idx,
+                           float* topk_w, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* RMS normalisation between stacked layers: x_next[t][h] =
  * bf16_rne(y[t][h] / sqrt(mean_h y[t][h]^2 + eps)), no learned scale.

@@ -28,6 +28,8 @@ LAYER_FIELDS = (
     "V_gate", "V_up", "A_down", "B_down",
 )
 
+DENSE_LAYER_FIELDS = ("router_w", "router_bias", "W_gate", "W_up", "W_down")
+
 KERNEL_KINDS = ("route", "expert", "rmsnorm")
 
 ERRORS = {-1: "NULL_PTR", -2: "BAD_SHAPE", -3: "UNSUPPORTED", -4: "WORKSPACE", -5: "HIP",
@@ -48,6 +50,10 @@ class LayerStruct(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in LAYER_FIELDS]
 
 
+class DenseLayerStruct(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in DENSE_LAYER_FIELDS]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
@@ -56,6 +62,7 @@ def _load():
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     sp = ctypes.POINTER(Shape)
     lp = ctypes.POINTER(LayerStruct)
+    dp = ctypes.POINTER(DenseLayerStruct)
     sig = {
         "cardan_abi_version": ([], ctypes.c_int),
         "cardan_last_error": ([], ctypes.c_char_p),
@@ -64,6 +71,8 @@ def _load():
         "cardan_shared_proj": ([sp, i32, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_vq_lr_expert_ffn": ([sp, i32, vp, vp, vp, vp, lp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_moe_layer": ([sp, i32, vp, lp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cardan_moe_layer_dense_down": ([sp, i32, vp, lp, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cardan_dense_moe_layer": ([sp, i32, vp, dp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_rmsnorm_bf16": ([i32, i32, vp, ctypes.c_float, vp, vp], ctypes.c_int),
         "cardan_profile_begin": ([i32], ctypes.c_int),
         "cardan_profile_end": ([ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)], ctypes.c_int),
@@ -79,7 +88,8 @@ _lib = _load()
 
 EXPORTED = (
     "cardan_abi_version", "cardan_last_error", "cardan_workspace_bytes", "cardan_route_topk",
-    "cardan_shared_proj", "cardan_vq_lr_expert_ffn", "cardan_moe_layer", "cardan_rmsnorm_bf16",
+    "cardan_shared_proj", "cardan_vq_lr_expert_ffn", "cardan_moe_layer",
+    "cardan_moe_layer_dense_down", "cardan_dense_moe_layer", "cardan_rmsnorm_bf16",
     "cardan_profile_begin", "cardan_profile_end",
 )
 
@@ -261,6 +271,74 @@ def moe_layer(shape: Shape, x, layer: DeviceLayer, ws=None, out=None, idx=None, 
         ws = new_workspace(shape, B, dev)
     st = layer.struct()
     _check(_lib.cardan_moe_layer(
+        ctypes.byref(shape), B, _ptr(x, torch.bfloat16, "x", (B, shape.H)), ctypes.byref(st),
+        _ptr(y, torch.float32, "y", (B, shape.H)),
+        _ptr(idx, torch.int32, "topk_idx", (B, shape.top_k)),
+        _ptr(w, torch.float32, "topk_w", (B, shape.top_k)),
+        _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(dev)))
+    return y, idx, w
+
+
+def _outputs(shape: Shape, x, out, idx, w):
+    B = x.shape[0]
+    dev = x.device
+    y = out if out is not None else torch.empty((B, shape.H), dtype=torch.float32, device=dev)
+    idx = idx if idx is not None else torch.empty((B, shape.top_k), dtype=torch.int32, device=dev)
+    w = w if w is not None else torch.empty((B, shape.top_k), dtype=torch.float32, device=dev)
+    return y, idx, w
+
+
+def moe_layer_dense_down(shape: Shape, x, layer: DeviceLayer, W_down, ws=None, out=None, idx=None,
+                         w=None):
+    """The layer with compressed gate/up and a dense bf16 ``W_down [E, I, H]``
+    (the layer's compressed down fields are not read). Returns
+    ``(y float32 [B, H], topk_idx, topk_w)``."""
+    B = x.shape[0]
+    dev = x.device
+    y, idx, w = _outputs(shape, x, out, idx, w)
+    if ws is None:
+        ws = new_workspace(shape, B, dev)
+    st = layer.struct()
+    _check(_lib.cardan_moe_layer_dense_down(
+        ctypes.byref(shape), B, _ptr(x, torch.bfloat16, "x", (B, shape.H)), ctypes.byref(st),
+        _ptr(W_down, torch.bfloat16, "W_down", (shape.E, shape.I, shape.H)),
+        _ptr(y, torch.float32, "y", (B, shape.H)),
+        _ptr(idx, torch.int32, "topk_idx", (B, shape.top_k)),
+        _ptr(w, torch.float32, "topk_w", (B, shape.top_k)),
+        _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(dev)))
+    return y, idx, w
+
+
+@dataclass
+class DenseLayer:
+    """An uncompressed layer's device tensors (fields of ``cardan_dense_layer``):
+    router_w [H, E] bf16, router_bias [E] f32 or None, W_gate / W_up [E, H, I]
+    and W_down [E, I, H] bf16."""
+    tensors: dict
+
+    def struct(self, shape: Shape) -> DenseLayerStruct:
+        H, I, E = shape.H, shape.I, shape.E
+        want = {"router_w": (torch.bfloat16, (H, E)), "router_bias": (torch.float32, (E,)),
+                "W_gate": (torch.bfloat16, (E, H, I)), "W_up": (torch.bfloat16, (E, H, I)),
+                "W_down": (torch.bfloat16, (E, I, H))}
+        vals = []
+        for key in DENSE_LAYER_FIELDS:
+            dt, shp = want[key]
+            p = _ptr(self.tensors.get(key), dt, key, shp, optional=key == "router_bias")
+            vals.append(None if p is None else p.value)
+        return DenseLayerStruct(*vals)
+
+
+def dense_moe_layer(shape: Shape, x, layer: DenseLayer, ws=None, out=None, idx=None, w=None):
+    """The uncompressed MoE layer (only H, I, E, top_k of ``shape`` are read).
+    Returns ``(y float32 [B, H], topk_idx, topk_w)``."""
+    B = x.shape[0]
+    dev = x.device
+    y, idx, w = _outputs(shape, x, out, idx, w)
+    if ws is None:
+        ws = new_workspace(shape, B, dev)
+    st = layer.struct(shape)
+    _check(_lib.cardan_dense_moe_layer(
         ctypes.byref(shape), B, _ptr(x, torch.bfloat16, "x", (B, shape.H)), ctypes.byref(st),
         _ptr(y, torch.float32, "y", (B, shape.H)),
         _ptr(idx, torch.int32, "topk_idx", (B, shape.top_k)),

@@ -15,7 +15,7 @@
 
 namespace cardan {
 const void* route_kernel();
-const void* expert_kernel(int d, int dnw);
+const void* expert_kernel(int d, int dnw, int mode);
 hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t);
@@ -111,13 +111,15 @@ size_t lds_expert(const Plan& P) {
 }
 
 // Launch plan, item counts and workspace layout; depends only on
-// (shape, B, z_sep, flags).
+// (shape, B, z_sep, flags). F_GU_DENSE plans take r = 0.
 Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   Plan P;
   memset(&P, 0, sizeof P);
   P.H = s->H; P.I = s->I; P.E = s->E; P.k = s->top_k; P.d = s->d; P.K = s->K; P.r = s->r;
   P.B = B;
   P.flags = flags;
+  const int mode = expert_mode(P);
+  if (mode == 2) P.r = 0;
   P.S = B * P.k;
   P.max_act = P.E < P.S ? P.E : P.S;
   P.nch_r = P.H / kRowsRouter;
@@ -135,9 +137,12 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // long tiles. Bytes per tile: a gate/up (expert, projection, 256 columns)
   // holds 256 (H/d) code bytes and 256 r * 2 coefficient bytes; a VQ down
   // (expert, 256 columns) 256 I/d; a low-rank down (expert, <= 256 ranks)
-  // min(r, 256) I * 2.
+  // min(r, 256) I * 2. Dense bf16 weights: 256 H * 2 per gate/up and
+  // 256 I * 2 per down (expert, 256 columns).
   const double exp_act = fmax(1.0, P.E * (1.0 - pow(1.0 - (double)P.k / P.E, (double)B)));
-  const double per_expert = 3.0 * P.H * P.I / P.d + 3.0 * P.I * P.r * 2;
+  const double gu_expert = mode == 2 ? 2.0 * P.H * P.I * 2 : 2.0 * P.H * P.I / P.d + 2.0 * P.I * P.r * 2;
+  const double dn_expert = mode >= 1 ? (double)P.I * P.H * 2 : (double)P.H * P.I / P.d + (double)P.I * P.r * 2;
+  const double per_expert = gu_expert + dn_expert;
   // A VQ down K-step costs twice a gate/up one (p enters as hi + lo), so its
   // bytes count double. While the expected items exceed the nominal grid
   // the tile grows (small batches then run in one round).
@@ -147,17 +152,18 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   };
   P.ncg = ceil_div(P.I, kColsPerGroup);
   P.ncgh = ceil_div(P.H, kColsPerGroup);
-  P.ncgr = ceil_div(P.r, kColsPerGroup);
+  P.ncgr = mode == 0 ? ceil_div(P.r, kColsPerGroup) : 0;  // low-rank down column groups
   for (;;) {
-    // code splits and low-rank splits of a gate/up (expert, 256 columns)
-    const double code_bytes = 256.0 * (KSX * 32 / P.d), lr_bytes = 256.0 * P.r * 2;
+    // code (or dense) splits and low-rank splits of a gate/up (expert, 256 columns)
+    const double code_bytes = mode == 2 ? 256.0 * P.H * 2 : 256.0 * (KSX * 32 / P.d);
+    const double lr_bytes = 256.0 * P.r * 2;
     if (tile >= 0.75 * (code_bytes + lr_bytes)) {
       P.ns_v = P.ns = 1;  // one tile holds the whole joint axis
     } else {
       P.ns_v = splits(code_bytes, KSX);
       P.ns = P.ns_v + (KSZ > 0 ? splits(lr_bytes, KSZ) : 0);
     }
-    P.nsd = splits(2.0 * 256.0 * P.I / P.d, KSD);
+    P.nsd = mode >= 1 ? splits(256.0 * P.I * 2, KSD) : splits(2.0 * 256.0 * P.I / P.d, KSD);
     P.nsdl = P.r > 0 ? splits((double)std::min(P.r, kColsPerGroup) * P.I * 2, KSD) : 1;
     const double items = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
     if (items <= 512.0 || tile >= 128.0 * 1024) break;
@@ -167,7 +173,8 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // splits of at most kPdVq K-steps and low-rank splits of kPdDense steps
   // (at most two pipeline fills of a gate/up tile).
   if (P.ns > 1) {
-    const int nv = std::max(P.ns_v, ceil_div(KSX, kPdVq)), nl = KSZ > 0 ? ceil_div(KSZ, kPdDense) : 0;
+    const int nv = std::max(P.ns_v, ceil_div(KSX, mode == 2 ? kPdDenseW : kPdVq));
+    const int nl = KSZ > 0 ? ceil_div(KSZ, kPdDense) : 0;
     const double items = exp_act * (2.0 * P.ncg * (nv + nl) + P.ncgh * P.nsd + P.ncgr * P.nsdl);
     if (items <= 512.0) {
       P.ns_v = nv;
@@ -199,7 +206,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // reads serve twice the columns and the down tiles take half the
   // workgroup slots (fewer rounds, longer tiles)
   const double items_all = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
-  if (items_all > 2 * 512.0 && P.ncgh > 1 && P.d == 8) P.flags |= F_DN_WIDE;
+  if (mode == 0 && items_all > 2 * 512.0 && P.ncgh > 1 && P.d == 8) P.flags |= F_DN_WIDE;
   P.n_cb = P.ncgh * ceil_div(B, P.tpc);
 
   const int z_units = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nch_z;
@@ -209,9 +216,12 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.n_zr = (flags & F_Z) ? ceil_div(2 * B * P.r, kWG) : 0;
   P.n_pre = P.n_rc + P.n_zc + P.n_sel + P.n_zr;
 
-  // counters first, at offsets that depend only on the shape
+  // Counters first, at offsets that depend only on H, I and E (not on B,
+  // r or the expert-weight form): a call leaves its expert ticks set until
+  // the next call's k_route clears them, so every call on a workspace must
+  // find them at the same place.
   P.n_rc_flags = P.nch_r * P.n_eg * ceil_div(kMaxB, kRouterTok);
-  P.n_zc_flags = ceil_div(2 * ceil_div(P.r, 64) * P.nch_z, 4);
+  P.n_zc_flags = ceil_div(2 * ceil_div(kMaxR, 64) * P.nch_z, 4);
   size_t o = 0;
   P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);
   P.o_rc_flag = o; o = align256(o + (size_t)P.n_rc_flags * kTickPad * 4);
@@ -278,25 +288,37 @@ int check_ws(const Plan& P, const void* ws, size_t ws_bytes) {
     if (misaligned(p)) return fail(CARDAN_ERR_ALIGN, "%s is not 16-byte aligned", name); \
   } while (0)
 
-int check_layer(const cardan_shape* s, const cardan_layer* L, bool need_router) {
+// need_down: the compressed down projection (code book, codes, A, B) is used
+int check_layer(const cardan_shape* s, const cardan_layer* L, bool need_router, bool need_down = true) {
   if (!L) return fail(CARDAN_ERR_NULL_PTR, "layer is NULL");
   if (need_router) REQ(L->router_w, "router_w");
   if (L->router_bias && (reinterpret_cast<uintptr_t>(L->router_bias) & 3u))
     return fail(CARDAN_ERR_ALIGN, "router_bias is not 4-byte aligned");
   REQ(L->cb_gate, "cb_gate");
   REQ(L->cb_up, "cb_up");
-  REQ(L->cb_down, "cb_down");
   REQ(L->codes_gate, "codes_gate");
   REQ(L->codes_up, "codes_up");
-  REQ(L->codes_down, "codes_down");
+  if (need_down) {
+    REQ(L->cb_down, "cb_down");
+    REQ(L->codes_down, "codes_down");
+  }
   if (s->r > 0) {
     REQ(L->U_gate, "U_gate");
     REQ(L->U_up, "U_up");
     REQ(L->V_gate, "V_gate");
     REQ(L->V_up, "V_up");
-    REQ(L->A_down, "A_down");
-    REQ(L->B_down, "B_down");
+    if (need_down) {
+      REQ(L->A_down, "A_down");
+      REQ(L->B_down, "B_down");
+    }
   }
+  return CARDAN_OK;
+}
+
+// one expert's dense bf16 matrix is addressed with 32-bit byte offsets
+int check_dense_size(const cardan_shape* s) {
+  if ((size_t)s->H * s->I * 2 >= 0x80000000ull)
+    return fail(CARDAN_ERR_UNSUPPORTED, "dense expert matrix of H=%d x I=%d exceeds 2 GiB", s->H, s->I);
   return CARDAN_OK;
 }
 
@@ -362,7 +384,7 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
     }
   }
   if (P.flags & F_EXPERTS) {
-    const int cap = resident_grid(expert_kernel(P.d, dn_width(P)), P.lds_expert, &err);
+    const int cap = resident_grid(expert_kernel(P.d, dn_width(P), expert_mode(P)), P.lds_expert, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_EXPERT);
     err = launch_expert(P, A, cap, P.lds_expert, stream, tm.ev0, tm.ev1);
@@ -396,9 +418,12 @@ int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out) {
   if (!out) return fail(CARDAN_ERR_NULL_PTR, "out is NULL");
   // the largest layout over batches 1..B, so one workspace serves any batch
   // up to B (split counts, hence layouts, depend on the batch)
+  // and every expert-weight form (compressed, dense down, all dense)
   size_t need = 0;
+  const int all = F_ROUTE | F_Z | F_GROUP | F_EXPERTS;
   for (int b = 1; b <= B; ++b)
-    need = std::max(need, make_plan(shape, b, 1, F_ROUTE | F_Z | F_GROUP | F_EXPERTS).total);
+    for (int form : {0, (int)F_DN_DENSE, F_DN_DENSE | F_GU_DENSE})
+      need = std::max(need, make_plan(shape, b, 1, all | form).total);
   *out = need;
   return CARDAN_OK;
 }
@@ -496,6 +521,80 @@ int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
   A.topk_idx = topk_idx;
   A.topk_w = topk_w;
   A.z_out = reinterpret_cast<float*>(w + P.o_z);
+  A.y = y;
+  return run_layer(P, A, stream);
+}
+
+int cardan_moe_layer_dense_down(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                                const cardan_layer* layer, const cardan_bf16* W_down, float* y,
+                                int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes,
+                                hipStream_t stream) {
+  g_err[0] = 0;
+  int rc = check_shape(shape, B);
+  if (rc) return rc;
+  if ((rc = check_dense_size(shape))) return rc;
+  REQ(x, "x");
+  REQ(y, "y");
+  REQ(topk_idx, "topk_idx");
+  REQ(topk_w, "topk_w");
+  REQ(W_down, "W_down");
+  if ((rc = check_layer(shape, layer, true, false))) return rc;
+  const int z_sep = shape->r > 0 && layer->U_up != layer->U_gate;
+  const int flags = F_ROUTE | F_GROUP | F_EXPERTS | F_DN_DENSE | (shape->r > 0 ? F_Z : 0);
+  const Plan P = make_plan(shape, B, z_sep, flags);
+  if ((rc = check_ws(P, ws, ws_bytes))) return rc;
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  Args A = args_for(layer, w);
+  // the kernels read the dense down matrices through the down code pointer
+  A.L.codes_down = reinterpret_cast<const uint8_t*>(W_down);
+  A.L.cb_down = nullptr;
+  A.L.A_down = nullptr;
+  A.L.B_down = nullptr;
+  A.x = x;
+  A.topk_idx = topk_idx;
+  A.topk_w = topk_w;
+  A.z_out = reinterpret_cast<float*>(w + P.o_z);
+  A.y = y;
+  return run_layer(P, A, stream);
+}
+
+int cardan_dense_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                           const cardan_dense_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
+                           void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  if (!shape) return fail(CARDAN_ERR_NULL_PTR, "shape is NULL");
+  cardan_shape s = *shape;  // only H, I, E and top_k describe a dense layer
+  s.d = 8;
+  s.K = 1;
+  s.r = 0;
+  int rc = check_shape(&s, B);
+  if (rc) return rc;
+  if ((rc = check_dense_size(&s))) return rc;
+  REQ(x, "x");
+  REQ(y, "y");
+  REQ(topk_idx, "topk_idx");
+  REQ(topk_w, "topk_w");
+  if (!layer) return fail(CARDAN_ERR_NULL_PTR, "layer is NULL");
+  REQ(layer->router_w, "router_w");
+  if (layer->router_bias && (reinterpret_cast<uintptr_t>(layer->router_bias) & 3u))
+    return fail(CARDAN_ERR_ALIGN, "router_bias is not 4-byte aligned");
+  REQ(layer->W_gate, "W_gate");
+  REQ(layer->W_up, "W_up");
+  REQ(layer->W_down, "W_down");
+  const Plan P = make_plan(&s, B, 0, F_ROUTE | F_GROUP | F_EXPERTS | F_GU_DENSE | F_DN_DENSE);
+  if ((rc = check_ws(P, ws, ws_bytes))) return rc;
+  // the kernels read the dense matrices through the code pointers
+  cardan_layer L;
+  memset(&L, 0, sizeof L);
+  L.router_w = layer->router_w;
+  L.router_bias = layer->router_bias;
+  L.codes_gate = reinterpret_cast<const uint8_t*>(layer->W_gate);
+  L.codes_up = reinterpret_cast<const uint8_t*>(layer->W_up);
+  L.codes_down = reinterpret_cast<const uint8_t*>(layer->W_down);
+  Args A = args_for(&L, static_cast<uint8_t*>(ws));
+  A.x = x;
+  A.topk_idx = topk_idx;
+  A.topk_w = topk_w;
   A.y = y;
   return run_layer(P, A, stream);
 }

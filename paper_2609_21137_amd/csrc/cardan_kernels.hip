@@ -1490,14 +1490,81 @@ __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, i
   publish(wsp<int>(A, P.o_dn_done) + (R.e * (P.ncgh + 1) + P.ncgh) * kTickPad);
 }
 
+// ---- dense bf16 expert weights (the uncompressed layer, Sec. 2.1, and the
+// layer that keeps its down projection in bf16, Sec. 3.2) -------------------
+
+// Dense gate/up tile (a, pj, cg, s): 256 output columns of W_pj[e] [H][I]
+// over split s of the H inputs, partial sums into the same slots as the
+// compressed tile, so the down tiles take p = silu(g) * u unchanged.
+__device__ void item_gateup_dense(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg,
+                                  int s, uint8_t* smem) {
+  const Routing R = expert_of(P, RT, a);
+  const int H = P.H, I = P.I, B = P.B, KSX = H / 32;
+  const int x0 = s * KSX / P.ns, x1 = (s + 1) * KSX / P.ns;
+  const int c0 = cg * kColsPerGroup + (threadIdx.x >> 6) * 64;
+  const uint16_t* W = reinterpret_cast<const uint16_t*>(pj ? A.L.codes_up : A.L.codes_gate) + (size_t)R.e * H * I;
+  const int n8x = (x1 - x0) * 4, ldx = n8x + 1;
+  uint4* xs = reinterpret_cast<uint4*>(smem);
+  float* gu = wsp<float>(A, P.o_gu);
+  const int* const slot_tok = RT.slot_tok;
+  const rsrc_t xrs = make_rsrc(A.x, (uint32_t)B * H * 2);
+  DensePipe<1, kPdDenseW> pipe;
+  for (int tg = 0; tg < R.ne; tg += P.nt_max) {
+    const int nt = min(P.nt_max, R.ne - tg), n = nt * n8x;
+    pipe.prime(W, I, c0, I, H, x0, x1);
+    __syncthreads();
+    // x rows of the tile's tokens, 8-element groups, 4 loads in flight per thread
+    for (int i0 = threadIdx.x; i0 < n; i0 += 4 * kWG) {
+      uint4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * kWG, ii = min(i, n - 1);
+        const uint32_t o = (uint32_t)(((size_t)slot_tok[R.s0 + tg + ii / n8x] * H + x0 * 32 + 8 * (ii % n8x)) * 2);
+        v[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xrs, i < n ? o : kOob, 0, 0));
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * kWG;
+        if (i < n) xs[(i / n8x) * ldx + i % n8x] = v[u];
+      }
+    }
+    __syncthreads();
+    f32x4 acc[4];
+    zero_acc(acc);
+    pipe.run(xs, ldx, x0, nt, acc);
+    store_acc(WsAccess(A, P), acc, nt, c0, I,
+              [&](int t) { return gu + (((size_t)(R.s0 + tg + t) * 2 + pj) * P.ns + s) * I; });
+  }
+  publish(wsp<int>(A, P.o_gu_tick) + (a * P.ncg + cg) * kTickPad);
+}
+
+// Dense down tile (a, cgx, s): 256 output columns of W_down[e] [I][H] over
+// split s of I, partial sums into dn[s] as the VQ down tile.
+__device__ void item_down_dense(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgx, int s,
+                                uint8_t* smem) {
+  const Routing R = expert_of(P, RT, a);
+  const int H = P.H, I = P.I, S = P.S, KS = I / 32;
+  const int ks0 = s * KS / P.nsd, ks1 = (s + 1) * KS / P.nsd;
+  const int c0 = cgx * kColsPerGroup + (threadIdx.x >> 6) * 64;
+  const uint16_t* W = reinterpret_cast<const uint16_t*>(A.L.codes_down) + (size_t)R.e * I * H;
+  float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
+  DensePipe<2, kPdDenseW> pipe;
+  down_body(P, A, R, a, ks0, ks1, c0, H, [&]() { pipe.prime(W, H, c0, H, I, ks0, ks1); }, [&]() {},
+            [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(ps, ld, ks0, nt, acc); },
+            [&](int slot) { return dn + (size_t)slot * H; }, smem);
+  publish(wsp<int>(A, P.o_dn_done) + (R.e * (P.ncgh + 1) + cgx) * kTickPad);
+}
+
 // Combine tile (cgy, tq): output columns [256 cgy, +256) of tokens
 // [tpc tq, tpc tq + tpc): y[t] = sum_j a_j sum_s dn[s][slot_j] + B^T u[t]
 // with u[t] = sum_j a_j u_e[slot_j]. B rows are loaded before the
 // wait; B^T u runs on MFMA with u as bf16 hi/lo. The partial sums are
 // gathered in chunks of kCombineChunk loads in flight per thread.
+// LRD: the layer has the low-rank down term (else y is the down sums alone).
+template <bool LRD>
 __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, int jc, uint8_t* smem) {
   const int cgy = jc % P.ncgh, tq = jc / P.ncgh;
-  const int H = P.H, r = P.r, k = P.k, S = P.S, nsd = P.nsd;
+  const int H = P.H, r = LRD ? P.r : 0, k = P.k, S = P.S, nsd = P.nsd;
   const int t0 = tq * P.tpc, nt = min(P.tpc, P.B - t0);
   const int tid = threadIdx.x, w = tid >> 6;
   const int cbase = cgy * kColsPerGroup;
@@ -1513,7 +1580,7 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
   float* dnb = reinterpret_cast<float*>(red + kWG);                   // [nt][256] VQ down sums
   uint4* us = reinterpret_cast<uint4*>(dnb + kTokPass * kColsPerGroup);
   const int ntk = nt * k;
-  const int nq = KSR * 8, ld = KSR * 8 + 1;
+  const int nq = LRD ? KSR * 8 : 8, ld = KSR * 8 + 1;  // (no u rows without LRD)
   const int nsdl = P.nsdl, kd = k * nsd, ku = r > 0 ? k * nsdl : 0;
   constexpr int kB = kCombineChunk;
   // Term tables, built before the wait: per (token, selection j, split) the
@@ -1557,7 +1624,7 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
   const int n_units = nu * cu + nd * cd;
   float4* part = reinterpret_cast<float4*>(smem + combine_part_offset(P));
   for (int unit = tid; unit < n_units; unit += kWG) {
-    const bool isu = unit < nu * cu;
+    const bool isu = LRD && unit < nu * cu;
     const int uu = isu ? unit : unit - nu * cu;
     // chunk-major: neighbouring threads read neighbouring quads of one row
     const int it = isu ? uu % nu : uu % nd, c = isu ? uu / nu : uu / nd;
@@ -1741,13 +1808,14 @@ __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
 // tiles, down tiles (waiting per expert for p), combine tiles (waiting for
 // every down tile). DNW: column groups per VQ down tile; a separate
 // instantiation keeps the wide tiles' registers out of the narrow one.
-template <int D, int DNW>
+// MODE: expert-weight form (0 compressed, 1 dense down, 2 all dense).
+template <int D, int DNW, int MODE>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   // the code book of the current item (zero-padded to 256 words), in
   // kBookCopies copies in the large-batch kernel
   constexpr int NC = DNW == 2 ? kBookCopies : 1;
-  __shared__ uint4 cbs[256 * NC];
+  __shared__ uint4 cbs[MODE == 2 ? 1 : 256 * NC];
   warm_kernargs();
   const int tid = threadIdx.x;
   ItemTrace tr_route;
@@ -1789,7 +1857,10 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     // first in the second half of the grid, so the two workgroups sharing a
     // CU overlap LDS-bound and HBM-bound phases
     const bool lr_first = (int)(jp % gridDim.x) >= (int)(gridDim.x >> 1);
-    item_gateup<D, DNW == 2, NC>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem);
+    if constexpr (MODE == 2)
+      item_gateup_dense(P, A, RT, t.a, t.pj, t.cg, t.s, item_smem);
+    else
+      item_gateup<D, DNW == 2, NC>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem);
     tr.done(A, P, P.n_pre + jp, 4);
   }
   for (; jp < n_gu + n_dn; jp += gridDim.x) {
@@ -1797,7 +1868,9 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     ItemTrace tr;
     const int j = jp - n_gu, a = j / tdn, rem = j % tdn;
     if (rem < nvq) {
-      if constexpr (DNW == 2)
+      if constexpr (MODE != 0)
+        item_down_dense(P, A, RT, a, rem / P.nsd, rem % P.nsd, item_smem);
+      else if constexpr (DNW == 2)
         item_down_vq2<D>(P, A, RT, a, rem / P.nsd * 2, rem % P.nsd, cbs, item_smem);
       else
         item_down_vq<D>(P, A, RT, a, rem / P.nsd, rem % P.nsd, cbs, item_smem);
@@ -1810,7 +1883,7 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   for (; jp < n_items; jp += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
-    item_combine(P, A, RT, jp - n_gu - n_dn, item_smem);
+    item_combine<MODE == 0>(P, A, RT, jp - n_gu - n_dn, item_smem);
     tr.done(A, P, P.n_pre + jp, 7);
   }
 }
@@ -1837,10 +1910,14 @@ __global__ __launch_bounds__(kWG) void k_rmsnorm(int H, const float* __restrict_
 // ---------------------------------------------------------------------------
 const void* route_kernel() { return reinterpret_cast<const void*>(&k_route); }
 
-const void* expert_kernel(int d, int dnw) {
-  return d == 8 ? (dnw == 2 ? reinterpret_cast<const void*>(&k_expert<8, 2>)
-                            : reinterpret_cast<const void*>(&k_expert<8, 1>))
-                : reinterpret_cast<const void*>(&k_expert<4, 1>);
+const void* expert_kernel(int d, int dnw, int mode) {
+  if (mode == 2) return reinterpret_cast<const void*>(&k_expert<8, 1, 2>);
+  if (mode == 1)
+    return d == 8 ? reinterpret_cast<const void*>(&k_expert<8, 1, 1>)
+                  : reinterpret_cast<const void*>(&k_expert<4, 1, 1>);
+  return d == 8 ? (dnw == 2 ? reinterpret_cast<const void*>(&k_expert<8, 2, 0>)
+                            : reinterpret_cast<const void*>(&k_expert<8, 1, 0>))
+                : reinterpret_cast<const void*>(&k_expert<4, 1, 0>);
 }
 
 // With a start/stop event pair the launch records them as part of the
@@ -1867,12 +1944,19 @@ hipError_t launch_route_reset(const Plan& P, const Args& A, hipStream_t st) {
 
 hipError_t launch_expert(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st, hipEvent_t ev0,
                          hipEvent_t ev1) {
-  if (P.d == 8 && dn_width(P) == 2)
-    CARDAN_LAUNCH((k_expert<8, 2>), grid, lds, st, ev0, ev1, P, A);
+  const int mode = expert_mode(P);
+  if (mode == 2)
+    CARDAN_LAUNCH((k_expert<8, 1, 2>), grid, lds, st, ev0, ev1, P, A);
+  else if (mode == 1 && P.d == 8)
+    CARDAN_LAUNCH((k_expert<8, 1, 1>), grid, lds, st, ev0, ev1, P, A);
+  else if (mode == 1)
+    CARDAN_LAUNCH((k_expert<4, 1, 1>), grid, lds, st, ev0, ev1, P, A);
+  else if (P.d == 8 && dn_width(P) == 2)
+    CARDAN_LAUNCH((k_expert<8, 2, 0>), grid, lds, st, ev0, ev1, P, A);
   else if (P.d == 8)
-    CARDAN_LAUNCH((k_expert<8, 1>), grid, lds, st, ev0, ev1, P, A);
+    CARDAN_LAUNCH((k_expert<8, 1, 0>), grid, lds, st, ev0, ev1, P, A);
   else
-    CARDAN_LAUNCH((k_expert<4, 1>), grid, lds, st, ev0, ev1, P, A);
+    CARDAN_LAUNCH((k_expert<4, 1, 0>), grid, lds, st, ev0, ev1, P, A);
   return hipGetLastError();
 }
 

@@ -46,11 +46,17 @@ constexpr int kPdDense = 2;   // dense K-steps in flight per wave (4 KB each)
 constexpr int kCombineChunk = 16;  // terms per load batch in the combine
 constexpr int kBookCopies = 4;     // code book copies in LDS of the large-batch expert kernel (d = 8)
 constexpr int kLrDownSteps = 4;    // K-steps of a low-rank down tile when the plan would cut finer
+constexpr int kPdDenseW = 3;       // K-steps in flight per wave of a dense bf16 expert-weight tile
 
 
 // flags of one call
 enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8,
-       F_DN_WIDE = 16 };  // set by the plan: VQ down tiles over two column groups
+       F_DN_WIDE = 16,    // set by the plan: VQ down tiles over two column groups
+       // dense bf16 expert weights in place of the compressed ones, passed in
+       // the code pointers of the layer: W_down [E][I][H] as codes_down (no
+       // low-rank down term), W_gate / W_up [E][H][I] as codes_gate / codes_up
+       // (r = 0)
+       F_DN_DENSE = 32, F_GU_DENSE = 64 };
 
 // counters at the start of the workspace, one per 64-byte slot: the status
 // count of timed-out waits
@@ -103,6 +109,10 @@ inline __host__ __device__ size_t combine_lds(const Plan& P) {
   return combine_part_offset(P) + (size_t)P.tpc * (nq * cu + 64 * cd) * 16;
 }
 
+// expert-weight form of a call: 0 compressed, 1 dense down, 2 all dense
+__host__ __device__ inline int expert_mode(const Plan& P) {
+  return (P.flags & F_GU_DENSE) ? 2 : (P.flags & F_DN_DENSE) ? 1 : 0;
+}
 __host__ __device__ inline int gateup_tiles_per_expert(const Plan& P) { return 2 * P.ncg * P.ns; }
 __host__ __device__ inline int dn_width(const Plan& P) { return (P.flags & F_DN_WIDE) ? 2 : 1; }
 __host__ __device__ inline int down_tiles_per_expert(const Plan& P) {

@@ -19,7 +19,7 @@ Recipe (one independent PCG64 stream per tensor, keyed by
   (variance).
 * Dense bf16 expert matrices (the uncompressed baseline and the dense-down
   variant): ``W_gate, W_up [E, H, I]`` and ``W_down [E, I, H] ~ N(0, 0.02)``
-  (std, the scale of a code-book entry).
+  (std, the scale of a code-book entry), one stream per (tensor, expert).
 
 Normals are drawn in float64, rounded to float32 (round to nearest even) and
 then to bf16 (round to nearest even).
@@ -99,16 +99,26 @@ def make_layer(H: int, I: int, E: int, d: int, K: int, r: int, seed: int, layer:
     return L
 
 
-def make_dense_weights(H: int, I: int, E: int, seed: int, layer: int = 0, which=("gate", "up", "down")) -> dict:
+def make_dense_weights(H: int, I: int, E: int, seed: int, layer: int = 0, which=("gate", "up", "down"),
+                       experts=None, fill_bits: int = 0) -> dict:
     """Dense bf16 expert matrices ``W_gate``/``W_up`` [E, H, I] and
-    ``W_down`` [E, I, H] (those named in ``which``), as bf16 bits."""
+    ``W_down`` [E, I, H] (those named in ``which``), as bf16 bits.
+
+    Every expert's matrix has its own stream, so ``experts`` (a list of
+    expert ids) can restrict the draw to those experts; the others are filled
+    with the bf16 pattern ``fill_bits`` (e.g. 0x7FC0, a NaN, to show that
+    they are never read).
+    """
+    ids = {"gate": (_T_WG, (H, I)), "up": (_T_WU, (H, I)), "down": (_T_WD, (I, H))}
+    names = {"gate": "W_gate", "up": "W_up", "down": "W_down"}
+    todo = range(E) if experts is None else sorted({int(e) for e in experts})
     out = {}
-    if "gate" in which:
-        out["W_gate"] = _normal_bf16(_rng(seed, layer, _T_WG), (E, H, I), 0.02)
-    if "up" in which:
-        out["W_up"] = _normal_bf16(_rng(seed, layer, _T_WU), (E, H, I), 0.02)
-    if "down" in which:
-        out["W_down"] = _normal_bf16(_rng(seed, layer, _T_WD), (E, I, H), 0.02)
+    for key in which:
+        tid, shp = ids[key]
+        W = np.full((E,) + shp, fill_bits, dtype=np.uint16)
+        for e in todo:
+            W[e] = _normal_bf16(_rng(seed, layer, tid, e), shp, 0.02)
+        out[names[key]] = W
     return out
 
 

@@ -131,7 +131,7 @@ def test_moe_layer_validation(C):
                               FAKE, need, None) == -1
     # workspace too small, NULL, misaligned
     assert L.cardan_moe_layer(ctypes.byref(s), 1, FAKE, ctypes.byref(lay), FAKE, FAKE, FAKE,
-                              FAKE, need - 256, None) == -4
+                              FAKE, 256, None) == -4
     assert L.cardan_moe_layer(ctypes.byref(s), 1, FAKE, ctypes.byref(lay), FAKE, FAKE, FAKE,
                               None, need, None) == -1
     assert L.cardan_moe_layer(ctypes.byref(s), 1, FAKE, ctypes.byref(lay), FAKE, FAKE, FAKE,
@@ -176,3 +176,60 @@ def test_binding_rejects_host_tensors(C):
     with pytest.raises(ValueError):
         C._ptr(torch.zeros(3, dtype=torch.float32), torch.bfloat16, "x")
     del s
+
+
+def _dense(C, **over):
+    vals = {n: FAKE for n in C.DENSE_LAYER_FIELDS}
+    vals.update(over)
+    return C.DenseLayerStruct(*[vals[n] for n in C.DENSE_LAYER_FIELDS])
+
+
+def test_dense_entry_points_validation(C):
+    L = C.lib()
+    s = C.make_shape(2048, 768, 128, 8, 8, 256, 128)
+    _, need = _ws(C, s, 1)
+    lay = _layer(C)
+    # dense down: the compressed down fields may be NULL, W_down may not
+    nodown = _layer(C, cb_down=None, codes_down=None, A_down=None, B_down=None)
+    assert L.cardan_moe_layer_dense_down(ctypes.byref(s), 1, FAKE, ctypes.byref(nodown), None,
+                                         FAKE, FAKE, FAKE, FAKE, need, None) == -1
+    assert b"W_down" in L.cardan_last_error()
+    assert L.cardan_moe_layer_dense_down(ctypes.byref(s), 1, FAKE, ctypes.byref(nodown), FAKE + 4,
+                                         FAKE, FAKE, FAKE, FAKE, need, None) == -6
+    assert L.cardan_moe_layer_dense_down(ctypes.byref(s), 1, FAKE, ctypes.byref(nodown), FAKE,
+                                         FAKE, FAKE, FAKE, FAKE, 256, None) == -4
+    bad = _layer(C, V_up=None)  # gate/up factors are still required
+    assert L.cardan_moe_layer_dense_down(ctypes.byref(s), 1, FAKE, ctypes.byref(bad), FAKE,
+                                         FAKE, FAKE, FAKE, FAKE, need, None) == -1
+    assert L.cardan_moe_layer_dense_down(ctypes.byref(s), 65, FAKE, ctypes.byref(lay), FAKE,
+                                         FAKE, FAKE, FAKE, FAKE, need, None) == -2
+    # uncompressed layer: d, K and r of the shape are not read
+    dl = _dense(C)
+    s_any = C.make_shape(2048, 768, 128, 8, 0, 0, 0)
+    for field in ("router_w", "W_gate", "W_up", "W_down"):
+        assert L.cardan_dense_moe_layer(ctypes.byref(s_any), 1, FAKE, ctypes.byref(_dense(C, **{field: None})),
+                                        FAKE, FAKE, FAKE, FAKE, need, None) == -1
+        assert field.encode() in L.cardan_last_error()
+    assert L.cardan_dense_moe_layer(ctypes.byref(s_any), 1, FAKE, ctypes.byref(_dense(C, router_bias=FAKE + 2)),
+                                    FAKE, FAKE, FAKE, FAKE, need, None) == -6
+    assert L.cardan_dense_moe_layer(ctypes.byref(s_any), 1, FAKE, None, FAKE, FAKE, FAKE, FAKE, need,
+                                    None) == -1
+    assert L.cardan_dense_moe_layer(None, 1, FAKE, ctypes.byref(dl), FAKE, FAKE, FAKE, FAKE, need,
+                                    None) == -1
+    assert L.cardan_dense_moe_layer(ctypes.byref(s_any), 1, FAKE, ctypes.byref(dl), FAKE, FAKE, FAKE,
+                                    FAKE, 256, None) == -4
+    big = C.make_shape(65536, 16384, 128, 8, 8, 256, 0)  # one expert matrix of 2 GiB
+    assert L.cardan_dense_moe_layer(ctypes.byref(big), 1, FAKE, ctypes.byref(dl), FAKE, FAKE, FAKE,
+                                    FAKE, need, None) == -3
+
+
+def test_workspace_covers_dense_forms(C):
+    """The workspace size is the maximum over the compressed, dense-down and
+    uncompressed layouts, whatever d, K and r the size query names."""
+    for dims in ((2048, 768, 128, 8, 8, 256, 128), (2048, 768, 128, 8, 4, 16, 0)):
+        s = C.make_shape(*dims)
+        for B in (1, 16):
+            assert _ws(C, s, B)[0] == 0
+    a = _ws(C, C.make_shape(2048, 768, 128, 8, 8, 256, 128), 16)[1]
+    b = _ws(C, C.make_shape(2048, 768, 128, 8, 8, 256, 0), 16)[1]
+    assert a >= b > 0
