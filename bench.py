@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--also", default="qwen3_30b_a3b_moe_layer_b16,wide_h4096_i1536_e64_top6_b4_skewed,"
                     "qwen3_48_layer_decode_step_b16",
                     help="comma-separated extra workloads timed the same way (reported under 'also')")
+    ap.add_argument("--dense", default="qwen3_30b_a3b_moe_layer_b1,qwen3_30b_a3b_moe_layer_b16",
+                    help="workloads also timed with dense bf16 expert weights (the uncompressed "
+                         "layer and the dense-down layer) on the same routing and inputs")
     ap.add_argument("--layers", type=int, default=8, help="independently seeded layers rotated")
     ap.add_argument("--inputs", type=int, default=64,
                     help="distinct seeded inputs rotated (a multiple of --layers), so that the "
@@ -84,6 +87,21 @@ def compressed_bytes(w, n_active: int, z_sep: bool = False) -> dict:
             "per_expert_gateup": per_gateup, "per_expert_down": per_down}
 
 
+def dense_bytes(w, n_active: int, form: str) -> dict:
+    """Algorithmic bytes of one step of a dense-weight form: the active
+    experts' bf16 matrices (and, for the dense-down form, the compressed
+    gate/up factors, the basis U and two code books); router counted apart."""
+    router = w.H * w.E * 2 + w.E * 4
+    dn = w.I * w.H * 2
+    if form == "dense":
+        expert = n_active * (2 * w.H * w.I * 2 + dn)
+        return {"weights": expert, "expert_kernel": expert, "route_kernel": router}
+    gu = 2 * (w.H * w.I // w.d) + 2 * (w.r * w.I * 2)
+    expert = n_active * (gu + dn) + 2 * w.K * w.d * 2
+    basis_u = w.H * w.r * 2
+    return {"weights": expert + basis_u, "expert_kernel": expert, "route_kernel": router + basis_u}
+
+
 def load_traffic(kernel: str, workload: str, src_hash: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
     taken on the current kernel sources (else None)."""
@@ -97,7 +115,31 @@ def load_traffic(kernel: str, workload: str, src_hash: str):
     return rec.get("hbm_bytes_per_launch")
 
 
-def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache):
+def dense_weights(torch, w, n_layers, dense_cache, form):
+    """Dense bf16 expert matrices per rotated layer, drawn on the device from
+    seeded generators (N(0, 0.02), the synthetic recipe's law; drawing the
+    1.2 GB per layer on the host would dominate the run)."""
+    key = (w.H, w.I, w.E, w.seed, form)
+    if key not in dense_cache:
+        dense_cache.clear()
+        torch.cuda.empty_cache()
+        mats = []
+        for li in range(n_layers):
+            g = torch.Generator(device="cuda")
+            g.manual_seed(1_000_003 * w.seed + li)
+            m = {}
+            names = ("W_gate", "W_up", "W_down") if form == "dense" else ("W_down",)
+            for n in names:
+                shp = (w.E, w.I, w.H) if n == "W_down" else (w.E, w.H, w.I)
+                m[n] = (torch.randn(shp, generator=g, device="cuda", dtype=torch.float32) * 0.02
+                        ).to(torch.bfloat16)
+            mats.append(m)
+        dense_cache[key] = mats
+    return dense_cache[key]
+
+
+def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache, form="compressed",
+                  dense_cache=None):
     from paper_2609_21137_amd import synth
     shape = C.shape_of(w)
     key = (w.H, w.I, w.E, w.d, w.K, w.r, w.seed, w.hot_experts, w.hot_bias)
@@ -119,6 +161,7 @@ def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache):
     structs = [dl.struct() for dl in dls]
 
     # routing (hence the active-expert count) is fixed per (layer, input)
+    # and the same in every form (the router weights are the layer's)
     n_act = []
     for j in range(n_inputs):
         C.moe_layer(shape, xs[j], dls[j % n_layers], ws=ws, out=y, idx=idx, w=wt)
@@ -128,15 +171,38 @@ def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache):
     import ctypes
     lib = C.lib()
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    ptrs = [(ctypes.c_void_p(xs[j].data_ptr()), structs[j % n_layers]) for j in range(n_inputs)]
     args_tail = (ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(idx.data_ptr()),
                  ctypes.c_void_p(wt.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(), stream)
-    fn = lib.cardan_moe_layer
     B = w.B
+    if form == "compressed":
+        fn = lib.cardan_moe_layer
+        ptrs = [(ctypes.c_void_p(xs[j].data_ptr()), structs[j % n_layers]) for j in range(n_inputs)]
+
+        def call(xp, st):
+            return fn(ctypes.byref(shape), B, xp, ctypes.byref(st), *args_tail)
+    elif form == "dense_down":
+        fn = lib.cardan_moe_layer_dense_down
+        mats = dense_weights(torch, w, n_layers, dense_cache, form)
+        ptrs = [(ctypes.c_void_p(xs[j].data_ptr()),
+                 (structs[j % n_layers], ctypes.c_void_p(mats[j % n_layers]["W_down"].data_ptr())))
+                for j in range(n_inputs)]
+
+        def call(xp, st):
+            return fn(ctypes.byref(shape), B, xp, ctypes.byref(st[0]), st[1], *args_tail)
+    else:
+        fn = lib.cardan_dense_moe_layer
+        mats = dense_weights(torch, w, n_layers, dense_cache, form)
+        dstructs = [C.DenseLayer({"router_w": dls[li].tensors["router_w"],
+                                  "router_bias": dls[li].tensors["router_bias"], **mats[li]}).struct(shape)
+                    for li in range(n_layers)]
+        ptrs = [(ctypes.c_void_p(xs[j].data_ptr()), dstructs[j % n_layers]) for j in range(n_inputs)]
+
+        def call(xp, st):
+            return fn(ctypes.byref(shape), B, xp, ctypes.byref(st), *args_tail)
 
     def step(i):
         xp, st = ptrs[i % n_inputs]
-        rc = fn(ctypes.byref(shape), B, xp, ctypes.byref(st), *args_tail)
+        rc = call(xp, st)
         if rc != 0:
             raise RuntimeError(lib.cardan_last_error().decode())
 
@@ -166,7 +232,11 @@ def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache):
     acts = [n_act[i % n_inputs] for i in range(steps)]
     tot = {"compressed": 0, "expert_kernel": 0, "route_kernel": 0}
     for a in acts:
-        b = compressed_bytes(w, a)
+        if form == "compressed":
+            b = compressed_bytes(w, a)
+        else:
+            b = dense_bytes(w, a, form)
+            b["compressed"] = b["weights"]  # the form's own weight bytes
         for k in tot:
             tot[k] += b[k]
     return {"wall_s": wall, "wall_events_s": wall_events, "prof": prof, "bytes": tot,
@@ -279,15 +349,16 @@ def cpu_baseline(w, budget_s):
                       f"{t_tot:.1f} s total, {1e3 * t_tot / n:.1f} ms/step"}
 
 
-def summarize(w, r, src_hash):
+def summarize(w, r, src_hash, name=None):
     prof = r["prof"]
     steps = prof["expert"][1]
     ex_ms = prof["expert"][0] / max(1, steps)
     ex_bytes = r["bytes"]["expert_kernel"] / max(1, steps)
     achieved = ex_bytes / (ex_ms * 1e-3) / 1e9
-    traffic = load_traffic("k_expert", w.name, src_hash)
+    name = name or w.name
+    traffic = load_traffic("k_expert", name, src_hash)
     return {
-        "workload": w.name,
+        "workload": name,
         "B": w.B,
         "us_per_layer": round(1e6 * r["wall_s"] / steps, 3),
         "us_per_layer_with_kernel_events": round(1e6 * r["wall_events_s"] / steps, 3),
@@ -399,6 +470,27 @@ def main():
         also.append(summarize(ww, rr, src_hash))
         print(f"[bench] {ww.name}: {also[-1]['us_per_layer']} us/layer", file=sys.stderr,
               flush=True)
+    # the same workloads with dense bf16 expert weights: the uncompressed layer
+    # and the dense-down layer, on the compressed layers' routing and inputs
+    dense_cache = {}
+    by_name = {main_sum["workload"]: main_sum, **{a["workload"]: a for a in also}}
+    for name in [s for s in args.dense.split(",") if s]:
+        ww = WORKLOADS[name]
+        for form, suffix in (("dense", "_dense_bf16"), ("dense_down", "_dense_down")):
+            print(f"[bench] {ww.name} ({form})", file=sys.stderr, flush=True)
+            rr = time_workload(C, torch, ww, args.steps, args.warmup, args.layers, args.inputs, cache,
+                               form=form, dense_cache=dense_cache)
+            sm = summarize(ww, rr, src_hash, name=ww.name + suffix)
+            sm["form"] = form
+            sm["weight_GBps"] = sm.pop("GBps")
+            comp = by_name.get(ww.name)
+            if comp is not None:
+                sm["compressed_us_per_layer"] = comp["us_per_layer"]
+                sm["compressed_speedup"] = round(sm["us_per_layer"] / comp["us_per_layer"], 3)
+            also.append(sm)
+            print(f"[bench] {ww.name} ({form}): {sm['us_per_layer']} us/layer", file=sys.stderr,
+                  flush=True)
+        dense_cache.clear()
     cache.clear()
     cpu = None
     if not args.no_cpu_baseline:
