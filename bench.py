@@ -36,7 +36,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="qwen3_30b_a3b_moe_layer_b1")
     ap.add_argument("--also", default="qwen3_30b_a3b_moe_layer_b16,wide_h4096_i1536_e64_top6_b4_skewed,"
-                    "qwen3_48_layer_decode_step_b16",
+                    "qwen3_48_layer_decode_step_b16,deepseek_v2_lite_moe_layer_b1,"
+                    "olmoe_1b_7b_moe_layer_b1,gemma4_26b_a4b_moe_layer_b1",
                     help="comma-separated extra workloads timed the same way (reported under 'also')")
     ap.add_argument("--dense", default="qwen3_30b_a3b_moe_layer_b1,qwen3_30b_a3b_moe_layer_b16",
                     help="workloads also timed with dense bf16 expert weights (the uncompressed "
@@ -50,6 +51,11 @@ def parse():
                     help="write profiles/k_expert_<workload>_pmc.json from rocprofv3 --pmc "
                          "FETCH_SIZE / WRITE_SIZE counter CSVs of a bench run and of a "
                          "--calibrate-copy-mb run, then exit")
+    ap.add_argument("--pmc-kernel", default="k_expert",
+                    help="--summarize-pmc: substring of the kernel name summarized (e.g. "
+                         "'k_expert<8, 1, 2>' for the dense layer's expert kernel)")
+    ap.add_argument("--pmc-name", default=None,
+                    help="--summarize-pmc: record name (default: --workload)")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
@@ -404,9 +410,10 @@ def summarize_pmc(args):
     copy_bytes = args.calibrate_copy_mb * (1 << 20)
     f_scale = copy_bytes / (cal_f[copy][1] * 1024)
     w_scale = copy_bytes / (cal_w[copy][1] * 1024)
-    name = next(k for k in fetch if "k_expert" in k)
+    name = next(k for k in fetch if args.pmc_kernel in k)
+    wl = args.pmc_name or args.workload
     rec = {
-        "kernel": name, "workload": args.workload, "kernel_source_hash": kernel_source_hash(),
+        "kernel": name, "workload": wl, "kernel_source_hash": kernel_source_hash(),
         "dispatches": fetch[name][0],
         "FETCH_SIZE_KiB_per_dispatch": round(fetch[name][1], 3),
         "WRITE_SIZE_KiB_per_dispatch": round(write[name][1], 3),
@@ -417,7 +424,7 @@ def summarize_pmc(args):
         "hbm_write_bytes_per_launch": round(write[name][1] * 1024 * w_scale),
     }
     rec["hbm_bytes_per_launch"] = rec["hbm_read_bytes_per_launch"] + rec["hbm_write_bytes_per_launch"]
-    out = os.path.join(ROOT, "profiles", f"k_expert_{args.workload}_pmc.json")
+    out = os.path.join(ROOT, "profiles", f"k_expert_{wl}_pmc.json")
     with open(out, "w") as f:
         json.dump(rec, f, indent=1)
         f.write("\n")
@@ -466,7 +473,8 @@ def main():
             print(f"[bench] {ww.name}: {also[-1]['ms_per_step']} ms/step", file=sys.stderr, flush=True)
             continue
         print(f"[bench] {ww.name}", file=sys.stderr, flush=True)
-        rr = time_workload(C, torch, ww, args.steps, args.warmup, args.layers, args.inputs, cache)
+        rr = time_workload(C, torch, ww, args.steps, args.warmup, ww.rotate_layers or args.layers,
+                           args.inputs, cache)
         also.append(summarize(ww, rr, src_hash))
         print(f"[bench] {ww.name}: {also[-1]['us_per_layer']} us/layer", file=sys.stderr,
               flush=True)

@@ -26,6 +26,7 @@ class Workload:
     layers: int = 1
     hot_experts: tuple = ()      # experts whose router logit gets +hot_bias
     hot_bias: float = 0.0
+    rotate_layers: int = 0       # layers a benchmark rotates over (0: its default)
     description: str = field(default="", compare=False)
 
     @property
@@ -49,4 +50,18 @@ QWEN3_48L_B16 = Workload("qwen3_48_layer_decode_step_b16", H=2048, I=768, E=128,
                          K=256, r=128, B=16, seed=1, layers=48,
                          description="48 stacked Qwen3-shaped layers, RMS-normalised between")
 
-WORKLOADS = {w.name: w for w in (TINY, QWEN3_B1, QWEN3_B16, WIDE_SKEW_B4, QWEN3_48L_B16)}
+# the other gate+up models of the paper's model table (Table 2), at their
+# (d, K, r); two rotated layers already exceed the last-level cache
+DSV2_LITE_B1 = Workload("deepseek_v2_lite_moe_layer_b1", H=2048, I=1408, E=64, top_k=6, d=8, K=256,
+                        r=384, B=1, seed=3, rotate_layers=2,
+                        description="DeepSeek-V2-Lite-shaped MoE layer, d=8, K=256, r=384, batch 1")
+OLMOE_B1 = Workload("olmoe_1b_7b_moe_layer_b1", H=2048, I=1024, E=64, top_k=8, d=4, K=256, r=256,
+                    B=1, seed=4, rotate_layers=2,
+                    description="OLMoE-1B-7B-shaped MoE layer, d=4, K=256, r=256, batch 1")
+GEMMA4_B1 = Workload("gemma4_26b_a4b_moe_layer_b1", H=2816, I=704, E=128, top_k=8, d=8, K=256,
+                     r=384, B=1, seed=5, rotate_layers=2,
+                     description="Gemma-4-26B-A4B-shaped MoE layer, d=8, K=256, r=384, batch 1")
+OTHER_MODELS_B1 = (DSV2_LITE_B1, OLMOE_B1, GEMMA4_B1)
+
+WORKLOADS = {w.name: w for w in (TINY, QWEN3_B1, QWEN3_B16, WIDE_SKEW_B4, QWEN3_48L_B16,
+                                 *OTHER_MODELS_B1)}

@@ -18,7 +18,7 @@ import torch
 
 import oracle.cardan_oracle as O
 from paper_2609_21137_amd import synth
-from paper_2609_21137_amd.configs import QWEN3_B1, QWEN3_B16, TINY, WIDE_SKEW_B4
+from paper_2609_21137_amd.configs import OTHER_MODELS_B1, QWEN3_B1, QWEN3_B16, TINY, WIDE_SKEW_B4
 
 pytestmark = pytest.mark.gpu
 
@@ -64,6 +64,9 @@ LAYER_CASES = {
     "qwen3_b1": (QWEN3_B1, None),
     "qwen3_b16": (QWEN3_B16, None),
     "wide_skew_b4": (WIDE_SKEW_B4, None),
+    # the other gate+up shapes of the model table (Table 2), batch 1 and 16
+    **{w.name: (w, None) for w in OTHER_MODELS_B1},
+    **{w.name + "_b16": (dataclasses.replace(w, B=16, name=w.name + "_b16"), None) for w in OTHER_MODELS_B1},
 }
 
 
