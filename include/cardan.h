@@ -159,7 +159,7 @@ typedef struct {
 
 /* The layer with compressed gate and up projections (Eq. (1)) and a dense
  * bf16 down projection W_down [E][I][H], the form whose down matrices the
- * paper leaves uncompressed (Sec. 3.2): routing as cardan_route_topk, g and
+ * paper leaves uncompressed (Sec. 3.1): routing as cardan_route_topk, g and
  * u as in cardan_vq_lr_expert_ffn, then y[t] = sum_j topk_w[t][j] *
  * W_down[e_j]^T p_j. The layer's cb_down, codes_down, A_down and B_down are
  * not read (may be NULL). Outputs as cardan_moe_layer. H * I * 2 must stay

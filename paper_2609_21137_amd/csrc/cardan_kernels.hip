@@ -1491,7 +1491,7 @@ __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, i
 }
 
 // ---- dense bf16 expert weights (the uncompressed layer, Sec. 2.1, and the
-// layer that keeps its down projection in bf16, Sec. 3.2) -------------------
+// layer that keeps its down projection in bf16, Sec. 3.1) -------------------
 
 // Dense gate/up tile (a, pj, cg, s): 256 output columns of W_pj[e] [H][I]
 // over split s of the H inputs, partial sums into the same slots as the

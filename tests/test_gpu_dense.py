@@ -3,7 +3,7 @@
 Two layers share the compressed layer's harness (routing, grouping, tiles,
 combine) with dense bf16 expert matrices: the uncompressed MoE layer (the
 baseline of Sec. 2.1) and the layer that keeps gate/up compressed (Eq. (1))
-with a dense bf16 down projection (Sec. 3.2). Bars as for the compressed
+with a dense bf16 down projection (Sec. 3.1). Bars as for the compressed
 layer: top-k identical as ordered lists (oracle margin > 1e-9), affinities
 within 1e-5, max|y - y_ref| <= 2e-2 max|y_ref|, and a 1e-4 headroom bar.
 
