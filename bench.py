@@ -42,6 +42,10 @@ def parse():
     ap.add_argument("--dense", default="qwen3_30b_a3b_moe_layer_b1,qwen3_30b_a3b_moe_layer_b16",
                     help="workloads also timed with dense bf16 expert weights (the uncompressed "
                          "layer and the dense-down layer) on the same routing and inputs")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the benchmark line: time the Qwen3-shaped layer at batch 1 and "
+                         "16 over block lengths d in {4, 8} and ranks r in {0, 128, 256, 384, 512} "
+                         "(the selections-versus-bytes trade-off) and print one JSON line")
     ap.add_argument("--layers", type=int, default=8, help="independently seeded layers rotated")
     ap.add_argument("--inputs", type=int, default=64,
                     help="distinct seeded inputs rotated (a multiple of --layers), so that the "
@@ -378,6 +382,33 @@ def summarize(w, r, src_hash, name=None):
     }
 
 
+def sweep(C, torch, args):
+    """Compressed layer latency over (d, r) at the Qwen3 shape, batches 1 and
+    16, each point over two rotated layers (the touched experts of a rotation
+    exceed the last-level cache)."""
+    import dataclasses
+
+    from paper_2609_21137_amd.configs import QWEN3_B1
+    rows = []
+    cache = {}
+    for d in (8, 4):
+        for r in (0, 128, 256, 384, 512):
+            for B in (1, 16):
+                w = dataclasses.replace(QWEN3_B1, d=d, r=r, B=B, name=f"qwen3_shape_d{d}_r{r}_b{B}")
+                print(f"[sweep] {w.name}", file=sys.stderr, flush=True)
+                rr = time_workload(C, torch, w, args.steps, args.warmup, 2, args.inputs, cache)
+                sm = summarize(w, rr, kernel_source_hash())
+                per_e = compressed_bytes(w, 1)
+                rows.append({"d": d, "r": r, "B": B, "us_per_layer": sm["us_per_layer"],
+                             "GBps": sm["GBps"], "kernel_us": sm["kernel_us"],
+                             "mean_active_experts": sm["mean_active_experts"],
+                             "bytes_per_expert": per_e["per_expert_gateup"] + per_e["per_expert_down"],
+                             "bits_per_weight": round(8.0 * (per_e["per_expert_gateup"] + per_e["per_expert_down"])
+                                                      / (3 * w.H * w.I), 3)})
+    print(json.dumps({"sweep": "qwen3 shape, compressed layer, (d, r) x batch", "steps": args.steps,
+                      "rows": rows, "kernel_source_hash": kernel_source_hash()}))
+
+
 def calibrate_copy(torch, mib):
     """A plain device-to-device copy of `mib` MiB, run 5 times: under
     rocprofv3 --pmc its FETCH_SIZE / WRITE_SIZE per dispatch against the
@@ -453,6 +484,9 @@ def main():
         sys.exit(1)
     if args.calibrate_copy_mb:
         calibrate_copy(torch, args.calibrate_copy_mb)
+        return
+    if args.sweep:
+        sweep(C, torch, args)
         return
     if args.inputs % args.layers:
         print("--inputs must be a multiple of --layers", file=sys.stderr)

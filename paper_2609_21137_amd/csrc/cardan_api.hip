@@ -175,16 +175,28 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
     if (items <= 512.0 || tile >= tile_max) break;
     tile *= 1.05;
   }
-  // Latency shape: if the item count still fits the nominal grid, code
-  // splits of at most kPdVq K-steps and low-rank splits of kPdDense steps
-  // (at most two pipeline fills of a gate/up tile).
+  // Latency shape: while the item count fits the nominal grid (with a
+  // quarter more for a short second round), code splits of at most L K-steps
+  // for the smallest L in {1, 2, 4} x the pipeline depth, with low-rank splits
+  // of kPdDense steps where they fit too, else as many as the byte balance
+  // gave. At large r the byte balance alone leaves one code split of H/32
+  // steps, a chain of H/32/kPdVq dependent pipeline refills (r = 384 at B=1:
+  // 35.7 us).
   if (P.ns > 1) {
-    const int nv = std::max(P.ns_v, ceil_div(KSX, mode == 2 ? kPdDenseW : kPdVq));
-    const int nl = KSZ > 0 ? ceil_div(KSZ, kPdDense) : 0;
-    const double items = exp_act * (2.0 * P.ncg * (nv + nl) + P.ncgh * P.nsd + P.ncgr * P.nsdl);
-    if (items <= 512.0) {
-      P.ns_v = nv;
-      P.ns = nv + nl;
+    const int pd = mode == 2 ? kPdDenseW : kPdVq;
+    const int nl_fine = KSZ > 0 ? ceil_div(KSZ, kPdDense) : 0, nl_keep = P.ns - P.ns_v;
+    bool done = false;
+    for (int mult = 1; mult <= 4 && !done; mult *= 2) {
+      const int nv = std::max(P.ns_v, ceil_div(KSX, pd * mult));
+      for (const int nl : {nl_fine, nl_keep}) {
+        const double items = exp_act * (2.0 * P.ncg * (nv + nl) + P.ncgh * P.nsd + P.ncgr * P.nsdl);
+        if (items <= 1.25 * 512.0) {
+          P.ns_v = nv;
+          P.ns = nv + nl;
+          done = true;
+          break;
+        }
+      }
     }
   }
   // token rows staged per pass: halve (down to 4) before splitting K further

@@ -58,6 +58,8 @@ SMALL = [
     ("passes_b37", 192, 96, 6, 4, 8, 32, 8, 37, 4),      # experts with > 16 tokens
     ("top1", 128, 64, 4, 1, 4, 16, 0, 2, 5),
     ("d4_r24", 256, 160, 12, 2, 4, 16, 24, 9, 6),
+    ("max_batch_64", 256, 128, 16, 4, 8, 64, 8, 64, 7),   # 256 selections
+    ("one_expert_i32", 128, 32, 1, 1, 8, 16, 0, 3, 10),   # E = 1, the smallest I
 ]
 
 

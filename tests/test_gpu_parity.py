@@ -215,6 +215,9 @@ EDGE_SHAPES = [
     # large-batch kernel (down tiles over two column groups) with an odd
     # number of column groups, the last one ragged (704 = 2 x 256 + 192)
     ("wide_tiles_ragged", 704, 768, 128, 8, 8, 256, 128, 32),
+    # corners of the (d, r) sweep at the Qwen3 shape
+    ("qwen3_d4_r512_b16", 2048, 768, 128, 8, 4, 256, 512, 16),
+    ("qwen3_d8_r0_b16", 2048, 768, 128, 8, 8, 256, 0, 16),
 ]
 
 
