@@ -15,7 +15,7 @@
 
 namespace cardan {
 const void* route_kernel();
-const void* expert_kernel(int d, int dnw, int mode);
+const void* expert_kernel(int d, int dnw, int mode, bool csk);
 hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t);
@@ -106,7 +106,7 @@ size_t lds_expert(const Plan& P) {
   // down: p operand rows + a reduction area of 2 float4 per thread
   const int ksd = std::max(ks_max(KSD, P.nsd), ks_max(KSD, P.nsdl));
   need = std::max(need, (size_t)P.nt_max * (ksd * 8 + 1) * 16 + kWG * 2 * 16);
-  need = std::max(need, combine_lds(P));
+  need = std::max(need, combine_lds(P) + ((P.flags & F_CB_SPLITK) ? kSplitKRed : 0));
   return round256(need);
 }
 
@@ -225,7 +225,11 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // workgroup slots (fewer rounds, longer tiles)
   const double items_all = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
   if (mode == 0 && items_all > 2 * 512.0 && P.ncgh > 1 && P.d == 8) P.flags |= F_DN_WIDE;
-  P.n_cb = P.ncgh * ceil_div(B, P.tpc);
+  // Small batches at ranks above 128: B^T u streams more of B than a
+  // combine tile primes before its wait, so the tiles shrink to 64 columns
+  // with the ranks split over their four waves (each wave's share primed).
+  if (mode == 0 && P.r > 128 && B <= 4) P.flags |= F_CB_SPLITK;
+  P.n_cb = P.ncgh * ceil_div(B, P.tpc) * ((P.flags & F_CB_SPLITK) ? 4 : 1);
 
   const int z_units = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nch_z;
   P.n_rc = (flags & F_ROUTE) ? P.nch_r * P.n_eg * ceil_div(B, kRouterTok) : 0;
@@ -402,7 +406,8 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
     }
   }
   if (P.flags & F_EXPERTS) {
-    const int cap = resident_grid(expert_kernel(P.d, dn_width(P), expert_mode(P)), P.lds_expert, &err);
+    const int cap = resident_grid(expert_kernel(P.d, dn_width(P), expert_mode(P), (P.flags & F_CB_SPLITK) != 0),
+                                  P.lds_expert, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_EXPERT);
     err = launch_expert(P, A, cap, P.lds_expert, stream, tm.ev0, tm.ev1);

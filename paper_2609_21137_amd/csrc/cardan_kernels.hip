@@ -1561,17 +1561,25 @@ __device__ void item_down_dense(const Plan& P, const Args& A, const RouteTab& RT
 // wait; B^T u runs on MFMA with u as bf16 hi/lo. The partial sums are
 // gathered in chunks of kCombineChunk loads in flight per thread.
 // LRD: the layer has the low-rank down term (else y is the down sums alone).
-template <bool LRD>
+// SK (large r, small batches): the tile covers 64 columns and its four waves
+// split the ranks of B^T u, so each wave's share of B fits its prime before
+// the wait; the waves' accumulators are summed through LDS.
+template <bool LRD, bool SK>
 __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, int jc, uint8_t* smem) {
-  const int cgy = jc % P.ncgh, tq = jc / P.ncgh;
+  constexpr int NQ4 = SK ? 4 : 1;  // tiles per 256-column group
+  constexpr int CW = 64 / NQ4;     // float4 column quads per token row of a tile
+  const int cgq = jc % (P.ncgh * NQ4), tq = jc / (P.ncgh * NQ4);
+  const int cgy = cgq / NQ4;
   const int H = P.H, r = LRD ? P.r : 0, k = P.k, S = P.S, nsd = P.nsd;
   const int t0 = tq * P.tpc, nt = min(P.tpc, P.B - t0);
   const int tid = threadIdx.x, w = tid >> 6;
-  const int cbase = cgy * kColsPerGroup;
+  const int cbase = cgy * kColsPerGroup + (cgq % NQ4) * 64;
   const int KSR = (r + 31) / 32;
-  // B is primed in full for r <= 128 (later K-steps load during the run)
+  // B is primed in full for r <= 128 (later K-steps load during the run);
+  // SK: wave w primes K-steps [w KSR / 4, (w + 1) KSR / 4) of the tile's columns
+  const int bk0 = SK ? w * KSR / 4 : 0, bk1 = SK ? (w + 1) * KSR / 4 : KSR;
   DensePipe<2, 4> bp;
-  if (r > 0) bp.prime(A.L.B_down, H, cbase + w * 64, H, r, 0, KSR);
+  if (r > 0) bp.prime(A.L.B_down, H, cbase + (SK ? 0 : w * 64), H, r, bk0, bk1);
 
   const int* s_slot = RT.tok_slot + t0 * k;  // (t, j) -> slot of the tile's tokens
   const float* s_w_slot = RT.slot_w;
@@ -1619,7 +1627,7 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
   // cut into chunks of kB taken by separate threads, so a thread has at most
   // kB loads in flight; the chunk sums are added in order afterwards.
   const WsAccess ws(A, P);
-  const int nu = r > 0 ? nt * nq : 0, nd = nt * 64;
+  const int nu = r > 0 ? nt * nq : 0, nd = nt * CW;
   const int cu = (ku + kB - 1) / kB, cd = (kd + kB - 1) / kB;
   const int n_units = nu * cu + nd * cd;
   float4* part = reinterpret_cast<float4*>(smem + combine_part_offset(P));
@@ -1628,8 +1636,8 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
     const int uu = isu ? unit : unit - nu * cu;
     // chunk-major: neighbouring threads read neighbouring quads of one row
     const int it = isu ? uu % nu : uu % nd, c = isu ? uu / nu : uu / nd;
-    const int t = isu ? it / nq : it >> 6, q = isu ? it % nq : 0;
-    const int col = cbase + 4 * (it & 63);
+    const int t = isu ? it / nq : it / CW, q = isu ? it % nq : 0;
+    const int col = cbase + 4 * (it % CW);
     // the column's (or rank quad's) byte offset within a term's row; a
     // padding quad or column reads out of range
     const uint32_t ocol = isu ? (4 * q < r ? (uint32_t)(16 * q) : kOob) : (col < H ? (uint32_t)(4 * col) : kOob);
@@ -1658,13 +1666,37 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
     }
     if (isu)
       put_split_quad(us + (item / nq) * ld, item % nq, acc);
-    else
-      reinterpret_cast<float4*>(dnb)[item - nu] = acc;
+    else  // token row (item - nu) / CW, quad (item - nu) % CW, rows 256 floats apart
+      reinterpret_cast<float4*>(dnb)[(item - nu) / CW * 64 + (item - nu) % CW] = acc;
   }
   trace_mark(3);
   __syncthreads();
   trace_mark(0);
-  if (r > 0) {
+  if (SK && r > 0) {
+    // each wave's partial B^T u over its ranks, summed through LDS; thread
+    // (i, l) writes token row 4 (l >> 4) + i, columns 4 (l & 15) .. + 3
+    f32x4 acc[4];
+    zero_acc(acc);
+    bp.run(us, ld, 0, nt, acc);
+    float* red4 = reinterpret_cast<float*>(smem + combine_lds(P));  // [4 waves][64 lanes][16]
+    const int l = tid & 63;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<float4*>(red4 + (w * 64 + l) * 16 + 4 * q) = make_float4(acc[q][0], acc[q][1], acc[q][2], acc[q][3]);
+    __syncthreads();
+    const int i = w, n = l & 15, t = 4 * (l >> 4) + i;
+    if (t < nt && cbase + 4 * n < H) {
+      float v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float sum = dnb[t * kColsPerGroup + 4 * n + q];
+#pragma unroll
+        for (int ww = 0; ww < 4; ++ww) sum += red4[(ww * 64 + l) * 16 + 4 * q + i];
+        v[q] = sum;
+      }
+      *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + cbase + 4 * n) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  } else if (r > 0) {
     // y = VQ sums + B^T u, written from the accumulators: token rows 4g + i,
     // columns 64 w + 4 n + q
     f32x4 acc[4];
@@ -1683,10 +1715,11 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
       }
     }
   } else {
-    for (int i = tid; i < nt * 64; i += kWG) {
-      const int t = i >> 6, col = cbase + 4 * (i & 63);
+    for (int i = tid; i < nt * CW; i += kWG) {
+      const int t = i / CW, col = cbase + 4 * (i % CW);
       if (col < H)
-        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) = reinterpret_cast<const float4*>(dnb)[i];
+        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) =
+            reinterpret_cast<const float4*>(dnb)[t * 64 + i % CW];
     }
   }
 }
@@ -1809,7 +1842,8 @@ __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
 // every down tile). DNW: column groups per VQ down tile; a separate
 // instantiation keeps the wide tiles' registers out of the narrow one.
 // MODE: expert-weight form (0 compressed, 1 dense down, 2 all dense).
-template <int D, int DNW, int MODE>
+// CSK: combine tiles split over the ranks of B^T u (large r, small batches).
+template <int D, int DNW, int MODE, bool CSK>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   // the code book of the current item (zero-padded to 256 words), in
@@ -1883,7 +1917,7 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   for (; jp < n_items; jp += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
-    item_combine<MODE == 0>(P, A, RT, jp - n_gu - n_dn, item_smem);
+    item_combine<MODE == 0, CSK>(P, A, RT, jp - n_gu - n_dn, item_smem);
     tr.done(A, P, P.n_pre + jp, 7);
   }
 }
@@ -1910,14 +1944,17 @@ __global__ __launch_bounds__(kWG) void k_rmsnorm(int H, const float* __restrict_
 // ---------------------------------------------------------------------------
 const void* route_kernel() { return reinterpret_cast<const void*>(&k_route); }
 
-const void* expert_kernel(int d, int dnw, int mode) {
-  if (mode == 2) return reinterpret_cast<const void*>(&k_expert<8, 1, 2>);
+const void* expert_kernel(int d, int dnw, int mode, bool csk) {
+  if (mode == 2) return reinterpret_cast<const void*>(&k_expert<8, 1, 2, false>);
   if (mode == 1)
-    return d == 8 ? reinterpret_cast<const void*>(&k_expert<8, 1, 1>)
-                  : reinterpret_cast<const void*>(&k_expert<4, 1, 1>);
-  return d == 8 ? (dnw == 2 ? reinterpret_cast<const void*>(&k_expert<8, 2, 0>)
-                            : reinterpret_cast<const void*>(&k_expert<8, 1, 0>))
-                : reinterpret_cast<const void*>(&k_expert<4, 1, 0>);
+    return d == 8 ? reinterpret_cast<const void*>(&k_expert<8, 1, 1, false>)
+                  : reinterpret_cast<const void*>(&k_expert<4, 1, 1, false>);
+  if (csk)
+    return d == 8 ? reinterpret_cast<const void*>(&k_expert<8, 1, 0, true>)
+                  : reinterpret_cast<const void*>(&k_expert<4, 1, 0, true>);
+  return d == 8 ? (dnw == 2 ? reinterpret_cast<const void*>(&k_expert<8, 2, 0, false>)
+                            : reinterpret_cast<const void*>(&k_expert<8, 1, 0, false>))
+                : reinterpret_cast<const void*>(&k_expert<4, 1, 0, false>);
 }
 
 // With a start/stop event pair the launch records them as part of the
@@ -1945,18 +1982,23 @@ hipError_t launch_route_reset(const Plan& P, const Args& A, hipStream_t st) {
 hipError_t launch_expert(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st, hipEvent_t ev0,
                          hipEvent_t ev1) {
   const int mode = expert_mode(P);
+  const bool csk = (P.flags & F_CB_SPLITK) != 0;
   if (mode == 2)
-    CARDAN_LAUNCH((k_expert<8, 1, 2>), grid, lds, st, ev0, ev1, P, A);
+    CARDAN_LAUNCH((k_expert<8, 1, 2, false>), grid, lds, st, ev0, ev1, P, A);
   else if (mode == 1 && P.d == 8)
-    CARDAN_LAUNCH((k_expert<8, 1, 1>), grid, lds, st, ev0, ev1, P, A);
+    CARDAN_LAUNCH((k_expert<8, 1, 1, false>), grid, lds, st, ev0, ev1, P, A);
   else if (mode == 1)
-    CARDAN_LAUNCH((k_expert<4, 1, 1>), grid, lds, st, ev0, ev1, P, A);
+    CARDAN_LAUNCH((k_expert<4, 1, 1, false>), grid, lds, st, ev0, ev1, P, A);
+  else if (csk && P.d == 8)
+    CARDAN_LAUNCH((k_expert<8, 1, 0, true>), grid, lds, st, ev0, ev1, P, A);
+  else if (csk)
+    CARDAN_LAUNCH((k_expert<4, 1, 0, true>), grid, lds, st, ev0, ev1, P, A);
   else if (P.d == 8 && dn_width(P) == 2)
-    CARDAN_LAUNCH((k_expert<8, 2, 0>), grid, lds, st, ev0, ev1, P, A);
+    CARDAN_LAUNCH((k_expert<8, 2, 0, false>), grid, lds, st, ev0, ev1, P, A);
   else if (P.d == 8)
-    CARDAN_LAUNCH((k_expert<8, 1, 0>), grid, lds, st, ev0, ev1, P, A);
+    CARDAN_LAUNCH((k_expert<8, 1, 0, false>), grid, lds, st, ev0, ev1, P, A);
   else
-    CARDAN_LAUNCH((k_expert<4, 1, 0>), grid, lds, st, ev0, ev1, P, A);
+    CARDAN_LAUNCH((k_expert<4, 1, 0, false>), grid, lds, st, ev0, ev1, P, A);
   return hipGetLastError();
 }
 

@@ -46,6 +46,7 @@ constexpr int kPdDense = 2;   // dense K-steps in flight per wave (4 KB each)
 constexpr int kCombineChunk = 16;  // terms per load batch in the combine
 constexpr int kBookCopies = 4;     // code book copies in LDS of the large-batch expert kernel (d = 8)
 constexpr int kLrDownSteps = 4;    // K-steps of a low-rank down tile when the plan would cut finer
+constexpr int kSplitKRed = 4 * 64 * 16 * 4;  // [4 waves][64 lanes][16] float
 constexpr int kPdDenseW = 2;       // K-steps in flight per wave of a dense bf16 expert-weight tile
                                    // (measured faster than 3 at batch 1 and 16)
 
@@ -57,7 +58,8 @@ enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8,
        // the code pointers of the layer: W_down [E][I][H] as codes_down (no
        // low-rank down term), W_gate / W_up [E][H][I] as codes_gate / codes_up
        // (r = 0)
-       F_DN_DENSE = 32, F_GU_DENSE = 64 };
+       F_DN_DENSE = 32, F_GU_DENSE = 64,
+       F_CB_SPLITK = 128 };  // set by the plan: combine tiles of 64 columns, ranks split over the waves
 
 // counters at the start of the workspace, one per 64-byte slot: the status
 // count of timed-out waits
@@ -96,7 +98,8 @@ struct Plan {
 
 // Combine item LDS: reduction area [kWG] float4, VQ down sums [kTokPass][256]
 // float, u operand rows [tpc][ld] uint4, term tables [tpc][k (nsdl + nsd)]
-// uint2, then the per-chunk partial sums (float4).
+// uint2, then the per-chunk partial sums (float4); with F_CB_SPLITK the
+// waves' B^T u accumulators follow (kSplitKRed bytes).
 inline __host__ __device__ size_t combine_part_offset(const Plan& P) {
   const size_t ld = (size_t)(P.r + 31) / 32 * 8 + 1;
   const size_t o = (size_t)kWG * 16 + (size_t)kTokPass * kColsPerGroup * 4 + (size_t)P.tpc * ld * 16 +

@@ -215,6 +215,10 @@ EDGE_SHAPES = [
     # large-batch kernel (down tiles over two column groups) with an odd
     # number of column groups, the last one ragged (704 = 2 x 256 + 192)
     ("wide_tiles_ragged", 704, 768, 128, 8, 8, 256, 128, 32),
+    # combine tiles of 64 columns with the ranks of B^T u split over the
+    # waves (r > 128, B <= 4), ragged H: tiles past H, five rank K-steps
+    ("splitk_combine_ragged", 320, 288, 10, 3, 8, 64, 160, 4),
+    ("splitk_combine_d4_b1", 512, 256, 16, 4, 4, 256, 264, 1),
     # corners of the (d, r) sweep at the Qwen3 shape
     ("qwen3_d4_r512_b16", 2048, 768, 128, 8, 4, 256, 512, 16),
     ("qwen3_d8_r0_b16", 2048, 768, 128, 8, 8, 256, 0, 16),
