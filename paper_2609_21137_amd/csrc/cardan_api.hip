@@ -15,7 +15,7 @@
 
 namespace cardan {
 const void* route_kernel();
-const void* expert_kernel(int d, int dnw, int mode, bool csk);
+const void* expert_kernel(int d, int dnw, int mode, bool csk, bool xpre);
 hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t);
@@ -230,6 +230,9 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // with the ranks split over their four waves (each wave's share primed).
   if (mode == 0 && P.r > 128 && B <= 4) P.flags |= F_CB_SPLITK;
   P.n_cb = P.ncgh * ceil_div(B, P.tpc) * ((P.flags & F_CB_SPLITK) ? 4 : 1);
+  // Batch 1: every gate/up tile's operands are the one token's x and z rows,
+  // so each workgroup stages them once while it builds its routing tables
+  if (mode == 0 && B == 1 && P.H <= 8 * kXpreXGroups) P.flags |= F_XPRE;
 
   const int z_units = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nch_z;
   P.n_rc = (flags & F_ROUTE) ? P.nch_r * P.n_eg * ceil_div(B, kRouterTok) : 0;
@@ -262,7 +265,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.lds_routing = round256((size_t)P.max_act * 16 + (size_t)4 * P.S * 4);
   // item LDS, also the grouping scratch at the start of the kernel
   const size_t group_scratch = round256((size_t)2 * P.S * 4 + (size_t)4 * P.E * 4 + 32);
-  P.lds_expert = P.lds_routing + std::max(lds_expert(P), group_scratch);
+  P.lds_expert = P.lds_routing + std::max(lds_expert(P), group_scratch) + ((P.flags & F_XPRE) ? kXpreBytes : 0);
   // the large-batch kernel holds kBookCopies code books in static LDS: only
   // where two workgroups still fit a CU (80 KB each)
   if ((P.flags & F_DN_WIDE) && P.lds_expert + (size_t)256 * kBookCopies * 16 + 512 > 80 * 1024)
@@ -406,7 +409,8 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
     }
   }
   if (P.flags & F_EXPERTS) {
-    const int cap = resident_grid(expert_kernel(P.d, dn_width(P), expert_mode(P), (P.flags & F_CB_SPLITK) != 0),
+    const int cap = resident_grid(expert_kernel(P.d, dn_width(P), expert_mode(P), (P.flags & F_CB_SPLITK) != 0,
+                                                (P.flags & F_XPRE) != 0),
                                   P.lds_expert, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_EXPERT);

@@ -1208,9 +1208,11 @@ __device__ __forceinline__ void book_store_copies(uint4* cb, uint4 v) {
 // LATE: a tile that runs more code steps than its pipeline holds, code
 // steps first, loads its coefficients during the last of them (fewer bytes
 // requested at once when every tile starts; large batches).
-template <int D, bool LATE, int NC>
+// XP (batch 1): the token's x row and z rows were staged into LDS (xpre,
+// zpre) by the workgroup at kernel start, so the tile stages nothing.
+template <int D, bool LATE, int NC, bool XP>
 __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg, int s,
-                            bool lr_first, uint4* cbs, uint8_t* smem) {
+                            bool lr_first, uint4* cbs, uint8_t* smem, const uint4* xpre, const uint4* zpre) {
   const Routing R = expert_of(P, RT, a);
   const int H = P.H, I = P.I, r = P.r, B = P.B;
   const int KSX = H / 32, KSZ = (r + 31) / 32;
@@ -1266,6 +1268,32 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
   };
   constexpr int kRegStage = 2;  // activation groups per thread loaded ahead of the weights
   const bool lr_late = LATE && !lr_first && x1 - x0 > kPdGateUp;
+  if constexpr (XP) {  // one token, one pass: operands already in LDS
+    const uint4 bk = book_load<D>(pj ? A.L.cb_up : A.L.cb_gate, P.K);
+    __builtin_amdgcn_sched_barrier(0);
+    vq.prime(codes, H / D, I, c0, I, x0, x1);
+    lr.prime(V, I, c0, I, r, z0, z1);
+    __syncthreads();
+    if constexpr (NC > 1)
+      book_store_copies<NC>(cbs, bk);
+    else
+      book_store<D>(cbs, bk);
+    __syncthreads();
+    trace_mark(0);
+    f32x4 acc[4];
+    zero_acc(acc);
+    const uint4* zs1 = zpre + pj * kXpreZRow;
+    if (lr_first) lr.run(zs1, 1, 0, 1, acc);
+    vq.run(cbs, xpre, 1, 0, 1, acc);
+    trace_mark(1);
+    if (!lr_first) lr.run(zs1, 1, 0, 1, acc);
+    // every slot of the expert is token 0 (a caller's routing may repeat an expert)
+    for (int t = 0; t < R.ne; ++t)
+      store_acc(WsAccess(A, P), acc, 1, c0, I, [&](int) { return gu + (((size_t)(R.s0 + t) * 2 + pj) * P.ns + s) * I; });
+    trace_mark(2);
+    publish(wsp<int>(A, P.o_gu_tick) + (a * P.ncg + cg) * kTickPad);
+    return;
+  }
   for (int tg = 0; tg < R.ne; tg += P.nt_max) {
     const int nt = min(P.nt_max, R.ne - tg);
     // Activation loads go out before the weight prime: loads complete in
@@ -1843,7 +1871,9 @@ __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
 // instantiation keeps the wide tiles' registers out of the narrow one.
 // MODE: expert-weight form (0 compressed, 1 dense down, 2 all dense).
 // CSK: combine tiles split over the ranks of B^T u (large r, small batches).
-template <int D, int DNW, int MODE, bool CSK>
+// XPRE (batch 1): the token's x and z rows are loaded at kernel start, while
+// the routing tables build, into an LDS area at the end of dynamic LDS.
+template <int D, int DNW, int MODE, bool CSK, bool XPRE>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   // the code book of the current item (zero-padded to 256 words), in
@@ -1868,11 +1898,49 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     clear_ints(wsp<int>(A, P.o_rc_flag), P.n_rc, kTickPad);
     clear_ints(wsp<int>(A, P.o_zc_flag), P.n_zc, kTickPad);
   }
+  uint4* xpre = reinterpret_cast<uint4*>(smem + P.lds_expert - kXpreBytes);
+  uint4* zpre = xpre + kXpreXGroups;
+  uint4 xv[2];
+  float4 zv[2];
+  if constexpr (XPRE) {  // token 0's x groups and z rank groups (zero past r)
+    const int nx = P.H / 8, nzq = P.r / 8;
+    const float* zsrc = (P.flags & F_Z) ? A.z_out : A.z_in;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int i = tid + u * kWG;
+      xv[u] = i < nx ? reinterpret_cast<const uint4*>(A.x)[i] : make_uint4(0, 0, 0, 0);
+    }
+    const int pj = tid / kXpreZGroups, q = tid % kXpreZGroups;
+    zv[0] = zv[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (pj < 2 && q < nzq) {  // z [2][1][r], written by k_route or given by the caller
+      zv[0] = *reinterpret_cast<const float4*>(zsrc + (size_t)pj * P.r + 8 * q);
+      zv[1] = *reinterpret_cast<const float4*>(zsrc + (size_t)pj * P.r + 8 * q + 4);
+    }
+  }
   // routing tables at the start of dynamic LDS, item LDS after them
   uint8_t* item_smem = smem + P.lds_routing;
   const RouteTab RT = wave_routing
                           ? build_routing_wave(P, (sel_e >= 0 && sel_e < P.E) ? sel_e : -1, sel_w, smem)
                           : build_routing(P, r_idx, r_w, smem, item_smem, (P.flags & F_ROUTE) != 0);
+  if constexpr (XPRE) {  // visible to the items after their first barrier
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      if (tid + u * kWG < kXpreXGroups) xpre[tid + u * kWG] = xv[u];
+    const int pj = tid / kXpreZGroups, q = tid % kXpreZGroups;
+    if (pj < 2) {
+      const float f[8] = {zv[0].x, zv[0].y, zv[0].z, zv[0].w, zv[1].x, zv[1].y, zv[1].z, zv[1].w};
+      uint32_t h[8], lw[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        h[u] = rne_bf16(f[u]);
+        lw[u] = rne_bf16(f[u] - bf(h[u]));
+      }
+      zpre[pj * kXpreZRow + 2 * q] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                                                 h[6] | (h[7] << 16));
+      zpre[pj * kXpreZRow + 2 * q + 1] = make_uint4(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16),
+                                                     lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
+    }
+  }
   tr_route.done(A, P, P.n_pre + P.max_act * (gateup_tiles_per_expert(P) + down_tiles_per_expert(P)) + P.n_cb +
                           blockIdx.x, 8);
   const int nact = RT.nact;
@@ -1894,7 +1962,7 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     if constexpr (MODE == 2)
       item_gateup_dense(P, A, RT, t.a, t.pj, t.cg, t.s, item_smem);
     else
-      item_gateup<D, DNW == 2, NC>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem);
+      item_gateup<D, DNW == 2, NC, XPRE>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem, xpre, zpre);
     tr.done(A, P, P.n_pre + jp, 4);
   }
   for (; jp < n_gu + n_dn; jp += gridDim.x) {
@@ -1944,17 +2012,22 @@ __global__ __launch_bounds__(kWG) void k_rmsnorm(int H, const float* __restrict_
 // ---------------------------------------------------------------------------
 const void* route_kernel() { return reinterpret_cast<const void*>(&k_route); }
 
-const void* expert_kernel(int d, int dnw, int mode, bool csk) {
-  if (mode == 2) return reinterpret_cast<const void*>(&k_expert<8, 1, 2, false>);
-  if (mode == 1)
-    return d == 8 ? reinterpret_cast<const void*>(&k_expert<8, 1, 1, false>)
-                  : reinterpret_cast<const void*>(&k_expert<4, 1, 1, false>);
-  if (csk)
-    return d == 8 ? reinterpret_cast<const void*>(&k_expert<8, 1, 0, true>)
-                  : reinterpret_cast<const void*>(&k_expert<4, 1, 0, true>);
-  return d == 8 ? (dnw == 2 ? reinterpret_cast<const void*>(&k_expert<8, 2, 0, false>)
-                            : reinterpret_cast<const void*>(&k_expert<8, 1, 0, false>))
-                : reinterpret_cast<const void*>(&k_expert<4, 1, 0, false>);
+template <int D, int DNW, int MODE, bool CSK, bool XPRE>
+const void* kx() {
+  return reinterpret_cast<const void*>(&k_expert<D, DNW, MODE, CSK, XPRE>);
+}
+
+template <int D>
+const void* kx_compressed(bool csk, bool xpre) {
+  return csk ? (xpre ? kx<D, 1, 0, true, true>() : kx<D, 1, 0, true, false>())
+             : (xpre ? kx<D, 1, 0, false, true>() : kx<D, 1, 0, false, false>());
+}
+
+const void* expert_kernel(int d, int dnw, int mode, bool csk, bool xpre) {
+  if (mode == 2) return kx<8, 1, 2, false, false>();
+  if (mode == 1) return d == 8 ? kx<8, 1, 1, false, false>() : kx<4, 1, 1, false, false>();
+  if (d == 8 && dnw == 2) return kx<8, 2, 0, false, false>();
+  return d == 8 ? kx_compressed<8>(csk, xpre) : kx_compressed<4>(csk, xpre);
 }
 
 // With a start/stop event pair the launch records them as part of the
@@ -1981,25 +2054,14 @@ hipError_t launch_route_reset(const Plan& P, const Args& A, hipStream_t st) {
 
 hipError_t launch_expert(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st, hipEvent_t ev0,
                          hipEvent_t ev1) {
-  const int mode = expert_mode(P);
-  const bool csk = (P.flags & F_CB_SPLITK) != 0;
-  if (mode == 2)
-    CARDAN_LAUNCH((k_expert<8, 1, 2, false>), grid, lds, st, ev0, ev1, P, A);
-  else if (mode == 1 && P.d == 8)
-    CARDAN_LAUNCH((k_expert<8, 1, 1, false>), grid, lds, st, ev0, ev1, P, A);
-  else if (mode == 1)
-    CARDAN_LAUNCH((k_expert<4, 1, 1, false>), grid, lds, st, ev0, ev1, P, A);
-  else if (csk && P.d == 8)
-    CARDAN_LAUNCH((k_expert<8, 1, 0, true>), grid, lds, st, ev0, ev1, P, A);
-  else if (csk)
-    CARDAN_LAUNCH((k_expert<4, 1, 0, true>), grid, lds, st, ev0, ev1, P, A);
-  else if (P.d == 8 && dn_width(P) == 2)
-    CARDAN_LAUNCH((k_expert<8, 2, 0, false>), grid, lds, st, ev0, ev1, P, A);
-  else if (P.d == 8)
-    CARDAN_LAUNCH((k_expert<8, 1, 0, false>), grid, lds, st, ev0, ev1, P, A);
-  else
-    CARDAN_LAUNCH((k_expert<4, 1, 0, false>), grid, lds, st, ev0, ev1, P, A);
-  return hipGetLastError();
+  // the instantiation expert_kernel() names, launched with its own arguments
+  const void* fn = expert_kernel(P.d, dn_width(P), expert_mode(P), (P.flags & F_CB_SPLITK) != 0,
+                                 (P.flags & F_XPRE) != 0);
+  Plan p = P;
+  Args a = A;
+  void* args[] = {&p, &a};
+  if (ev0) return hipExtLaunchKernel(fn, dim3(grid), dim3(kWG), args, lds, st, ev0, ev1, 0);
+  return hipLaunchKernel(fn, dim3(grid), dim3(kWG), args, lds, st);
 }
 
 hipError_t launch_rmsnorm(hipStream_t st, int B, int H, const float* y, float eps, uint16_t* xn, hipEvent_t ev0,

@@ -47,6 +47,11 @@ constexpr int kCombineChunk = 16;  // terms per load batch in the combine
 constexpr int kBookCopies = 4;     // code book copies in LDS of the large-batch expert kernel (d = 8)
 constexpr int kLrDownSteps = 4;    // K-steps of a low-rank down tile when the plan would cut finer
 constexpr int kSplitKRed = 4 * 64 * 16 * 4;  // [4 waves][64 lanes][16] float
+// batch-1 operand area at the end of k_expert's dynamic LDS: x (H <= 4096,
+// groups of 8 bf16) and z of both projections as bf16 hi/lo pairs per group
+// of 8 ranks (r <= 512, zero past r)
+constexpr int kXpreXGroups = 512, kXpreZGroups = 64, kXpreZRow = 2 * kXpreZGroups;
+constexpr int kXpreBytes = (kXpreXGroups + 2 * kXpreZRow) * 16;
 constexpr int kPdDenseW = 2;       // K-steps in flight per wave of a dense bf16 expert-weight tile
                                    // (measured faster than 3 at batch 1 and 16)
 
@@ -59,7 +64,8 @@ enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8,
        // low-rank down term), W_gate / W_up [E][H][I] as codes_gate / codes_up
        // (r = 0)
        F_DN_DENSE = 32, F_GU_DENSE = 64,
-       F_CB_SPLITK = 128 };  // set by the plan: combine tiles of 64 columns, ranks split over the waves
+       F_CB_SPLITK = 128,  // set by the plan: combine tiles of 64 columns, ranks split over the waves
+       F_XPRE = 256 };     // set by the plan (batch 1): x and z staged once per workgroup
 
 // counters at the start of the workspace, one per 64-byte slot: the status
 // count of timed-out waits
