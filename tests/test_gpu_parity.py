@@ -287,9 +287,10 @@ def test_workspace_reused_across_batch_sizes(C):
         assert np.array_equal(y.cpu().numpy().astype(np.float64), y_f)
 
 
-def test_rmsnorm(C):
-    rng = np.random.default_rng(0)
-    y = rng.standard_normal((16, 2048)).astype(np.float32) * 0.3
+@pytest.mark.parametrize("H", [2048, 2052, 4096, 1001, 8192])  # row in registers; strided loop
+def test_rmsnorm(C, H):
+    rng = np.random.default_rng(H)
+    y = rng.standard_normal((16, H)).astype(np.float32) * 0.3
     xn = C.rmsnorm_bf16(torch.from_numpy(y).cuda(), 1e-6)
     torch.cuda.synchronize()
     got = O.bf16_to_f64(C.bf16_bits(xn))
