@@ -44,7 +44,7 @@ def parse():
                          "layer and the dense-down layer) on the same routing and inputs")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the benchmark line: time the Qwen3-shaped layer at batch 1 and "
-                         "16 over block lengths d in {4, 8} and ranks r in {0, 128, 256, 384, 512} "
+                         "16 over block lengths d in {2, 4, 8} and ranks r in {0, 128, 256, 384, 512} "
                          "(the selections-versus-bytes trade-off) and print one JSON line")
     ap.add_argument("--layers", type=int, default=8, help="independently seeded layers rotated")
     ap.add_argument("--inputs", type=int, default=64,
@@ -391,7 +391,7 @@ def sweep(C, torch, args):
     from paper_2609_21137_amd.configs import QWEN3_B1
     rows = []
     cache = {}
-    for d in (8, 4):
+    for d in (8, 4, 2):
         for r in (0, 128, 256, 384, 512):
             for B in (1, 16):
                 w = dataclasses.replace(QWEN3_B1, d=d, r=r, B=B, name=f"qwen3_shape_d{d}_r{r}_b{B}")

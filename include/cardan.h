@@ -32,7 +32,7 @@
  *     cardan_workspace_bytes() bytes. It must be zero-filled once before its
  *     first use; every completed call leaves it ready for the next. Calls
  *     that overlap in time must not share a workspace.
- *   - Supported shapes: d in {4, 8}; 1 <= K <= 256; H % 64 == 0;
+ *   - Supported shapes: d in {2, 4, 8}; 1 <= K <= 256; H % 64 == 0;
  *     I % 32 == 0; 1 <= E <= 1024; 1 <= top_k <= min(E, 32); 0 <= r <= 512;
  *     1 <= B <= 64. Other shapes return CARDAN_ERR_UNSUPPORTED or
  *     CARDAN_ERR_BAD_SHAPE.
@@ -64,7 +64,7 @@ enum {
   CARDAN_OK = 0,
   CARDAN_ERR_NULL_PTR = -1,   /* a required pointer is NULL               */
   CARDAN_ERR_BAD_SHAPE = -2,  /* shape or batch outside the valid domain  */
-  CARDAN_ERR_UNSUPPORTED = -3,/* valid but not compiled (e.g. d == 2)     */
+  CARDAN_ERR_UNSUPPORTED = -3,/* valid but not compiled (e.g. d == 16)    */
   CARDAN_ERR_WORKSPACE = -4,  /* ws_bytes below cardan_workspace_bytes()  */
   CARDAN_ERR_HIP = -5,        /* a HIP launch or event call failed        */
   CARDAN_ERR_ALIGN = -6       /* a pointer is not 16-byte aligned         */

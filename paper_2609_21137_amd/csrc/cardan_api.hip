@@ -58,7 +58,7 @@ int check_shape(const cardan_shape* s, int32_t B) {
     return fail(CARDAN_ERR_BAD_SHAPE, "H=%d and I=%d must be multiples of d=%d", s->H, s->I, s->d);
   if (B < 1 || B > kMaxB) return fail(CARDAN_ERR_BAD_SHAPE, "B=%d outside [1, %d]", B, kMaxB);
   if (s->K > 256) return fail(CARDAN_ERR_BAD_SHAPE, "K=%d exceeds 256 (uint8 codes)", s->K);
-  if (s->d != 4 && s->d != 8) return fail(CARDAN_ERR_UNSUPPORTED, "d=%d not compiled (4, 8)", s->d);
+  if (s->d != 2 && s->d != 4 && s->d != 8) return fail(CARDAN_ERR_UNSUPPORTED, "d=%d not compiled (2, 4, 8)", s->d);
   if (s->H % 64) return fail(CARDAN_ERR_UNSUPPORTED, "H=%d must be a multiple of 64", s->H);
   if (s->I % 32) return fail(CARDAN_ERR_UNSUPPORTED, "I=%d must be a multiple of 32", s->I);
   if (s->E > kMaxE) return fail(CARDAN_ERR_UNSUPPORTED, "E=%d exceeds %d", s->E, kMaxE);

@@ -755,7 +755,7 @@ struct WsAccess {
 // lanes of one LDS pass collide less on the random code-word rows.
 template <int D, int NOPS, int PD, int NC = 1>
 struct VqPipe {
-  static constexpr int W = D == 8 ? 1 : 2;
+  static constexpr int W = 8 / D;  // code rows per lane and K-step (d = 8, 4, 2)
   uint32_t buf[PD][W];
   rsrc_t rs;
   uint32_t lane_off, step_bytes, row_len;
@@ -764,8 +764,8 @@ struct VqPipe {
   // steps i >= nks read zeros without touching memory
   __device__ __forceinline__ void load(int i, uint32_t (&b)[W]) {
     const uint32_t o = i < nks ? lane_off + (uint32_t)(ks0 + i) * step_bytes : kOob;
-    b[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, o, 0, 0);
-    if constexpr (D == 4) b[1] = __builtin_amdgcn_raw_buffer_load_b32(rs, o + row_len, 0, 0);
+#pragma unroll
+    for (int v = 0; v < W; ++v) b[v] = __builtin_amdgcn_raw_buffer_load_b32(rs, o + v * row_len, 0, 0);
   }
   // codes [n_rows][rl] of one expert; columns [c0, c0 + 64) of n_out (lanes
   // past n_out read the last valid columns, whose results are never stored);
@@ -797,10 +797,14 @@ struct VqPipe {
     for (int q = 0; q < 4; ++q) {
       if constexpr (D == 8) {
         w[q] = cb_s[((b[0] >> (8 * q)) & 255u) * NC + (l & (NC - 1))];
-      } else {
+      } else if constexpr (D == 4) {
         const uint2 lo = cb2[(b[0] >> (8 * q)) & 255u];
         const uint2 hi = cb2[(b[1] >> (8 * q)) & 255u];
         w[q] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      } else {  // d = 2: four 4-byte code words
+        const uint32_t* cb1 = reinterpret_cast<const uint32_t*>(cb_s);
+        w[q] = make_uint4(cb1[(b[0] >> (8 * q)) & 255u], cb1[(b[1] >> (8 * q)) & 255u],
+                          cb1[(b[2] >> (8 * q)) & 255u], cb1[(b[3] >> (8 * q)) & 255u]);
       }
     }
 #pragma unroll
@@ -808,7 +812,7 @@ struct VqPipe {
       acc[q] = mfma_bf16(a0, w[q], acc[q]);
       if (NOPS == 2) acc[q] = mfma_bf16(a1, w[q], acc[q]);
     }
-    sched_step<NOPS + (D == 8 ? 4 : 8), 4 * NOPS>();
+    sched_step<NOPS + 4 * W, 4 * NOPS>();
   }
   __device__ __forceinline__ void run(const uint4* cb_s, const uint4* ops, int ops_ld, int ops_ks0,
                                       int nt, f32x4 acc[4]) {
@@ -1449,7 +1453,8 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
   const int c0 = cgx * kColsPerGroup + (threadIdx.x >> 6) * 64;
   const uint8_t* codes = A.L.codes_down + (size_t)R.e * (I / D) * H;
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
-  VqPipe<D, 2, kPdVq> pipe;
+  // d = 2 holds four code rows per K-step: half the steps in flight (same registers as d = 4)
+  VqPipe<D, 2, D == 2 ? kPdVq / 2 : kPdVq> pipe;
   uint4 bk;
   down_body(P, A, R, a, ks0, ks1, c0, H,
             [&]() {
@@ -2053,9 +2058,10 @@ const void* kx_compressed(bool csk, bool xpre) {
 
 const void* expert_kernel(int d, int dnw, int mode, bool csk, bool xpre) {
   if (mode == 2) return kx<8, 1, 2, false, false>();
-  if (mode == 1) return d == 8 ? kx<8, 1, 1, false, false>() : kx<4, 1, 1, false, false>();
+  if (mode == 1)
+    return d == 8 ? kx<8, 1, 1, false, false>() : d == 4 ? kx<4, 1, 1, false, false>() : kx<2, 1, 1, false, false>();
   if (d == 8 && dnw == 2) return kx<8, 2, 0, false, false>();
-  return d == 8 ? kx_compressed<8>(csk, xpre) : kx_compressed<4>(csk, xpre);
+  return d == 8 ? kx_compressed<8>(csk, xpre) : d == 4 ? kx_compressed<4>(csk, xpre) : kx_compressed<2>(csk, xpre);
 }
 
 // With a start/stop event pair the launch records them as part of the

@@ -73,7 +73,7 @@ BAD_SHAPES = [
     ((2048, 768, 8, 9, 8, 256, 128), 1, -2),      # top_k > E
     ((2048, 770, 128, 8, 8, 256, 128), 1, -2),    # I % d
     ((2048, 768, 128, 8, 8, 300, 128), 1, -2),    # K > 256
-    ((2048, 768, 128, 8, 2, 256, 128), 1, -3),    # d = 2 not compiled
+    ((2048, 768, 128, 8, 16, 256, 128), 1, -3),   # d = 16 not compiled
     ((2016, 768, 128, 8, 8, 256, 128), 1, -3),    # H % 64
     ((2048, 784, 128, 8, 8, 256, 128), 1, -3),    # I % 32
     ((2048, 768, 128, 8, 8, 256, 12), 1, -3),     # r % 8

@@ -60,6 +60,7 @@ SMALL = [
     ("d4_r24", 256, 160, 12, 2, 4, 16, 24, 9, 6),
     ("max_batch_64", 256, 128, 16, 4, 8, 64, 8, 64, 7),   # 256 selections
     ("one_expert_i32", 128, 32, 1, 1, 8, 16, 0, 3, 10),   # E = 1, the smallest I
+    ("d2_r16", 256, 160, 12, 2, 2, 16, 16, 5, 11),        # d = 2 gate/up codes
 ]
 
 

@@ -219,6 +219,12 @@ EDGE_SHAPES = [
     # waves (r > 128, B <= 4), ragged H: tiles past H, five rank K-steps
     ("splitk_combine_ragged", 320, 288, 10, 3, 8, 64, 160, 4),
     ("splitk_combine_d4_b1", 512, 256, 16, 4, 4, 256, 264, 1),
+    # d = 2 (four 4-byte code words per MFMA operand), including the
+    # paper's VQ-only comparison point (d, r) = (2, 0) at the Qwen3 shape
+    ("d2_small", 256, 160, 8, 2, 2, 16, 8, 3),
+    ("qwen3_d2_r0_b1", 2048, 768, 128, 8, 2, 256, 0, 1),
+    ("qwen3_d2_r0_b16", 2048, 768, 128, 8, 2, 256, 0, 16),
+    ("d2_r160_b2", 512, 288, 16, 4, 2, 64, 160, 2),
     # corners of the (d, r) sweep at the Qwen3 shape
     ("qwen3_d4_r512_b16", 2048, 768, 128, 8, 4, 256, 512, 16),
     ("qwen3_d8_r0_b16", 2048, 768, 128, 8, 8, 256, 0, 16),
