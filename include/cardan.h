@@ -42,6 +42,20 @@
  *     internal waits that gave up after their bound (seconds); nonzero means
  *     the results of the calls since it was last zero are invalid. The
  *     library never clears it; the caller may.
+ *   - The layer kernels are persistent: each launches at most as many
+ *     workgroups as the device holds at once and their work items wait on
+ *     one another. They need the device's compute units to themselves while
+ *     they run; other resident work (another stream or process) can keep
+ *     workgroups from starting, and the waits that depend on them then give
+ *     up into the status count above (the results are invalid, nothing hangs).
+ *   - A workspace serves one (H, I, E): its counter offsets depend on those
+ *     three only, so calls of any batch, rank, block length or expert-weight
+ *     form on that shape may share it in turn; zero it again before using it
+ *     for another (H, I, E).
+ *   - Reentrancy: the entry points keep no mutable host state apart from the
+ *     thread-local error text and an occupancy cache guarded by a mutex; host
+ *     threads may call them concurrently on separate workspaces. The
+ *     profiling hooks below are the exception (host-global, not thread-safe).
  */
 #ifndef CARDAN_H
 #define CARDAN_H
@@ -141,9 +155,12 @@ int cardan_vq_lr_expert_ffn(const cardan_shape* shape, int32_t B, const cardan_b
                             const cardan_layer* layer, float* y,
                             void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* The whole layer: route + top-k + gating, shared projections, grouped
- * expert computation and combine. Writes y [B][H] float32 and the routing
- * topk_idx [B][top_k] int32, topk_w [B][top_k] float32. */
+/* The whole layer (paper Sec. 2.1 with the experts of Sec. 3.1, Eq. (1), and
+ * the once-per-token shared projections and cross-expert batching of
+ * Sec. 4.2): route + top-k + gating as cardan_route_topk, z = U^T x as
+ * cardan_shared_proj, then the grouped expert computation and weighted
+ * combine of cardan_vq_lr_expert_ffn. Writes y [B][H] float32 and the
+ * routing topk_idx [B][top_k] int32, topk_w [B][top_k] float32. */
 int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
                      const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
                      void* ws, size_t ws_bytes, hipStream_t stream);

@@ -272,40 +272,6 @@ def moe_layer_factored(x, layer: dict, k: int, d: int):
     return expert_ffn_factored(x, idx, a, layer, d), idx, a, margin
 
 
-def expert_outputs_sampled(x, idx, a, layer: dict, d: int, cols) -> np.ndarray:
-    """Output columns ``cols`` of ``expert_ffn_factored`` for every token.
-
-    The down projection is evaluated only for the requested output columns,
-    which lets full-size parity checks compare a sample of outputs.
-    """
-    xf = _f(x)
-    idx = np.asarray(idx)
-    a = np.asarray(a, dtype=np.float64)
-    cols = np.asarray(cols)
-    B = xf.shape[0]
-    has_lr = layer.get("U_gate") is not None and _f(layer["U_gate"]).shape[1] > 0
-    if has_lr:
-        zg = shared_proj(xf, layer["U_gate"])
-        zu = shared_proj(xf, layer["U_up"])
-        Bd = _f(layer["B_down"])[:, cols]
-    out = np.zeros((B, len(cols)))
-    for t in range(B):
-        for j in range(idx.shape[1]):
-            e = int(idx[t, j])
-            g = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d).T @ xf[t]
-            u = decode_vq(layer["codes_up"][e], layer["cb_up"], d).T @ xf[t]
-            if has_lr:
-                g = g + _f(layer["V_gate"][e]).T @ zg[t]
-                u = u + _f(layer["V_up"][e]).T @ zu[t]
-            p = silu(g) * u
-            Qd = decode_vq(layer["codes_down"][e][:, cols], layer["cb_down"], d)
-            ye = Qd.T @ p
-            if has_lr:
-                ye = ye + Bd.T @ (_f(layer["A_down"][e]).T @ p)
-            out[t] += a[t, j] * ye
-    return out
-
-
 # --------------------------------------------------------------------------
 # dense-weight baselines
 # --------------------------------------------------------------------------

@@ -20,7 +20,8 @@ import numpy as np
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libcardan.so")
+# CARDAN_LIB names another build of the library (the tests' sanitizer build)
+LIB_PATH = os.environ.get("CARDAN_LIB") or os.path.join(HERE, "libcardan.so")
 
 LAYER_FIELDS = (
     "router_w", "router_bias", "cb_gate", "cb_up", "cb_down",

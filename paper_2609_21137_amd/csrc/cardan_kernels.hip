@@ -1757,41 +1757,6 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
   }
 }
 
-// Gate/up tile of position p. The tiles of splits s < s_vq read codes (LDS
-// code-book lookups bound the CU), the others only coefficients (HBM bound).
-// Workgroups b and b + G/2 share a CU when two are resident per CU, so code
-// tiles take the first half of every grid-sized round of positions and
-// coefficient tiles the second, each class in its natural (expert, gate|up,
-// column group, split) order; once one class runs out the other fills every
-// position. Gate/up tiles wait for nothing, so any order is deadlock-free.
-struct GateUpTile {
-  int a, pj, cg, s;
-};
-__device__ __forceinline__ GateUpTile gateup_at(const Plan& P, int p, int nact, int s_vq, int G) {
-  const int half = G >> 1;
-  const int n_v = nact * 2 * P.ncg * s_vq, n_l = nact * 2 * P.ncg * (P.ns - s_vq);
-  const int r = p / G, w = p - r * G;
-  const int v = r * half + min(w, half);  // code-preferring positions before p
-  const int l = p - v;                     // coefficient-preferring positions before p
-  // tiles of each class handed out before p (at most one class runs out)
-  int cv = v, cl = l;
-  if (v > n_v) {
-    cv = n_v;
-    cl = p - n_v;
-  } else if (l > n_l) {
-    cl = n_l;
-    cv = p - n_l;
-  }
-  const bool code = w < half ? cv < n_v : !(cl < n_l);
-  int i = code ? cv : cl;
-  const int nsc = code ? s_vq : P.ns - s_vq;
-  const int s = i % nsc + (code ? 0 : s_vq);
-  i /= nsc;
-  const int cg = i % P.ncg;
-  i /= P.ncg;
-  return {i >> 1, i & 1, cg, s};
-}
-
 // ===========================================================================
 // the two persistent kernels of a layer call
 // ===========================================================================

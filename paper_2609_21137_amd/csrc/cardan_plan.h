@@ -145,6 +145,50 @@ __host__ __device__ inline void joint_split(int s, int ns, int ns_v, int KSX, in
   }
 }
 
+// Gate/up tile of position p. The tiles of splits s < s_vq read codes (LDS
+// code-book lookups bound the CU), the others only coefficients (HBM bound).
+// Workgroups b and b + G/2 share a CU when two are resident per CU, so code
+// tiles take the first half of every grid-sized round of positions and
+// coefficient tiles the second, each class in its natural (expert, gate|up,
+// column group, split) order; once one class runs out the other fills every
+// position. Gate/up tiles wait for nothing, so any order is deadlock-free.
+struct GateUpTile {
+  int a, pj, cg, s;
+};
+__host__ __device__ inline GateUpTile gateup_at(const Plan& P, int p, int nact, int s_vq, int G) {
+  const int half = G >> 1;
+  const int n_v = nact * 2 * P.ncg * s_vq, n_l = nact * 2 * P.ncg * (P.ns - s_vq);
+  const int r = p / G, w = p - r * G;
+  const int v = r * half + (w < half ? w : half);  // code-preferring positions before p
+  const int l = p - v;                             // coefficient-preferring positions before p
+  // tiles of each class handed out before p (at most one class runs out)
+  int cv = v, cl = l;
+  if (v > n_v) {
+    cv = n_v;
+    cl = p - n_v;
+  } else if (l > n_l) {
+    cl = n_l;
+    cv = p - n_l;
+  }
+  const bool code = w < half ? cv < n_v : !(cl < n_l);
+  int i = code ? cv : cl;
+  const int nsc = code ? s_vq : P.ns - s_vq;
+  const int s = i % nsc + (code ? 0 : s_vq);
+  i /= nsc;
+  const int cg = i % P.ncg;
+  i /= P.ncg;
+  return {i >> 1, i & 1, cg, s};
+}
+
+// Dynamic LDS limit of either kernel; a plan needing more is rejected.
+constexpr size_t kLdsMax = 96 * 1024;
+
+// Launch plan, item counts and workspace layout of one call (host only,
+// cardan_planner.cpp); depends only on (shape, B, z_sep, flags). Flags with
+// F_GU_DENSE plan r = 0. The shape must have passed the entry points' shape
+// validation.
+Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags);
+
 // Device pointers of one call.
 struct Args {
   cardan_layer L;

@@ -276,6 +276,13 @@ def pin_silu_and_rmsnorm():
     assert abs(O.silu(np.array([-2.0]))[0] + 2.0 / (1.0 + math.exp(2.0))) < 1e-16
     r = O.rmsnorm(np.array([[3.0, 4.0]]), eps=0.0)
     assert np.allclose(r, [[3.0 / math.sqrt(12.5), 4.0 / math.sqrt(12.5)]], rtol=0, atol=1e-15)
+    # eps as large as mean(y^2) = 12.5: the root of 12.5 + 12.5 is 5, so the row
+    # becomes the unit vector [0.6, 0.8]; eps outside the root would give
+    # [3, 4] / (sqrt(12.5) + 12.5) instead
+    r = O.rmsnorm(np.array([[3.0, 4.0], [-6.0, 8.0]]), eps=12.5)
+    assert np.allclose(r[0], [0.6, 0.8], rtol=0, atol=1e-15)
+    # second row: mean 50, root of 62.5
+    assert np.allclose(r[1], np.array([-6.0, 8.0]) / math.sqrt(62.5), rtol=0, atol=1e-15)
 
 
 def pin_bf16_widening():
@@ -441,6 +448,11 @@ def _mut_dense_no_silu(x, idx, a, W_gate, W_up, W_down):
     return y
 
 
+def _mut_rmsnorm_eps_outside(y, eps=1e-6):
+    y = np.asarray(y, dtype=np.float64)
+    return y / (np.sqrt(np.mean(y * y, axis=1, keepdims=True)) + eps)
+
+
 def _mut_dense_down_transposed(x, layer, W_down, k, d):
     Wt = np.ascontiguousarray(np.swapaxes(np.asarray(W_down), 1, 2))
     return _ORIG["moe_layer_dense_down"](x, layer, Wt, k, d)
@@ -464,6 +476,7 @@ MUTATIONS = {
     "shared_basis_not_amortised": ("storage_bits_per_weight", _mut_storage_no_basis),
     "dense_baseline_silu_dropped": ("expert_ffn_dense", _mut_dense_no_silu),
     "dense_down_transposed": ("moe_layer_dense_down", _mut_dense_down_transposed),
+    "rmsnorm_eps_outside_sqrt": ("rmsnorm", _mut_rmsnorm_eps_outside),
 }
 
 
