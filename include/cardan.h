@@ -165,6 +165,29 @@ int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
                      const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
                      void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Size of the library's own scratch array, one per GPU (16 MiB). */
+#define CARDAN_SCRATCH_BYTES (16u << 20)
+
+/* cardan_moe_layer without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc. The kernels use a fixed device-resident
+ * scratch array of CARDAN_SCRATCH_BYTES inside the library (each GPU the
+ * library runs on holds its own copy until the process ends); this call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine).
+ * Arguments, outputs, results and errors are those of cardan_moe_layer; a
+ * layer whose workspace at this batch exceeds the array returns
+ * CARDAN_ERR_WORKSPACE before anything is enqueued.
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents: calls that overlap in time on one GPU (several streams or host
+ * threads) race and give undefined results, so serialise them. A call whose
+ * (H, I, E) differs from the previous call's on the GPU, the first call, and
+ * any call recorded under graph capture enqueue a small zero-fill kernel of
+ * the array's counters before the layer. The wait-timeout status count of
+ * these calls is not readable (cardan_moe_layer with a workspace reports it). */
+int cardan_moe_layer_noalloc(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                             const cardan_layer* layer, float* y, int32_t* topk_idx,
+                             float* topk_w, hipStream_t stream);
+
 /* Dense bf16 expert weights of an uncompressed layer (device pointers). */
 typedef struct {
   const cardan_bf16* router_w;    /* [H][E]                                  */

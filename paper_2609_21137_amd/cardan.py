@@ -72,6 +72,7 @@ def _load():
         "cardan_shared_proj": ([sp, i32, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_vq_lr_expert_ffn": ([sp, i32, vp, vp, vp, vp, lp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_moe_layer": ([sp, i32, vp, lp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cardan_moe_layer_noalloc": ([sp, i32, vp, lp, vp, vp, vp, vp], ctypes.c_int),
         "cardan_moe_layer_dense_down": ([sp, i32, vp, lp, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_dense_moe_layer": ([sp, i32, vp, dp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_rmsnorm_bf16": ([i32, i32, vp, ctypes.c_float, vp, vp], ctypes.c_int),
@@ -89,7 +90,7 @@ _lib = _load()
 
 EXPORTED = (
     "cardan_abi_version", "cardan_last_error", "cardan_workspace_bytes", "cardan_route_topk",
-    "cardan_shared_proj", "cardan_vq_lr_expert_ffn", "cardan_moe_layer",
+    "cardan_shared_proj", "cardan_vq_lr_expert_ffn", "cardan_moe_layer", "cardan_moe_layer_noalloc",
     "cardan_moe_layer_dense_down", "cardan_dense_moe_layer", "cardan_rmsnorm_bf16",
     "cardan_profile_begin", "cardan_profile_end",
 )
@@ -277,6 +278,21 @@ def moe_layer(shape: Shape, x, layer: DeviceLayer, ws=None, out=None, idx=None, 
         _ptr(idx, torch.int32, "topk_idx", (B, shape.top_k)),
         _ptr(w, torch.float32, "topk_w", (B, shape.top_k)),
         _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(dev)))
+    return y, idx, w
+
+
+def moe_layer_noalloc(shape: Shape, x, layer: DeviceLayer, out=None, idx=None, w=None):
+    """The whole layer on the library's own scratch array (no workspace, no
+    device allocation inside the call). Returns ``(y, topk_idx, topk_w)``."""
+    B = x.shape[0]
+    dev = x.device
+    y, idx, w = _outputs(shape, x, out, idx, w)
+    st = layer.struct()
+    _check(_lib.cardan_moe_layer_noalloc(
+        ctypes.byref(shape), B, _ptr(x, torch.bfloat16, "x", (B, shape.H)), ctypes.byref(st),
+        _ptr(y, torch.float32, "y", (B, shape.H)),
+        _ptr(idx, torch.int32, "topk_idx", (B, shape.top_k)),
+        _ptr(w, torch.float32, "topk_w", (B, shape.top_k)), _stream(dev)))
     return y, idx, w
 
 

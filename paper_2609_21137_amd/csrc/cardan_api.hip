@@ -20,6 +20,7 @@ const void* expert_kernel(int d, int dnw, int mode, bool csk, bool xpre);
 hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t);
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t);
 hipError_t launch_rmsnorm(hipStream_t, int, int, const float*, float, uint16_t*, hipEvent_t, hipEvent_t);
 }  // namespace cardan
 
@@ -219,6 +220,60 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
   return CARDAN_OK;
 }
 
+// ---- the library's own scratch array (no-allocation entry point) ----------
+// A fixed device-resident workspace for callers that cannot allocate. Each
+// GPU holds its own copy, zero-filled when the code object loads, until the
+// process ends. Host code never uses the array's name as an address: its
+// device address is looked up once per device (hipGetSymbolAddress, with
+// that device current) and kept in g_scratch.
+constexpr size_t kScratchBytes = (size_t)CARDAN_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+struct ScratchState {
+  void* ptr = nullptr;  // device address of `scratch` on this device
+  int H = 0, I = 0, E = 0;  // shape of the last call enqueued outside graph capture
+};
+std::mutex g_scratch_mu;
+ScratchState g_scratch[kMaxDevices];
+
+// Device address of the scratch array on the current device, and whether
+// its counters must be cleared before a call of shape (H, I, E): counter
+// offsets depend on (H, I, E), and a call leaves its expert ticks set for the
+// next call of the same shape to clear. They are cleared when the shape
+// differs from the last call's, on the first call, and for every call
+// recorded under graph capture (a replay may follow calls of any shape; the
+// next eager call then clears again).
+int scratch_for_call(const Plan& P, hipStream_t stream, void** ptr, bool* clear) {
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return hip_fail(err, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(CARDAN_ERR_UNSUPPORTED, "device %d >= %d", dev, kMaxDevices);
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  err = hipStreamIsCapturing(stream, &cap);
+  if (err != hipSuccess) return hip_fail(err, "hipStreamIsCapturing");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  ScratchState& st = g_scratch[dev];
+  if (!st.ptr) {
+    void* p = nullptr;
+    err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess || !p) return hip_fail(err, "hipGetSymbolAddress(scratch)");
+    st.ptr = p;
+  }
+  const bool same = st.H == P.H && st.I == P.I && st.E == P.E;
+  if (cap != hipStreamCaptureStatusNone) {
+    *clear = true;
+    st.H = st.I = st.E = 0;
+  } else {
+    *clear = !same;
+    st.H = P.H;
+    st.I = P.I;
+    st.E = P.E;
+  }
+  *ptr = st.ptr;
+  return CARDAN_OK;
+}
+
 Args args_for(const cardan_layer* L, uint8_t* ws) {
   Args A;
   memset(&A, 0, sizeof A);
@@ -339,6 +394,40 @@ int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
   const int flags = F_ROUTE | F_GROUP | F_EXPERTS | (shape->r > 0 ? F_Z : 0);
   const Plan P = make_plan(shape, B, z_sep, flags);
   if ((rc = check_ws(P, ws, ws_bytes))) return rc;
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  Args A = args_for(layer, w);
+  A.x = x;
+  A.topk_idx = topk_idx;
+  A.topk_w = topk_w;
+  A.z_out = reinterpret_cast<float*>(w + P.o_z);
+  A.y = y;
+  return run_layer(P, A, stream);
+}
+
+int cardan_moe_layer_noalloc(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                             const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
+                             hipStream_t stream) {
+  g_err[0] = 0;
+  int rc = check_shape(shape, B);
+  if (rc) return rc;
+  REQ(x, "x");
+  REQ(y, "y");
+  REQ(topk_idx, "topk_idx");
+  REQ(topk_w, "topk_w");
+  if ((rc = check_layer(shape, layer, true))) return rc;
+  const int z_sep = shape->r > 0 && layer->U_up != layer->U_gate;
+  const int flags = F_ROUTE | F_GROUP | F_EXPERTS | (shape->r > 0 ? F_Z : 0);
+  const Plan P = make_plan(shape, B, z_sep, flags);
+  if (P.total > kScratchBytes)
+    return fail(CARDAN_ERR_WORKSPACE, "layer needs %zu bytes of workspace, more than the %zu-byte scratch array",
+                P.total, kScratchBytes);
+  void* ws = nullptr;
+  bool clear = false;
+  if ((rc = scratch_for_call(P, stream, &ws, &clear))) return rc;
+  if (clear) {
+    hipError_t err = launch_zero(ws, P.o_rl, stream);
+    if (err != hipSuccess) return hip_fail(err, "scratch clear launch");
+  }
   uint8_t* w = static_cast<uint8_t*>(ws);
   Args A = args_for(layer, w);
   A.x = x;

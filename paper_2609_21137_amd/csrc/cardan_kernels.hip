@@ -1960,6 +1960,12 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
 }
 
+// Zeroes n16 16-byte words at p (vector stores; a grid-stride loop).
+__global__ __launch_bounds__(kWG) void k_zero16(uint4* p, size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * kWG + threadIdx.x; i < n16; i += (size_t)gridDim.x * kWG)
+    p[i] = make_uint4(0, 0, 0, 0);
+}
+
 // x_next = bf16_rne(y / sqrt(mean(y^2) + eps)) per token. Rows of up to
 // 4096 floats with H % 4 == 0 are held in registers: every load of the row is
 // in flight at once and y is read once (a strided loop over the row, read
@@ -2061,6 +2067,13 @@ hipError_t launch_expert(const Plan& P, const Args& A, int grid, size_t lds, hip
   void* args[] = {&p, &a};
   if (ev0) return hipExtLaunchKernel(fn, dim3(grid), dim3(kWG), args, lds, st, ev0, ev1, 0);
   return hipLaunchKernel(fn, dim3(grid), dim3(kWG), args, lds, st);
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t st) {
+  const size_t n16 = bytes / 16;
+  const int grid = (int)(n16 / kWG < 256 ? n16 / kWG + 1 : 256);
+  hipLaunchKernelGGL(k_zero16, dim3(grid), dim3(kWG), 0, st, static_cast<uint4*>(p), n16);
+  return hipGetLastError();
 }
 
 hipError_t launch_rmsnorm(hipStream_t st, int B, int H, const float* y, float eps, uint16_t* xn, hipEvent_t ev0,

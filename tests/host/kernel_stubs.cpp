@@ -16,6 +16,7 @@ hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t, hip
   return hipErrorInvalidDeviceFunction;
 }
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t) { return hipErrorInvalidDeviceFunction; }
+hipError_t launch_zero(void*, size_t, hipStream_t) { return hipErrorInvalidDeviceFunction; }
 hipError_t launch_rmsnorm(hipStream_t, int, int, const float*, float, uint16_t*, hipEvent_t, hipEvent_t) {
   return hipErrorInvalidDeviceFunction;
 }

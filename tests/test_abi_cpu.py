@@ -233,3 +233,22 @@ def test_workspace_covers_dense_forms(C):
     a = _ws(C, C.make_shape(2048, 768, 128, 8, 8, 256, 128), 16)[1]
     b = _ws(C, C.make_shape(2048, 768, 128, 8, 8, 256, 0), 16)[1]
     assert a >= b > 0
+
+
+def test_noalloc_validation(C):
+    """The no-allocation entry point validates before touching a device: a
+    NULL argument, a bad shape and a layer whose workspace exceeds the
+    library's scratch array are refused."""
+    lib = C.lib()
+    fake = ctypes.c_void_p(0x100000)  # 16-byte aligned, never dereferenced
+    st = C.LayerStruct(*([0x100000] * len(C.LAYER_FIELDS)))
+    qwen = C.make_shape(2048, 768, 128, 8, 8, 256, 128)
+    assert lib.cardan_moe_layer_noalloc(None, 1, fake, ctypes.byref(st), fake, fake, fake, None) == -1
+    assert lib.cardan_moe_layer_noalloc(ctypes.byref(qwen), 1, None, ctypes.byref(st), fake, fake, fake,
+                                        None) == -1
+    assert lib.cardan_moe_layer_noalloc(ctypes.byref(qwen), 0, fake, ctypes.byref(st), fake, fake, fake,
+                                        None) == -2
+    wide = C.make_shape(4096, 1536, 64, 6, 8, 256, 256)
+    rc = lib.cardan_moe_layer_noalloc(ctypes.byref(wide), 64, fake, ctypes.byref(st), fake, fake, fake, None)
+    assert rc == -4, lib.cardan_last_error().decode()
+    assert b"scratch" in lib.cardan_last_error()
