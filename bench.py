@@ -9,6 +9,17 @@ from HBM, not from the 256 MB last-level cache. Prints one JSON line.
 value  = compressed-weight bytes touched per step (active experts' codes and
          low-rank coefficients, plus the shared bases and code books) summed
          over the timed steps, divided by the timed wall time (GB/s).
+
+Protocol: the rotated layers are drawn on the device (``synth_device``: the
+synthetic recipe's laws, torch generators); one running input index runs
+through the warm-up and every timed pass, so no pass starts on inputs the
+previous one just read, and the rotation is sized so that more than 256 MB
+(the last-level cache) is read between two visits of any input. Passes, each
+followed by a check of the workspace status word: warm-up; a wall-clock pass
+(``ms_per_step``, ``value``); a pass with a HIP event pair around every step
+(per-step latency: median and a 10,000-resample bootstrap 95% interval,
+Sec. 5.1's timing method); a pass with event pairs recorded by each kernel's
+own dispatch (per-kernel durations, ``roofline``).
 """
 
 from __future__ import annotations
@@ -126,41 +137,62 @@ def load_traffic(kernel: str, workload: str, src_hash: str):
 
 
 def dense_weights(torch, w, n_layers, dense_cache, form):
-    """Dense bf16 expert matrices per rotated layer, drawn on the device from
-    seeded generators (N(0, 0.02), the synthetic recipe's law; drawing the
-    1.2 GB per layer on the host would dominate the run)."""
+    """Dense bf16 expert matrices per rotated layer, drawn on the device
+    (``synth_device``; drawing 1.2 GB per layer on the host would dominate
+    the run)."""
+    from paper_2609_21137_amd import synth_device
     key = (w.H, w.I, w.E, w.seed, form)
     if key not in dense_cache:
         dense_cache.clear()
         torch.cuda.empty_cache()
-        mats = []
-        for li in range(n_layers):
-            g = torch.Generator(device="cuda")
-            g.manual_seed(1_000_003 * w.seed + li)
-            m = {}
-            names = ("W_gate", "W_up", "W_down") if form == "dense" else ("W_down",)
-            for n in names:
-                shp = (w.E, w.I, w.H) if n == "W_down" else (w.E, w.H, w.I)
-                m[n] = (torch.randn(shp, generator=g, device="cuda", dtype=torch.float32) * 0.02
-                        ).to(torch.bfloat16)
-            mats.append(m)
-        dense_cache[key] = mats
+        names = ("W_gate", "W_up", "W_down") if form == "dense" else ("W_down",)
+        dense_cache[key] = [synth_device.dense_tensors(w, li, names) for li in range(n_layers)]
     return dense_cache[key]
+
+
+MALL_BYTES = 256 << 20
+
+
+def device_layers(C, torch, w, n_layers, layers_cache):
+    """``n_layers`` independently seeded layers of workload ``w`` on the device."""
+    from paper_2609_21137_amd import synth_device
+    key = (w.H, w.I, w.E, w.d, w.K, w.r, w.seed, w.hot_experts, w.hot_bias)
+    have = layers_cache.get(key, [])
+    if len(have) < n_layers:
+        if not have:
+            layers_cache.clear()
+            torch.cuda.empty_cache()
+        have = have + [C.DeviceLayer(synth_device.layer_tensors(w, li))
+                       for li in range(len(have), n_layers)]
+        layers_cache[key] = have
+    return have[:n_layers]
+
+
+def bootstrap_ci(v, n_boot=10_000, seed=0):
+    """Median of v and the 2.5 / 97.5 percentiles of the median over
+    ``n_boot`` resamples with replacement."""
+    v = np.asarray(v, dtype=np.float64)
+    rng = np.random.default_rng(seed)
+    meds = np.median(v[rng.integers(0, len(v), size=(n_boot, len(v)))], axis=1)
+    return float(np.median(v)), float(np.percentile(meds, 2.5)), float(np.percentile(meds, 97.5))
+
+
+def hold_stream(torch, ms):
+    """Keeps the current stream busy for about ``ms`` so the host can enqueue
+    a whole pass ahead of the device (per-step event pairs then time the GPU,
+    not host launch gaps). Returns False where torch has no sleep kernel."""
+    try:
+        torch.cuda._sleep(int(ms * 2.4e6))
+        return True
+    except Exception:
+        return False
 
 
 def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache, form="compressed",
                   dense_cache=None):
     from paper_2609_21137_amd import synth
     shape = C.shape_of(w)
-    key = (w.H, w.I, w.E, w.d, w.K, w.r, w.seed, w.hot_experts, w.hot_bias)
-    if key not in layers_cache:
-        layers_cache.clear()
-        torch.cuda.empty_cache()
-        dls = []
-        for li in range(n_layers):
-            dls.append(C.DeviceLayer.from_numpy(synth.workload_layer(w, li)))
-        layers_cache[key] = dls
-    dls = layers_cache[key]
+    dls = device_layers(C, torch, w, n_layers, layers_cache)
     # input j always runs on layer j % n_layers
     xs = [C.bf16_tensor(synth.workload_input(w, j % n_layers, step=j // n_layers))
           for j in range(n_inputs)]
@@ -210,69 +242,93 @@ def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache, 
         def call(xp, st):
             return fn(ctypes.byref(shape), B, xp, ctypes.byref(st), *args_tail)
 
-    def step(i):
-        xp, st = ptrs[i % n_inputs]
+    def step_bytes(j):
+        if form == "compressed":
+            return compressed_bytes(w, n_act[j])
+        b = dense_bytes(w, n_act[j], form)
+        b["compressed"] = b["weights"]  # the form's own weight bytes
+        return b
+
+    per_input = [step_bytes(j)["compressed"] for j in range(n_inputs)]
+    rotation = sum(per_input)
+    pos = [0]  # one running input index through every pass
+
+    def step():
+        j = pos[0] % n_inputs
+        pos[0] += 1
+        xp, st = ptrs[j]
         rc = call(xp, st)
         if rc != 0:
             raise RuntimeError(lib.cardan_last_error().decode())
+        return j
 
-    for i in range(warmup):
-        step(i)
-    torch.cuda.synchronize()
+    def check_status(what):
+        torch.cuda.synchronize()
+        st = C.workspace_status(ws)
+        if st != 0:
+            raise RuntimeError(f"{w.name} ({form}): {st} in-kernel waits gave up during the {what}")
 
-    # timed region: exactly `steps` layer calls, bracketed by device syncs
+    for _ in range(warmup):
+        step()
+    check_status("warm-up")
+
+    def pass_bytes(js):
+        tot = {"compressed": 0, "expert_kernel": 0, "route_kernel": 0}
+        for j in js:
+            b = step_bytes(j)
+            for k in tot:
+                tot[k] += b[k]
+        return tot
+
+    # wall pass: exactly `steps` layer calls, bracketed by device syncs
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(steps):
-        step(i)
+    js_wall = [step() for _ in range(steps)]
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    check_status("wall-clock pass")
 
-    # the same steps again with HIP events around every kernel, recorded by
-    # the library on the stream the kernels run on: per-kernel durations
+    # per-step pass: an event pair around every layer call on the launch stream
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    held = hold_stream(torch, 0.05 * steps)
+    js_ev = []
+    for i in range(steps):
+        ev[i][0].record()
+        js_ev.append(step())
+        ev[i][1].record()
+    check_status("per-step event pass")
+    per_step_us = [1e3 * a.elapsed_time(b) for a, b in ev]
+
+    # kernel pass: event pairs recorded by each kernel's own dispatch
     C.profile_begin(steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    for i in range(steps):
-        step(i)
+    js_k = [step() for _ in range(steps)]
     torch.cuda.synchronize()
     wall_events = time.perf_counter() - t1
     prof = C.profile_end()
+    check_status("kernel event pass")
 
-    acts = [n_act[i % n_inputs] for i in range(steps)]
-    tot = {"compressed": 0, "expert_kernel": 0, "route_kernel": 0}
-    for a in acts:
-        if form == "compressed":
-            b = compressed_bytes(w, a)
-        else:
-            b = dense_bytes(w, a, form)
-            b["compressed"] = b["weights"]  # the form's own weight bytes
-        for k in tot:
-            tot[k] += b[k]
-    return {"wall_s": wall, "wall_events_s": wall_events, "prof": prof, "bytes": tot,
-            "mean_active": float(np.mean(acts)), "layers": n_layers, "inputs": n_inputs}
+    return {"wall_s": wall, "wall_events_s": wall_events, "prof": prof, "bytes": pass_bytes(js_wall),
+            "bytes_kernel_pass": pass_bytes(js_k), "per_step_us": per_step_us, "stream_held": held,
+            "mean_active": float(np.mean([n_act[j] for j in js_wall])), "layers": n_layers,
+            "inputs": n_inputs, "rotation_bytes": rotation,
+            "min_bytes_between_revisits": rotation - max(per_input)}
 
 
-def time_decode_step(C, torch, w, steps, warmup, n_distinct, layers_cache):
-    """The stacked-layer decode step: w.layers MoE layers, each layer's output
-    RMS-normalised (bf16) into the next layer's input. The layers cycle over
-    `n_distinct` independently seeded layers (every layer holds all E experts,
-    so the weights touched per step exceed the last-level cache). The step is
-    captured once as a HIP graph and replayed; eager timing is the fallback."""
+def time_decode_step(C, torch, w, steps, warmup, layers_cache):
+    """The stacked-layer decode step: w.layers MoE layers with independently
+    seeded weights (drawn on the device), each layer's output RMS-normalised
+    (bf16) into the next layer's input. The step is captured once as a HIP
+    graph and replayed; eager launches are the fallback. Per-step latency:
+    an event pair around every replay."""
     import ctypes
 
     from paper_2609_21137_amd import synth
     shape = C.shape_of(w)
-    key = (w.H, w.I, w.E, w.d, w.K, w.r, w.seed, w.hot_experts, w.hot_bias)
-    if key not in layers_cache:
-        layers_cache.clear()
-        torch.cuda.empty_cache()
-        layers_cache[key] = [C.DeviceLayer.from_numpy(synth.workload_layer(w, li))
-                             for li in range(n_distinct)]
-    dls = layers_cache[key][:n_distinct]
-    n_distinct = len(dls)
-    structs = [dl.struct() for dl in dls]
     B, L = w.B, w.layers
+    dls = device_layers(C, torch, w, L, layers_cache)
+    structs = [dl.struct() for dl in dls]
     x0 = C.bf16_tensor(synth.workload_input(w, 0))
     xa = torch.empty_like(x0)
     xb = torch.empty_like(x0)
@@ -288,8 +344,7 @@ def time_decode_step(C, torch, w, steps, warmup, n_distinct, layers_cache):
         for li in range(L):
             xout = xa if li % 2 == 0 else xb
             rc = lib.cardan_moe_layer(ctypes.byref(shape), B, ctypes.c_void_p(xin.data_ptr()),
-                                      ctypes.byref(structs[li % n_distinct]),
-                                      ctypes.c_void_p(y.data_ptr()),
+                                      ctypes.byref(structs[li]), ctypes.c_void_p(y.data_ptr()),
                                       ctypes.c_void_p(idx[li].data_ptr()),
                                       ctypes.c_void_p(wt[li].data_ptr()),
                                       ctypes.c_void_p(ws.data_ptr()), ws.numel(), st)
@@ -328,16 +383,42 @@ def time_decode_step(C, torch, w, steps, warmup, n_distinct, layers_cache):
         run()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record()
+        run()
+        b.record()
+    torch.cuda.synchronize()
+    st = C.workspace_status(ws)
+    if st != 0:
+        raise RuntimeError(f"{w.name}: {st} in-kernel waits gave up")
+    per_step_ms = [a.elapsed_time(b) for a, b in ev]
+    med, lo, hi = bootstrap_ci(per_step_ms)
     bytes_step = sum(compressed_bytes(w, a)["compressed"] for a in n_act)
-    return {"workload": w.name, "B": B, "layers": L, "distinct_layers": n_distinct, "mode": mode,
+    return {"workload": w.name, "B": B, "layers": L, "distinct_layers": len(dls), "mode": mode,
             "ms_per_step": round(1e3 * wall / steps, 4),
+            "ms_per_step_median": round(med, 4), "ms_per_step_ci95": [round(lo, 4), round(hi, 4)],
             "us_per_layer": round(1e6 * wall / steps / L, 3),
+            "us_per_layer_median": round(1e3 * med / L, 3),
             "GBps": round(bytes_step * steps / wall / 1e9, 2),
+            "bytes_per_step": bytes_step,
             "mean_active_experts": float(np.mean(n_act))}
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, budget_s):
-    """The float64 oracle timed on this host's cores on a bounded sample."""
+    """The float64 oracle timed on this host's cores on a bounded sample: all
+    the cores this process may use (the reported value), then one core."""
     import threadpoolctl
 
     import oracle.cardan_oracle as O
@@ -345,40 +426,58 @@ def cpu_baseline(w, budget_s):
     cores = len(os.sched_getaffinity(0))
     L = synth.workload_layer(w, 0)
     x = synth.workload_input(w, 0)
-    n, t_tot, nbytes = 0, 0.0, 0
-    with threadpoolctl.threadpool_limits(cores):
-        while t_tot < budget_s or n == 0:
-            t0 = time.perf_counter()
-            _, idx, _, _ = O.moe_layer_factored(x, L, w.top_k, w.d)
-            t_tot += time.perf_counter() - t0
-            nbytes += compressed_bytes(w, len(np.unique(idx)))["compressed"]
-            n += 1
+
+    def leg(threads, budget):
+        n, t_tot, nbytes = 0, 0.0, 0
+        with threadpoolctl.threadpool_limits(threads):
+            while t_tot < budget or n == 0:
+                t0 = time.perf_counter()
+                _, idx, _, _ = O.moe_layer_factored(x, L, w.top_k, w.d)
+                t_tot += time.perf_counter() - t0
+                nbytes += compressed_bytes(w, len(np.unique(idx)))["compressed"]
+                n += 1
+        return n, t_tot, nbytes
+
+    n, t_tot, nbytes = leg(cores, budget_s * 0.6)
+    n1, t1, b1 = leg(1, budget_s * 0.4)
     return {"value": round(nbytes / t_tot / 1e9, 4), "unit": "GB/s", "cores": cores,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"{n} steps of {w.name} (layer 0), float64 numpy factored form, "
-                      f"{t_tot:.1f} s total, {1e3 * t_tot / n:.1f} ms/step"}
+                      f"{t_tot:.1f} s total, {1e3 * t_tot / n:.1f} ms/step",
+            "one_core": {"value": round(b1 / t1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                         "sample": f"{n1} steps, {t1:.1f} s total, {1e3 * t1 / n1:.1f} ms/step"}}
 
 
 def summarize(w, r, src_hash, name=None):
     prof = r["prof"]
     steps = prof["expert"][1]
     ex_ms = prof["expert"][0] / max(1, steps)
-    ex_bytes = r["bytes"]["expert_kernel"] / max(1, steps)
+    ex_bytes = r["bytes_kernel_pass"]["expert_kernel"] / max(1, steps)
     achieved = ex_bytes / (ex_ms * 1e-3) / 1e9
     name = name or w.name
     traffic = load_traffic("k_expert", name, src_hash)
+    n = len(r["per_step_us"])
+    med, lo, hi = bootstrap_ci(r["per_step_us"])
     return {
         "workload": name,
         "B": w.B,
-        "us_per_layer": round(1e6 * r["wall_s"] / steps, 3),
-        "us_per_layer_with_kernel_events": round(1e6 * r["wall_events_s"] / steps, 3),
+        "us_per_layer": round(1e6 * r["wall_s"] / n, 3),
+        "us_per_layer_median": round(med, 3),
+        "us_per_layer_ci95": [round(lo, 3), round(hi, 3)],
+        "us_per_layer_event_mean": round(float(np.mean(r["per_step_us"])), 3),
+        "us_per_layer_with_kernel_events": round(1e6 * r["wall_events_s"] / n, 3),
         "GBps": round(r["bytes"]["compressed"] / r["wall_s"] / 1e9, 2),
+        "GBps_median": round(r["bytes"]["compressed"] / n / (med * 1e-6) / 1e9, 2),
         "mean_active_experts": r["mean_active"],
         "kernel_us": {k: round(1e3 * v[0] / max(1, v[1]), 3) for k, v in prof.items() if v[1]},
         "roofline": {"kernel": "k_expert", "bound": "hbm", "achieved": round(achieved, 2),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "bytes_per_launch": round(ex_bytes)},
+        "rotation": {"layers": r["layers"], "inputs": r["inputs"], "bytes": r["rotation_bytes"],
+                     "min_bytes_between_revisits": r["min_bytes_between_revisits"],
+                     "exceeds_last_level_cache": r["min_bytes_between_revisits"] > MALL_BYTES,
+                     "per_step_pass_host_ahead": r["stream_held"]},
     }
 
 
@@ -494,7 +593,7 @@ def main():
     src_hash = kernel_source_hash()
     w = WORKLOADS[args.workload]
     cache = {}
-    print(f"[bench] {w.name}: synthesizing {args.layers} layers", file=sys.stderr, flush=True)
+    print(f"[bench] {w.name}: drawing {args.layers} layers on the device", file=sys.stderr, flush=True)
     r = time_workload(C, torch, w, args.steps, args.warmup, args.layers, args.inputs, cache)
     main_sum = summarize(w, r, src_hash)
     print(f"[bench] {w.name}: {main_sum['us_per_layer']} us/layer", file=sys.stderr, flush=True)
@@ -503,7 +602,7 @@ def main():
         ww = WORKLOADS[name]
         if ww.layers > 1:
             print(f"[bench] {ww.name}: {ww.layers}-layer decode step", file=sys.stderr, flush=True)
-            also.append(time_decode_step(C, torch, ww, max(5, args.steps // 10), 2, args.layers, cache))
+            also.append(time_decode_step(C, torch, ww, max(5, args.steps // 4), 2, cache))
             print(f"[bench] {ww.name}: {also[-1]['ms_per_step']} ms/step", file=sys.stderr, flush=True)
             continue
         print(f"[bench] {ww.name}", file=sys.stderr, flush=True)
@@ -557,7 +656,10 @@ def main():
                    "inputs_rotated": args.inputs,
                    "parallelism": "none"},
         "us_per_layer": main_sum["us_per_layer"],
+        "us_per_layer_median": main_sum["us_per_layer_median"],
+        "us_per_layer_ci95": main_sum["us_per_layer_ci95"],
         "hbm_frac_of_peak": round(main_sum["GBps"] / HBM_PEAK_GBPS, 4),
+        "rotation": main_sum["rotation"],
         "kernel_us": main_sum["kernel_us"],
         "mean_active_experts": main_sum["mean_active_experts"],
         "us_per_layer_with_kernel_events": main_sum["us_per_layer_with_kernel_events"],
