@@ -49,6 +49,17 @@ __device__ __forceinline__ f32x4 mfma_bf16(uint4 a, uint4 b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// Weight streams read through buffer resources: a load whose offset is past
+// the resource's size returns zeros without a memory access, so every
+// pipeline slot is always issued (a static number of loads in flight, hence
+// exact waits) while steps past the end cost no traffic.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOob = 0x80000000u;  // an offset past every resource
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 __device__ __forceinline__ int* ctr(const Args& A, int i) {
   return reinterpret_cast<int*>(A.ws) + i * kCtrStride;
 }
@@ -239,66 +250,58 @@ __device__ int block_exclusive_scan(int* arr, int n, int* tmp4) {
 }
 
 // Router chunk (c, g, tb): partial logits over hidden rows [64c, 64c + 64)
-// for experts [64g, 64g + 64) of tokens [4tb, 4tb + 4). Lane l of wave w
-// owns expert 64g + l and rows 64c + 16w .. + 16; float64 FMAs of exact bf16
-// products, four independent chains per token, then the four waves'
+// for experts [64g, 64g + 64) of tokens [4tb, 4tb + 4). Lane l of wave w owns
+// expert 64g + l and rows 64c + 16w .. + 16 (rows past H read zeros); float64
+// FMAs of exact bf16 products in row order per token, then the four waves'
 // partials are added in wave order through LDS.
 __device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c, int g, int tb, uint8_t* smem) {
-  float* xs = reinterpret_cast<float*>(smem);                          // [16][64]
-  double* part = reinterpret_cast<double*>(smem + kTokPass * kRowsRouter * 4);  // [4][16][64]
+  constexpr int RW = kRowsRouter / 4;  // rows per wave
+  float* xs = reinterpret_cast<float*>(smem);                                     // [4][64]
+  double* part = reinterpret_cast<double*>(smem + kRouterTok * kRowsRouter * 4);  // [4][4][64]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int E = P.E, H = P.H, B = P.B, h0 = c * kRowsRouter;
   const int e = min(g * 64 + lane, E - 1);  // lanes past E compute a copy that is never stored
-  const uint16_t* Wr = A.L.router_w + (size_t)(h0 + 16 * w) * E + e;
-  uint32_t wv[16];
+  const rsrc_t wr = make_rsrc(A.L.router_w, (uint32_t)H * E * 2);
+  uint32_t wv[RW];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) wv[i] = Wr[(size_t)i * E];
+  for (int i = 0; i < RW; ++i) {
+    const int h = h0 + RW * w + i;
+    wv[i] = __builtin_amdgcn_raw_buffer_load_b16(wr, h < H ? (uint32_t)((h * E + e) * 2) : kOob, 0, 0);
+  }
   double* rl = wsp<double>(A, P.o_rl);
-  {
-    const int tg = tb * kRouterTok, nt = min(kRouterTok, B - tg);
-    for (int i = tid; i < nt * kRowsRouter; i += kWG) {
-      const int t = i / kRowsRouter, h = i % kRowsRouter;
-      xs[i] = bf(A.x[(size_t)(tg + t) * H + h0 + h]);
-    }
-    __syncthreads();
-    trace_mark(0);
-    double wd[16];
+  const int tg = tb * kRouterTok, nt = min(kRouterTok, B - tg);
+  for (int i = tid; i < nt * kRowsRouter; i += kWG) {
+    const int t = i / kRowsRouter, h = i % kRowsRouter;
+    xs[i] = h0 + h < H ? bf(A.x[(size_t)(tg + t) * H + h0 + h]) : 0.0f;
+  }
+  __syncthreads();
+  trace_mark(0);
+  double wd[RW];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) wd[i] = (double)bf(wv[i]);
-    for (int t = 0; t < nt; ++t) {
-      // the wave's 16 inputs of token t: the same LDS words for every lane
-      const float4* xr = reinterpret_cast<const float4*>(xs + t * kRowsRouter + 16 * w);
-      const float4 x0 = xr[0], x1 = xr[1], x2 = xr[2], x3 = xr[3];
-      double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
-      a0 = fma(wd[0], (double)x0.x, a0);
-      a1 = fma(wd[1], (double)x0.y, a1);
-      a2 = fma(wd[2], (double)x0.z, a2);
-      a3 = fma(wd[3], (double)x0.w, a3);
-      a0 = fma(wd[4], (double)x1.x, a0);
-      a1 = fma(wd[5], (double)x1.y, a1);
-      a2 = fma(wd[6], (double)x1.z, a2);
-      a3 = fma(wd[7], (double)x1.w, a3);
-      a0 = fma(wd[8], (double)x2.x, a0);
-      a1 = fma(wd[9], (double)x2.y, a1);
-      a2 = fma(wd[10], (double)x2.z, a2);
-      a3 = fma(wd[11], (double)x2.w, a3);
-      a0 = fma(wd[12], (double)x3.x, a0);
-      a1 = fma(wd[13], (double)x3.y, a1);
-      a2 = fma(wd[14], (double)x3.z, a2);
-      a3 = fma(wd[15], (double)x3.w, a3);
-      part[(w * kTokPass + t) * 64 + lane] = (a0 + a1) + (a2 + a3);
+  for (int i = 0; i < RW; ++i) wd[i] = (double)bf(wv[i]);
+  for (int t = 0; t < nt; ++t) {
+    // the wave's inputs of token t: the same LDS words for every lane
+    const float4* xr = reinterpret_cast<const float4*>(xs + t * kRowsRouter + RW * w);
+    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+#pragma unroll
+    for (int q = 0; q < RW / 4; ++q) {
+      const float4 xq = xr[q];
+      a0 = fma(wd[4 * q + 0], (double)xq.x, a0);
+      a1 = fma(wd[4 * q + 1], (double)xq.y, a1);
+      a2 = fma(wd[4 * q + 2], (double)xq.z, a2);
+      a3 = fma(wd[4 * q + 3], (double)xq.w, a3);
     }
-    __syncthreads();
-    trace_mark(1);
-    for (int i = tid; i < nt * 64; i += kWG) {
-      const int t = i >> 6, el = i & 63;
-      if (g * 64 + el < E) {
-        const double v = (part[(0 * kTokPass + t) * 64 + el] + part[(1 * kTokPass + t) * 64 + el]) +
-                         (part[(2 * kTokPass + t) * 64 + el] + part[(3 * kTokPass + t) * 64 + el]);
-        st_dev(rl + ((size_t)c * B + tg + t) * E + g * 64 + el, v);
-      }
+    part[(w * kRouterTok + t) * 64 + lane] = (a0 + a1) + (a2 + a3);
+  }
+  __syncthreads();
+  trace_mark(1);
+  for (int i = tid; i < nt * 64; i += kWG) {
+    const int t = i >> 6, el = i & 63;
+    if (g * 64 + el < E) {
+      const double v = (part[(0 * kRouterTok + t) * 64 + el] + part[(1 * kRouterTok + t) * 64 + el]) +
+                       (part[(2 * kRouterTok + t) * 64 + el] + part[(3 * kRouterTok + t) * 64 + el]);
+      st_dev(rl + ((size_t)c * B + tg + t) * E + g * 64 + el, v);
     }
-    __syncthreads();
   }
   trace_mark(2);
   set_flag(wsp<int>(A, P.o_rc_flag) + item * kTickPad);
@@ -552,9 +555,26 @@ __device__ void wave_topk(const double* lg, int E, int k, int* sel, unsigned lon
   wave_lds_sync();
 }
 
-// Select item for token t: logits (fixed-order sum of the chunk partials plus
-// bias), top-k by descending logit with ties to the lower index, softmax over
-// the k selected logits, written to topk_idx / topk_w.
+// Logit of expert e for token t: the router chunks' partials summed in chunk
+// order, plus the bias (the same arithmetic wherever the select runs).
+__device__ __forceinline__ double router_logit(const Plan& P, const Args& A, int t, int e, float bias) {
+  constexpr int RB = 32;  // partials in flight; past the end re-read the last one, masked out
+  const double* rl = wsp<const double>(A, P.o_rl);
+  double s = 0.0;
+  for (int c0 = 0; c0 < P.nch_r; c0 += RB) {
+    double v[RB];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) v[i] = ld_dev(rl + ((size_t)min(c0 + i, P.nch_r - 1) * P.B + t) * P.E + e);
+#pragma unroll
+    for (int i = 0; i < RB; ++i) s += (c0 + i < P.nch_r) ? v[i] : 0.0;
+  }
+  return A.L.router_bias ? s + (double)bias : s;
+}
+
+// Top-k and gating of one token from its logits lg[0..E) in LDS (smem, lg_cap
+// doubles, then the scratch below) and each thread's own logit (expert tid):
+// top-k by descending logit with ties to the lower index, softmax over the k
+// selected logits; lanes j < k of wave 0 return selection j (expert, weight).
 //
 // Up to kWG experts, each thread holds its expert's key and counts the
 // experts with a larger high key half (comparisons split over the waves):
@@ -564,39 +584,16 @@ __device__ void wave_topk(const double* lg, int E, int k, int* sel, unsigned lon
 // held by a single expert, or by the correct best of a group at rank k - 1,
 // so the slots are the exact selection. Otherwise (and for more experts) one
 // wave selects exactly on the full keys.
-__device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) {
+__device__ void select_core(const Plan& P, uint8_t* smem, int lg_cap, double own, int& e_out, float& w_out) {
   const int tid = threadIdx.x;
-  const int E = P.E, k = P.k, B = P.B;
+  const int E = P.E, k = P.k;
   double* lg = reinterpret_cast<double*>(smem);                                    // [E]
-  unsigned long long* slot = reinterpret_cast<unsigned long long*>(lg + kMaxE);    // [k]
+  unsigned long long* slot = reinterpret_cast<unsigned long long*>(lg + lg_cap);   // [k]
   unsigned long long* ck = slot + kMaxK;                                           // [k]
   unsigned* hk = reinterpret_cast<unsigned*>(ck + kMaxK);                          // [kWG]
   int* rank = reinterpret_cast<int*>(hk + kWG);                                    // [kWG]
   int* sel = rank + kWG;                                                           // [k]
   int* ce = sel + kMaxK;                                                           // [k]
-  // the bias is read before the wait so its latency is hidden
-  const float b0 = (A.L.router_bias && tid < E) ? A.L.router_bias[tid] : 0.0f;
-  const int* rcf = wsp<const int>(A, P.o_rc_flag);
-  const int nrt = P.nch_r * P.n_eg;  // router chunks of this token's block
-  rcf += (t / kRouterTok) * nrt * kTickPad;
-  wait_all(A, nrt, [&](int i) { return ld_dev(rcf + i * kTickPad) != 0; });
-  const double* rl = wsp<const double>(A, P.o_rl);
-  double own = 0.0;  // logit of expert tid
-  for (int e = tid; e < E; e += kWG) {
-    double s = 0.0;
-    for (int c0 = 0; c0 < P.nch_r; c0 += 32) {
-      // 32 chunk partials in flight; chunks past the end re-read the last
-      // one and are masked out of the sum
-      double v[32];
-#pragma unroll
-      for (int i = 0; i < 32; ++i) v[i] = ld_dev(rl + ((size_t)min(c0 + i, P.nch_r - 1) * B + t) * E + e);
-#pragma unroll
-      for (int i = 0; i < 32; ++i) s += (c0 + i < P.nch_r) ? v[i] : 0.0;
-    }
-    if (A.L.router_bias) s += (double)(e == tid ? b0 : A.L.router_bias[e]);
-    lg[e] = s;
-    if (e == tid) own = s;
-  }
   const bool counted = E <= kWG;
   if (counted) {
     const int Ep = (E + 31) & ~31;
@@ -630,6 +627,8 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
   }
   __syncthreads();
   trace_mark(0);
+  e_out = -1;
+  w_out = 0.0f;
   if (tid < 64) {
     const unsigned long long v = counted && tid < k ? slot[tid] : 1ull;
     int e;
@@ -658,11 +657,56 @@ __device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) 
     const double ex = tid < k ? (double)expf((float)(x - mx)) : 0.0;
     const double sum = wave_sum(ex);
     if (tid < k) {
-      st_dev(A.topk_idx + t * k + tid, e);
-      st_dev(A.topk_w + t * k + tid, (float)(ex / sum));
+      e_out = e;
+      w_out = (float)(ex / sum);
     }
     trace_mark(2);
   }
+}
+
+// Select item for token t (see select_core): waits for its token block's
+// router chunks, sums their partials per expert in chunk order (plus the
+// bias) and writes topk_idx / topk_w.
+__device__ void item_select(const Plan& P, const Args& A, int t, uint8_t* smem) {
+  const int tid = threadIdx.x;
+  const int E = P.E, k = P.k;
+  double* lg = reinterpret_cast<double*>(smem);  // [E]
+  // the bias is read before the wait so its latency is hidden
+  const float b0 = (A.L.router_bias && tid < E) ? A.L.router_bias[tid] : 0.0f;
+  const int* rcf = wsp<const int>(A, P.o_rc_flag);
+  const int nrt = P.nch_r * P.n_eg;  // router chunks of this token's block
+  rcf += (t / kRouterTok) * nrt * kTickPad;
+  wait_all(A, nrt, [&](int i) { return ld_dev(rcf + i * kTickPad) != 0; });
+  double own = 0.0;  // logit of expert tid
+  for (int e = tid; e < E; e += kWG) {
+    const double s = router_logit(P, A, t, e, e == tid ? b0 : (A.L.router_bias ? A.L.router_bias[e] : 0.0f));
+    lg[e] = s;
+    if (e == tid) own = s;
+  }
+  int e_sel;
+  float w_sel;
+  select_core(P, smem, kMaxE, own, e_sel, w_sel);
+  if (tid < k) {
+    st_dev(A.topk_idx + t * k + tid, e_sel);
+    st_dev(A.topk_w + t * k + tid, w_sel);
+  }
+}
+
+// z value (basis src, row-major [B][r] index rem): the z items' partials
+// summed in item order.
+__device__ __forceinline__ float z_sum(const Plan& P, const Args& A, int src, int rem) {
+  constexpr int ZB = 8;
+  const int B = P.B, r = P.r;
+  const float* zp = wsp<const float>(A, P.o_zp) + ((size_t)src * P.nq_z * B) * r + rem;
+  float s = 0.0f;
+  for (int c0 = 0; c0 < P.nq_z; c0 += ZB) {
+    float v[ZB];
+#pragma unroll
+    for (int j = 0; j < ZB; ++j) v[j] = ld_dev(zp + (size_t)min(c0 + j, P.nq_z - 1) * B * r);
+#pragma unroll
+    for (int j = 0; j < ZB; ++j) s += (c0 + j < P.nq_z) ? v[j] : 0.0f;
+  }
+  return s;
 }
 
 __device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
@@ -673,16 +717,7 @@ __device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
   if (o < 2 * B * r) {
     const int pj = o / (B * r), rem = o % (B * r);
     const int src = P.z_sep ? pj : 0;
-    const float* zp = wsp<const float>(A, P.o_zp) + ((size_t)src * P.nch_z * B) * r + rem;
-    float s = 0.0f;
-    for (int c0 = 0; c0 < P.nch_z; c0 += 32) {
-      float v[32];
-#pragma unroll
-      for (int j = 0; j < 32; ++j) v[j] = ld_dev(zp + (size_t)min(c0 + j, P.nch_z - 1) * B * r);
-#pragma unroll
-      for (int j = 0; j < 32; ++j) s += (c0 + j < P.nch_z) ? v[j] : 0.0f;
-    }
-    A.z_out[o] = s;
+    A.z_out[o] = z_sum(P, A, src, rem);
   }
 }
 
@@ -714,17 +749,6 @@ template <int NREAD, int NMFMA>
 __device__ __forceinline__ void sched_step() {
   __builtin_amdgcn_sched_group_barrier(0x100, NREAD, 0);  // DS reads
   __builtin_amdgcn_sched_group_barrier(0x008, NMFMA, 0);  // MFMA
-}
-
-// Weight streams read through buffer resources: a load whose offset is past
-// the resource's size returns zeros without a memory access, so every
-// pipeline slot is always issued (a static number of loads in flight, hence
-// exact waits) while steps past the end cost no traffic.
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-constexpr uint32_t kOob = 0x80000000u;  // an offset past every resource
-
-__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
 constexpr int kSc1 = 16;  // cache policy operand of a device-scope (sc1) buffer access
@@ -1123,26 +1147,27 @@ __device__ __forceinline__ float4 fma4(float w, float4 v, float4 a) {
 // ===========================================================================
 // shared projections on MFMA
 // ===========================================================================
-// z unit u (one wave): basis pj, 64 columns, K-split s of H; item j runs the
-// four units 4 j .. 4 j + 3 side by side. Partial z goes to zp[pj][s][t][q].
+// z item j: basis pj, 64 columns of z, and four consecutive K-splits of H,
+// one per wave (split 4q + w); the waves' partial U^T x are added in wave
+// order through LDS and item j stores one partial, zp[pj][q][t][col].
 __device__ void item_z(const Plan& P, const Args& A, int j, uint8_t* smem) {
-  const int w = threadIdx.x >> 6;
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   const int ncol = (P.r + 63) / 64;
-  const int units = (P.z_sep ? 2 : 1) * ncol * P.nch_z;
-  const int u = j * 4 + w;
-  const bool active = u < units;
-  const int uu = active ? u : 0;
-  const int pj = uu / (ncol * P.nch_z), rem = uu % (ncol * P.nch_z);
-  const int c64 = rem % ncol, s = rem / ncol;
+  const int q = j % P.nq_z, rem = j / P.nq_z;
+  const int c64 = rem % ncol, pj = rem / ncol;
+  const int s = 4 * q + w;
+  const bool active = s < P.nch_z;
   const int KS = P.H / 32;
-  const int ks0 = s * KS / P.nch_z, ks1 = (s + 1) * KS / P.nch_z;
+  const int ks0 = active ? s * KS / P.nch_z : 0, ks1 = active ? (s + 1) * KS / P.nch_z : 0;
   const int c0 = c64 * 64;
   const uint16_t* U = pj ? A.L.U_up : A.L.U_gate;
   // each wave stages its own activations: [16 tokens][(ks1 - ks0) * 4 + 1] uint4
   const int ld = (KS + P.nch_z - 1) / P.nch_z * 4 + 1;
   uint4* ops = reinterpret_cast<uint4*>(smem) + w * kTokPass * ld;
+  float* red = reinterpret_cast<float*>(smem + (size_t)4 * kTokPass * ld * 16);  // [4][64][16]
   float* zp = wsp<float>(A, P.o_zp);
   const int B = P.B, H = P.H, r = P.r;
+  const WsAccess ws(A, P);
   DensePipe<1, kPdDense> pipe;
   for (int tg = 0; tg < B; tg += kTokPass) {
     const int nt = min(kTokPass, B - tg);
@@ -1150,14 +1175,31 @@ __device__ void item_z(const Plan& P, const Args& A, int j, uint8_t* smem) {
     __syncthreads();
     if (active)  // this wave's own region: lanes stride by 64
       stage_bf16(ops, ld, nt, (ks1 - ks0) * 4,
-                 [&](int t) { return A.x + (size_t)(tg + t) * H + ks0 * 32; }, threadIdx.x & 63, 64);
+                 [&](int t) { return A.x + (size_t)(tg + t) * H + ks0 * 32; }, l, 64);
     __syncthreads();
-    if (active) {
-      f32x4 acc[4];
-      zero_acc(acc);
-      pipe.run(ops, ld, ks0, nt, acc);
-      store_acc(WsAccess(A, P), acc, nt, c0, r, [&](int t) { return zp + (((size_t)pj * P.nch_z + s) * B + tg + t) * r; });
+    f32x4 acc[4];
+    zero_acc(acc);
+    if (active) pipe.run(ops, ld, ks0, nt, acc);
+    // lane (n, g) holds token rows 4 g + i, columns c0 + 4 n + qq of MFMA qq
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq)
+      *reinterpret_cast<float4*>(red + (w * 64 + l) * 16 + 4 * qq) =
+          make_float4(acc[qq][0], acc[qq][1], acc[qq][2], acc[qq][3]);
+    __syncthreads();
+    // thread (i = w, lane l): token row 4 (l >> 4) + i, columns c0 + 4 (l & 15) .. + 3
+    const int n = l & 15, t = 4 * (l >> 4) + w, col = c0 + 4 * n;
+    if (t < nt && col < r) {
+      float v[4];
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) {
+        float sum = red[(0 * 64 + l) * 16 + 4 * qq + w];
+#pragma unroll
+        for (int ww = 1; ww < 4; ++ww) sum += red[(ww * 64 + l) * 16 + 4 * qq + w];
+        v[qq] = sum;
+      }
+      ws.st4(ws.off(zp + (((size_t)pj * P.nq_z + q) * B + tg + t) * r + col), make_float4(v[0], v[1], v[2], v[3]));
     }
+    __syncthreads();
   }
   set_flag(wsp<int>(A, P.o_zc_flag) + j * kTickPad);
 }
@@ -1214,7 +1256,7 @@ __device__ __forceinline__ void book_store_copies(uint4* cb, uint4 v) {
 // requested at once when every tile starts; large batches).
 // XP (batch 1): the token's x row and z rows were staged into LDS (xpre,
 // zpre) by the workgroup at kernel start, so the tile stages nothing.
-template <int D, bool LATE, int NC, bool XP>
+template <int D, bool LATE, int NC, bool XP, int PDC>
 __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg, int s,
                             bool lr_first, uint4* cbs, uint8_t* smem, const uint4* xpre, const uint4* zpre) {
   const Routing R = expert_of(P, RT, a);
@@ -1236,7 +1278,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
   const int* const slot_tok = RT.slot_tok;
   const float* zsrc = (P.flags & F_Z) ? A.z_out : A.z_in;
 
-  VqPipe<D, 1, kPdGateUp, NC> vq;
+  VqPipe<D, 1, PDC, NC> vq;
   DensePipe<2, kPdDense> lr;
   const int n8x = (x1 - x0) * 4, n8z = (z1 - z0) * 4;  // 8-element groups per token row
   // Activation loads through buffer resources over x [B][H] and z [2][B][r]
@@ -1271,7 +1313,7 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
                                           lw[4] | (lw[5] << 16), lw[6] | (lw[7] << 16));
   };
   constexpr int kRegStage = 2;  // activation groups per thread loaded ahead of the weights
-  const bool lr_late = LATE && !lr_first && x1 - x0 > kPdGateUp;
+  const bool lr_late = LATE && !lr_first && x1 - x0 > PDC;
   if constexpr (XP) {  // one token, one pass: operands already in LDS
     const uint4 bk = book_load<D>(pj ? A.L.cb_up : A.L.cb_gate, P.K);
     __builtin_amdgcn_sched_barrier(0);
@@ -1882,7 +1924,7 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     }
     const int pj = tid / kXpreZGroups, q = tid % kXpreZGroups;
     zv[0] = zv[1] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (pj < 2 && q < nzq) {  // z [2][1][r], written by k_route or given by the caller
+    if (pj < 2 && q < nzq) {  // z [2][1][r], written by k_route's z reduce or given by the caller
       zv[0] = *reinterpret_cast<const float4*>(zsrc + (size_t)pj * P.r + 8 * q);
       zv[1] = *reinterpret_cast<const float4*>(zsrc + (size_t)pj * P.r + 8 * q + 4);
     }
@@ -1932,7 +1974,8 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     if constexpr (MODE == 2)
       item_gateup_dense(P, A, RT, t.a, t.pj, t.cg, t.s, item_smem);
     else
-      item_gateup<D, DNW == 2, NC, XPRE>(P, A, RT, t.a, t.pj, t.cg, t.s, lr_first, cbs, item_smem, xpre, zpre);
+      item_gateup<D, DNW == 2, NC, XPRE, DNW == 2 ? kPdGateUpWide : kPdGateUp>(P, A, RT, t.a, t.pj, t.cg, t.s,
+                                                                          lr_first, cbs, item_smem, xpre, zpre);
     tr.done(A, P, P.n_pre + jp, 4);
   }
   for (; jp < n_gu + n_dn; jp += gridDim.x) {

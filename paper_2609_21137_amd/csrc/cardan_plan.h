@@ -10,9 +10,10 @@
 //
 // Item lists (k_route: router chunks, z items, select, z reduce; k_expert:
 // gate/up, down, combine):
-//   router chunks   (64 hidden rows x 64 experts), float64 partial logits
-//   z items         four waves, each (basis, 64 ranks, split of H): partial
-//                   U^T x on MFMA
+//   router chunks   (64 hidden rows x 64 experts x 4 tokens), float64
+//                   partial logits
+//   z items         (basis, 64 ranks, four consecutive splits of H, one per
+//                   wave): partial U^T x on MFMA, the waves' sums added
 //   select          per token: logits, top-k, gating
 //   z reduce        256 outputs of z = U^T x each
 //   gate/up tiles   (active expert a, gate|up, 256 columns, split of the
@@ -34,7 +35,7 @@
 namespace cardan {
 
 constexpr int kWG = 256;            // threads per workgroup (4 wave64)
-constexpr int kRowsRouter = 64;     // hidden rows per router / shared-projection chunk
+constexpr int kRowsRouter = 64;     // hidden rows per router chunk (16 per wave)
 constexpr int kRouterTok = 4;       // tokens per router chunk item
 constexpr int kColsPerGroup = 256;  // output columns per expert tile (4 waves x 64)
 constexpr int kTokPass = 16;        // token slots per MFMA pass (N of 16x16x32)
@@ -42,6 +43,8 @@ constexpr int kMaxE = 1024, kMaxK = 32, kMaxR = 512, kMaxB = 64;
 constexpr int kPdVq = 16;     // code K-steps in flight per wave (4 B per lane each)
 constexpr int kPdGateUp = 8;  // the same for gate/up tiles: half the bytes requested at once when
                               // every tile starts together, the rest as the first steps complete
+constexpr int kPdGateUpWide = 16;  // gate/up code steps in flight in the large-batch kernel: 4 KB of
+                                   // codes per wave, the bytes in flight HBM needs when every tile streams
 constexpr int kPdDense = 2;   // dense K-steps in flight per wave (4 KB each)
 constexpr int kCombineChunk = 16;  // terms per load batch in the combine
 constexpr int kBookCopies = 4;     // code book copies in LDS of the large-batch expert kernel (d = 8)
@@ -52,6 +55,7 @@ constexpr int kSplitKRed = 4 * 64 * 16 * 4;  // [4 waves][64 lanes][16] float
 // of 8 ranks (r <= 512, zero past r)
 constexpr int kXpreXGroups = 512, kXpreZGroups = 64, kXpreZRow = 2 * kXpreZGroups;
 constexpr int kXpreBytes = (kXpreXGroups + 2 * kXpreZRow) * 16;
+constexpr int kZRed = 4 * 64 * 16 * 4;       // z item: [4 waves][64 lanes][16] float sums
 constexpr int kPdDenseW = 2;       // K-steps in flight per wave of a dense bf16 expert-weight tile
                                    // (measured faster than 3 at batch 1 and 16)
 
@@ -80,7 +84,8 @@ struct Plan {
   int flags;
   int nch_r;      // router chunks of kRowsRouter hidden rows
   int n_eg;       // router expert groups of 64
-  int nch_z;      // splits of H for the shared projection
+  int nch_z;      // splits of H for the shared projection (one wave each)
+  int nq_z;       // z partials per value (nch_z / 4 rounded up: one per z item)
   int z_sep;      // 1 when U_up is a different array from U_gate
   int ncg;        // gate/up column groups (I / 256, rounded up)
   int ns;         // gate/up splits of the joint K axis (H/32 + ceil(r/32) steps)

@@ -40,11 +40,11 @@ size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
 // Dynamic LDS of k_route for a plan.
 size_t lds_route(const Plan& P) {
   const int KSX = P.H / 32;
-  size_t need = (size_t)kTokPass * kRowsRouter * (4 + 4 * 8);          // router chunk
+  size_t need = (size_t)kRouterTok * kRowsRouter * 4 + (size_t)4 * kRouterTok * 64 * 8;  // router chunk
   need = std::max(need, (size_t)kMaxE * 8 + kMaxK * (8 + 8 + 4 + 4) + (size_t)kWG * 8);  // select
   need = std::max(need, (size_t)(kMaxB * kMaxK + 2 * kMaxE + 4) * 4);   // grouping
   if (P.flags & F_Z)
-    need = std::max(need, (size_t)4 * kTokPass * (ks_max(KSX, P.nch_z) * 4 + 1) * 16);
+    need = std::max(need, (size_t)4 * kTokPass * (ks_max(KSX, P.nch_z) * 4 + 1) * 16 + kZRed);
   return round256(need);
 }
 
@@ -73,15 +73,20 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   if (mode == 2) P.r = 0;
   P.S = B * P.k;
   P.max_act = P.E < P.S ? P.E : P.S;
-  P.nch_r = P.H / kRowsRouter;
+  P.nch_r = ceil_div(P.H, kRowsRouter);
   P.n_eg = ceil_div(P.E, 64);
   P.z_sep = z_sep;
-  P.nt_max = std::min(B, kTokPass);
+  // token rows a tile stages per pass: 8 above batch 8 (an expert with more
+  // tokens streams its weights again per pass, rare at these batches), which
+  // keeps the large-batch kernel's operand staging small enough for its
+  // code book copies
+  P.nt_max = B > 8 ? 8 : B;
   // combine tiles of up to B/8 tokens: eight per column group at large
   // batches, so the final gather is spread over more workgroups
   P.tpc = std::min(kTokPass, ceil_div(B, 8));
   const int KSX = P.H / 32, KSZ = ceil_div(P.r, 32), KSD = P.I / 32;
-  P.nch_z = std::max(1, KSX / 2);                  // two K-steps of U per z unit
+  P.nch_z = std::max(1, KSX / 2);                  // two K-steps of U per z unit (one wave)
+  P.nq_z = ceil_div(P.nch_z, 4);                   // four units per z item, summed in LDS
   // Tile sizes: the expected active experts' weight bytes spread over a
   // nominal grid of 512 workgroups (2 per CU), kept between 16 and 64 KB per
   // tile, so small batches run every tile in one round and large ones stream
@@ -176,6 +181,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // workgroup slots (fewer rounds, longer tiles)
   const double items_all = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
   if (mode == 0 && items_all > 2 * 512.0 && P.ncgh > 1 && P.d == 8) P.flags |= F_DN_WIDE;
+
   // Small batches at ranks above 128: B^T u streams more of B than a
   // combine tile primes before its wait, so the tiles shrink to 64 columns
   // with the ranks split over their four waves (each wave's share primed).
@@ -185,9 +191,9 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // so each workgroup stages them once while it builds its routing tables
   if (mode == 0 && B == 1 && P.H <= 8 * kXpreXGroups) P.flags |= F_XPRE;
 
-  const int z_units = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nch_z;
+  const int z_items = (z_sep ? 2 : 1) * ceil_div(P.r, 64) * P.nq_z;
   P.n_rc = (flags & F_ROUTE) ? P.nch_r * P.n_eg * ceil_div(B, kRouterTok) : 0;
-  P.n_zc = (flags & F_Z) ? ceil_div(z_units, 4) : 0;
+  P.n_zc = (flags & F_Z) ? z_items : 0;
   P.n_sel = (flags & F_ROUTE) ? B : 0;
   P.n_zr = (flags & F_Z) ? ceil_div(2 * B * P.r, kWG) : 0;
   P.n_pre = P.n_rc + P.n_zc + P.n_sel + P.n_zr;
@@ -197,7 +203,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // the next call's k_route clears them, so every call on a workspace must
   // find them at the same place.
   P.n_rc_flags = P.nch_r * P.n_eg * ceil_div(kMaxB, kRouterTok);
-  P.n_zc_flags = ceil_div(2 * ceil_div(kMaxR, 64) * P.nch_z, 4);
+  P.n_zc_flags = 2 * ceil_div(kMaxR, 64) * P.nq_z;
   size_t o = 0;
   P.o_ctr = o; o = align256(o + (size_t)C_NUM * kCtrStride * 4);
   P.o_rc_flag = o; o = align256(o + (size_t)P.n_rc_flags * kTickPad * 4);
@@ -205,7 +211,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.o_gu_tick = o; o = align256(o + (size_t)P.E * ceil_div(P.I, kColsPerGroup) * kTickPad * 4);
   P.o_dn_done = o; o = align256(o + (size_t)P.E * (ceil_div(P.H, kColsPerGroup) + 1) * kTickPad * 4);
   P.o_rl = o; o = align256(o + (size_t)P.nch_r * B * P.E * 8);
-  P.o_zp = o; o = align256(o + (size_t)2 * P.nch_z * B * P.r * 4);
+  P.o_zp = o; o = align256(o + (size_t)2 * P.nq_z * B * P.r * 4);
   P.o_z = o; o = align256(o + (size_t)2 * B * P.r * 4);
   P.o_gu = o; o = align256(o + (size_t)P.S * 2 * P.ns * P.I * 4);
   P.o_dn = o; o = align256(o + (size_t)P.nsd * P.S * P.H * 4);

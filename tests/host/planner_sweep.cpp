@@ -62,7 +62,8 @@ static void check_plan(const cardan_shape& s, int B, int z_sep, int flags, Count
   CHECK(P.o_dn_done - P.o_gu_tick >= (size_t)P.E * P.ncg * kTickPad * 4);
   CHECK(P.o_rl - P.o_dn_done >= (size_t)P.E * (P.ncgh + 1) * kTickPad * 4);
   CHECK(P.o_zp - P.o_rl >= (size_t)P.nch_r * B * P.E * 8);
-  CHECK(P.o_z - P.o_zp >= (size_t)2 * P.nch_z * B * P.r * 4);
+  CHECK(P.o_z - P.o_zp >= (size_t)2 * P.nq_z * B * P.r * 4);
+  CHECK(P.nq_z * 4 >= P.nch_z && (P.nq_z - 1) * 4 < P.nch_z);
   CHECK(P.o_gu - P.o_z >= (size_t)2 * B * P.r * 4);
   CHECK(P.o_dn - P.o_gu >= (size_t)P.S * 2 * P.ns * P.I * 4);
   CHECK(P.o_uap - P.o_dn >= (size_t)P.nsd * P.S * P.H * 4);
