@@ -319,9 +319,13 @@ def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache, 
 def time_decode_step(C, torch, w, steps, warmup, layers_cache):
     """The stacked-layer decode step: w.layers MoE layers with independently
     seeded weights (drawn on the device), each layer's output RMS-normalised
-    (bf16) into the next layer's input. The step is captured once as a HIP
-    graph and replayed; eager launches are the fallback. Per-step latency:
-    an event pair around every replay."""
+    (bf16) into the next layer's input. Two forms of the same step, each
+    captured once as a HIP graph and replayed (eager launches are the
+    fallback): the library's decode step (cardan_moe_decode_step: the
+    normalisation inside the next layer's routing kernel, the next layer's
+    shared tensors read ahead; two kernels per layer) and the unfused chain
+    (cardan_moe_layer, then cardan_rmsnorm_bf16: three kernels per layer).
+    Per-step latency: an event pair around every replay."""
     import ctypes
 
     from paper_2609_21137_amd import synth
@@ -329,6 +333,7 @@ def time_decode_step(C, torch, w, steps, warmup, layers_cache):
     B, L = w.B, w.layers
     dls = device_layers(C, torch, w, L, layers_cache)
     structs = [dl.struct() for dl in dls]
+    arr = (C.LayerStruct * L)(*structs)
     x0 = C.bf16_tensor(synth.workload_input(w, 0))
     xa = torch.empty_like(x0)
     xb = torch.empty_like(x0)
@@ -338,7 +343,15 @@ def time_decode_step(C, torch, w, steps, warmup, layers_cache):
     ws = C.new_workspace(shape, B)
     lib = C.lib()
 
-    def one_step(stream):
+    def fused(stream):
+        rc = lib.cardan_moe_decode_step(ctypes.byref(shape), B, L, ctypes.c_void_p(x0.data_ptr()), arr,
+                                        ctypes.c_float(1e-6), ctypes.c_void_p(y.data_ptr()), None,
+                                        ctypes.c_void_p(idx.data_ptr()), ctypes.c_void_p(wt.data_ptr()),
+                                        ctypes.c_void_p(ws.data_ptr()), ws.numel(), ctypes.c_void_p(stream))
+        if rc != 0:
+            raise RuntimeError(lib.cardan_last_error().decode())
+
+    def unfused(stream):
         st = ctypes.c_void_p(stream)
         xin = x0
         for li in range(L):
@@ -356,53 +369,63 @@ def time_decode_step(C, torch, w, steps, warmup, layers_cache):
                 raise RuntimeError(lib.cardan_last_error().decode())
             xin = xout
 
-    stream = torch.cuda.current_stream().cuda_stream
-    for _ in range(max(1, warmup)):
-        one_step(stream)
-    torch.cuda.synchronize()
-    n_act = [len(np.unique(idx[li].cpu().numpy())) for li in range(L)]
-    mode = "hip_graph"
-    try:
-        g = torch.cuda.CUDAGraph()
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            with torch.cuda.graph(g, stream=s):
-                one_step(torch.cuda.current_stream().cuda_stream)
-        torch.cuda.current_stream().wait_stream(s)
-        g.replay()
+    def measure(one_step):
+        stream = torch.cuda.current_stream().cuda_stream
+        for _ in range(max(1, warmup)):
+            one_step(stream)
         torch.cuda.synchronize()
-        run = g.replay
-    except Exception as e:  # capture unsupported here: time the eager launches
-        print(f"[bench] graph capture failed ({e}); timing eager launches", file=sys.stderr)
-        mode = "eager"
-        run = lambda: one_step(stream)  # noqa: E731
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        run()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for a, b in ev:
-        a.record()
-        run()
-        b.record()
-    torch.cuda.synchronize()
-    st = C.workspace_status(ws)
-    if st != 0:
-        raise RuntimeError(f"{w.name}: {st} in-kernel waits gave up")
-    per_step_ms = [a.elapsed_time(b) for a, b in ev]
-    med, lo, hi = bootstrap_ci(per_step_ms)
+        mode = "hip_graph"
+        try:
+            g = torch.cuda.CUDAGraph()
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                with torch.cuda.graph(g, stream=s):
+                    one_step(torch.cuda.current_stream().cuda_stream)
+            torch.cuda.current_stream().wait_stream(s)
+            g.replay()
+            torch.cuda.synchronize()
+            run = g.replay
+        except Exception as e:  # capture unsupported here: time the eager launches
+            print(f"[bench] graph capture failed ({e}); timing eager launches", file=sys.stderr)
+            mode = "eager"
+            run = lambda: one_step(stream)  # noqa: E731
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            run()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for a, b in ev:
+            a.record()
+            run()
+            b.record()
+        torch.cuda.synchronize()
+        st = C.workspace_status(ws)
+        if st != 0:
+            raise RuntimeError(f"{w.name}: {st} in-kernel waits gave up")
+        med, lo, hi = bootstrap_ci([a.elapsed_time(b) for a, b in ev])
+        return mode, wall, med, lo, hi
+
+    mode, wall, med, lo, hi = measure(fused)
+    n_act = [len(np.unique(idx[li].cpu().numpy())) for li in range(L)]
+    _, wall_u, med_u, lo_u, hi_u = measure(unfused)
     bytes_step = sum(compressed_bytes(w, a)["compressed"] for a in n_act)
     return {"workload": w.name, "B": B, "layers": L, "distinct_layers": len(dls), "mode": mode,
+            "form": "cardan_moe_decode_step (normalisation fused into the next routing kernel, "
+                    "next-layer prefetch)",
             "ms_per_step": round(1e3 * wall / steps, 4),
             "ms_per_step_median": round(med, 4), "ms_per_step_ci95": [round(lo, 4), round(hi, 4)],
             "us_per_layer": round(1e6 * wall / steps / L, 3),
             "us_per_layer_median": round(1e3 * med / L, 3),
             "GBps": round(bytes_step * steps / wall / 1e9, 2),
             "bytes_per_step": bytes_step,
-            "mean_active_experts": float(np.mean(n_act))}
+            "mean_active_experts": float(np.mean(n_act)),
+            "unfused_chain": {"ms_per_step": round(1e3 * wall_u / steps, 4),
+                              "ms_per_step_median": round(med_u, 4),
+                              "ms_per_step_ci95": [round(lo_u, 4), round(hi_u, 4)],
+                              "us_per_layer": round(1e6 * wall_u / steps / L, 3)}}
 
 
 def cpu_model() -> str:

@@ -119,7 +119,8 @@ int cardan_abi_version(void);
 const char* cardan_last_error(void);
 
 /* Workspace size in bytes needed by every ws-taking entry point for this
- * shape and any batch up to B (the dense-weight entry points included).
+ * shape and any batch up to B (the dense-weight entry points and the decode
+ * step included).
  * Host-only; no device is touched. */
 int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out);
 
@@ -164,6 +165,27 @@ int cardan_vq_lr_expert_ffn(const cardan_shape* shape, int32_t B, const cardan_b
 int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
                      const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
                      void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* One decode step through n_layers stacked MoE layers (the 48-layer workload
+ * of the paper's Qwen3 decoding, attention omitted): layer 0 reads x0
+ * [B][H] bf16; layer l + 1 reads x_{l+1} = bf16_rne(y_l / sqrt(mean_h(y_l^2)
+ * + eps)) of layer l's output y_l (no learned scale), as cardan_rmsnorm_bf16
+ * would form it; y [B][H] float32 receives the last layer's output. Every
+ * layer is cardan_moe_layer on its own weights layers[l] (Sec. 2.1, Sec. 3.1
+ * Eq. (1), Sec. 4.2), all with the same shape. Per layer l the routing goes
+ * to topk_idx / topk_w [n_layers][B][top_k]; x_norm, if not NULL, receives
+ * the normalised inputs of layers 1..n_layers-1 as [n_layers - 1][B][H] bf16.
+ * The normalisation runs inside the next layer's routing kernel (the layer's
+ * combine writes per-token partial sums of y^2), so a layer costs two kernel
+ * launches; the expert kernel's idle workgroups read the next layer's router
+ * weights, bases and code books ahead of its routing kernel (the paper's
+ * overlap of routing-independent reads, Sec. 4.1). ws: at least
+ * cardan_workspace_bytes(shape, B) bytes; one workspace serves every layer.
+ * 1 <= n_layers <= 4096, eps finite and >= 0. */
+int cardan_moe_decode_step(const cardan_shape* shape, int32_t B, int32_t n_layers, const cardan_bf16* x0,
+                           const cardan_layer* layers, float eps, float* y, cardan_bf16* x_norm,
+                           int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
 
 /* Size of the library's own scratch array, one per GPU (16 MiB). */
 #define CARDAN_SCRATCH_BYTES (16u << 20)

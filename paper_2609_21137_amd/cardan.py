@@ -73,6 +73,8 @@ def _load():
         "cardan_vq_lr_expert_ffn": ([sp, i32, vp, vp, vp, vp, lp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_moe_layer": ([sp, i32, vp, lp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_moe_layer_noalloc": ([sp, i32, vp, lp, vp, vp, vp, vp], ctypes.c_int),
+        "cardan_moe_decode_step": ([sp, i32, i32, vp, lp, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp],
+                                   ctypes.c_int),
         "cardan_moe_layer_dense_down": ([sp, i32, vp, lp, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_dense_moe_layer": ([sp, i32, vp, dp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_rmsnorm_bf16": ([i32, i32, vp, ctypes.c_float, vp, vp], ctypes.c_int),
@@ -91,6 +93,7 @@ _lib = _load()
 EXPORTED = (
     "cardan_abi_version", "cardan_last_error", "cardan_workspace_bytes", "cardan_route_topk",
     "cardan_shared_proj", "cardan_vq_lr_expert_ffn", "cardan_moe_layer", "cardan_moe_layer_noalloc",
+    "cardan_moe_decode_step",
     "cardan_moe_layer_dense_down", "cardan_dense_moe_layer", "cardan_rmsnorm_bf16",
     "cardan_profile_begin", "cardan_profile_end",
 )
@@ -277,6 +280,32 @@ def moe_layer(shape: Shape, x, layer: DeviceLayer, ws=None, out=None, idx=None, 
         _ptr(y, torch.float32, "y", (B, shape.H)),
         _ptr(idx, torch.int32, "topk_idx", (B, shape.top_k)),
         _ptr(w, torch.float32, "topk_w", (B, shape.top_k)),
+        _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(dev)))
+    return y, idx, w
+
+
+def moe_decode_step(shape: Shape, x0, layers, eps: float = 1e-6, ws=None, out=None, x_norm=None,
+                    idx=None, w=None):
+    """``len(layers)`` stacked layers, each output RMS-normalised (bf16) into
+    the next layer's input. Returns ``(y [B, H] of the last layer,
+    topk_idx [L, B, k], topk_w [L, B, k])``; ``x_norm`` (optional,
+    ``[L - 1, B, H]`` bf16) receives the normalised inputs of layers 1..L-1."""
+    B = x0.shape[0]
+    L = len(layers)
+    dev = x0.device
+    y = out if out is not None else torch.empty((B, shape.H), dtype=torch.float32, device=dev)
+    idx = idx if idx is not None else torch.empty((L, B, shape.top_k), dtype=torch.int32, device=dev)
+    w = w if w is not None else torch.empty((L, B, shape.top_k), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = new_workspace(shape, B, dev)
+    structs = (LayerStruct * L)(*[dl.struct() for dl in layers])
+    xn = (_ptr(x_norm, torch.bfloat16, "x_norm", (L - 1, B, shape.H)) if x_norm is not None and L > 1
+          else None)
+    _check(_lib.cardan_moe_decode_step(
+        ctypes.byref(shape), B, L, _ptr(x0, torch.bfloat16, "x0", (B, shape.H)), structs,
+        ctypes.c_float(eps), _ptr(y, torch.float32, "y", (B, shape.H)), xn,
+        _ptr(idx, torch.int32, "topk_idx", (L, B, shape.top_k)),
+        _ptr(w, torch.float32, "topk_w", (L, B, shape.top_k)),
         _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(dev)))
     return y, idx, w
 

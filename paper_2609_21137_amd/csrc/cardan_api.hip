@@ -17,8 +17,8 @@
 namespace cardan {
 const void* route_kernel();
 const void* expert_kernel(int d, int dnw, int mode, bool csk, bool xpre);
-hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
-hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
+hipError_t launch_route(const Plan&, const Args&, const Chain&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
+hipError_t launch_expert(const Plan&, const Args&, const Chain&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t);
 hipError_t launch_rmsnorm(hipStream_t, int, int, const float*, float, uint16_t*, hipEvent_t, hipEvent_t);
@@ -105,6 +105,24 @@ int check_ws(const Plan& P, const void* ws, size_t ws_bytes) {
   return CARDAN_OK;
 }
 
+// Stacked decode step: buffers after the layer's workspace layout: y and the
+// partial sums of squares of two layers (ping-pong), and two normalised bf16
+// inputs (used when the caller keeps none).
+struct StepBufs {
+  size_t o_y, o_ssq, o_x, total;
+};
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+StepBufs step_bufs(const Plan& P) {
+  StepBufs b;
+  size_t o = P.total;
+  b.o_y = o; o = align256(o + (size_t)2 * P.B * P.H * 4);
+  b.o_ssq = o; o = align256(o + (size_t)2 * P.B * combine_col_tiles(P) * 4);
+  b.o_x = o; o = align256(o + (size_t)2 * P.B * P.H * 2);
+  b.total = o;
+  return b;
+}
+
 #define REQ(p, name)                                                                  \
   do {                                                                                \
     if (!(p)) return fail(CARDAN_ERR_NULL_PTR, "%s is NULL", name);                   \
@@ -185,7 +203,10 @@ int hip_fail(hipError_t e, const char* what) {
 
 // Sizes the grids and launches k_route (if the call has routing items) and
 // k_expert (if it has expert work) for one call.
-int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
+int run_layer(const Plan& P, const Args& A, hipStream_t stream, const Chain* chain = nullptr) {
+  Chain none;
+  memset(&none, 0, sizeof none);
+  const Chain& C = chain ? *chain : none;
   if (P.total >= 0x80000000ull)  // workspace offsets must stay below the out-of-range marker
     return fail(CARDAN_ERR_UNSUPPORTED, "workspace layout of %zu bytes exceeds 2 GiB", P.total);
   if (P.lds_route > kLdsMax || P.lds_expert > kLdsMax)
@@ -198,7 +219,7 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
     const int cap = resident_grid(route_kernel(), P.lds_route, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_ROUTE);
-    err = launch_route(P, A, std::max(1, std::min(cap, P.n_pre)), P.lds_route, stream, tm.ev0, tm.ev1);
+    err = launch_route(P, A, C, std::max(1, std::min(cap, P.n_pre)), P.lds_route, stream, tm.ev0, tm.ev1);
     if (err != hipSuccess) return hip_fail(err, "k_route launch");
     tm.done();
     if (!(P.flags & F_EXPERTS)) {  // k_expert would clear these counters
@@ -212,7 +233,7 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream) {
                                   P.lds_expert, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_EXPERT);
-    err = launch_expert(P, A, cap, P.lds_expert, stream, tm.ev0, tm.ev1);
+    err = launch_expert(P, A, C, cap, P.lds_expert, stream, tm.ev0, tm.ev1);
     if (err != hipSuccess) return hip_fail(err, "k_expert launch");
     tm.done();
   }
@@ -300,9 +321,11 @@ int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out) {
   // and every expert-weight form (compressed, dense down, all dense)
   size_t need = 0;
   const int all = F_ROUTE | F_Z | F_GROUP | F_EXPERTS;
-  for (int b = 1; b <= B; ++b)
+  for (int b = 1; b <= B; ++b) {
     for (int form : {0, (int)F_DN_DENSE, F_DN_DENSE | F_GU_DENSE})
       need = std::max(need, make_plan(shape, b, 1, all | form).total);
+    need = std::max(need, step_bufs(make_plan(shape, b, 1, all | F_NORM_IN | F_SSQ_OUT)).total);
+  }
   *out = need;
   return CARDAN_OK;
 }
@@ -402,6 +425,79 @@ int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
   A.z_out = reinterpret_cast<float*>(w + P.o_z);
   A.y = y;
   return run_layer(P, A, stream);
+}
+
+int cardan_moe_decode_step(const cardan_shape* shape, int32_t B, int32_t n_layers, const cardan_bf16* x0,
+                           const cardan_layer* layers, float eps, float* y, cardan_bf16* x_norm,
+                           int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  int rc = check_shape(shape, B);
+  if (rc) return rc;
+  if (n_layers < 1 || n_layers > 4096) return fail(CARDAN_ERR_BAD_SHAPE, "n_layers=%d outside [1, 4096]", n_layers);
+  if (!(eps >= 0.0f) || !isfinite(eps)) return fail(CARDAN_ERR_BAD_SHAPE, "eps must be finite and >= 0");
+  REQ(x0, "x0");
+  REQ(y, "y");
+  REQ(topk_idx, "topk_idx");
+  REQ(topk_w, "topk_w");
+  if (x_norm && misaligned(x_norm)) return fail(CARDAN_ERR_ALIGN, "x_norm is not 16-byte aligned");
+  if (!layers) return fail(CARDAN_ERR_NULL_PTR, "layers is NULL");
+  for (int l = 0; l < n_layers; ++l)
+    if ((rc = check_layer(shape, &layers[l], true))) {
+      char msg[512];
+      snprintf(msg, sizeof msg, "layer %d: %s", l, g_err);
+      return fail(rc, "%s", msg);
+    }
+  const int base = F_ROUTE | F_GROUP | F_EXPERTS | (shape->r > 0 ? F_Z : 0);
+  // every layer's plan has this layout (flags and bases change item counts only)
+  const Plan P0 = make_plan(shape, B, 1, base | F_NORM_IN | F_SSQ_OUT);
+  const StepBufs sb = step_bufs(P0);
+  if ((rc = check_ws(P0, ws, ws_bytes))) return rc;
+  if (ws_bytes < sb.total)
+    return fail(CARDAN_ERR_WORKSPACE, "workspace of %zu bytes < required %zu", ws_bytes, sb.total);
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  float* ybuf[2] = {reinterpret_cast<float*>(w + sb.o_y), reinterpret_cast<float*>(w + sb.o_y) + (size_t)B * shape->H};
+  float* ssq[2] = {reinterpret_cast<float*>(w + sb.o_ssq),
+                   reinterpret_cast<float*>(w + sb.o_ssq) + (size_t)B * combine_col_tiles(P0)};
+  uint16_t* xbuf[2] = {reinterpret_cast<uint16_t*>(w + sb.o_x),
+                       reinterpret_cast<uint16_t*>(w + sb.o_x) + (size_t)B * shape->H};
+  const size_t BH = (size_t)B * shape->H, Bk = (size_t)B * shape->top_k;
+  for (int l = 0; l < n_layers; ++l) {
+    const cardan_layer& L = layers[l];
+    const bool last = l == n_layers - 1;
+    const int z_sep = shape->r > 0 && L.U_up != L.U_gate;
+    const int flags = base | (l > 0 ? F_NORM_IN : 0) | (last ? 0 : F_SSQ_OUT | F_PREFETCH);
+    const Plan P = make_plan(shape, B, z_sep, flags);
+    uint16_t* xin = l == 0 ? nullptr : (x_norm ? x_norm + (size_t)(l - 1) * BH : xbuf[l % 2]);
+    Args A = args_for(&L, w);
+    A.x = l == 0 ? x0 : xin;
+    A.topk_idx = topk_idx + (size_t)l * Bk;
+    A.topk_w = topk_w + (size_t)l * Bk;
+    A.z_out = reinterpret_cast<float*>(w + P.o_z);
+    A.y = last ? y : ybuf[l % 2];
+    Chain C;
+    memset(&C, 0, sizeof C);
+    C.eps = eps;
+    C.nssq = combine_col_tiles(P);
+    if (l > 0) {
+      C.y_in = ybuf[(l - 1) % 2];
+      C.ssq_in = ssq[(l - 1) % 2];
+      C.x_norm = xin;
+    }
+    if (!last) {
+      C.ssq_out = ssq[l % 2];
+      const cardan_layer& N = layers[l + 1];
+      const size_t H = shape->H, E = shape->E, r = shape->r, book = (size_t)shape->K * shape->d * 2;
+      const void* pf[kPrefetchTensors] = {N.router_w, N.U_gate, N.U_up != N.U_gate ? N.U_up : nullptr,
+                                          N.B_down, N.cb_gate, N.cb_up, N.cb_down};
+      const size_t nb[kPrefetchTensors] = {H * E * 2, H * r * 2, H * r * 2, r * H * 2, book, book, book};
+      for (int j = 0; j < kPrefetchTensors; ++j) {
+        C.pf[j] = nb[j] > 0 && nb[j] < 0x80000000ull ? pf[j] : nullptr;
+        C.pf_bytes[j] = C.pf[j] ? (uint32_t)nb[j] : 0;
+      }
+    }
+    if ((rc = run_layer(P, A, stream, &C))) return rc;
+  }
+  return CARDAN_OK;
 }
 
 int cardan_moe_layer_noalloc(const cardan_shape* shape, int32_t B, const cardan_bf16* x,

@@ -249,12 +249,24 @@ __device__ int block_exclusive_scan(int* arr, int n, int* tmp4) {
   return total;
 }
 
+// 1 / rms of token t of the previous layer's output (stacked decode step):
+// its partial sums of squares added in column-tile order, the same value in
+// every item that normalises the token.
+__device__ __forceinline__ float norm_inv(const Plan& P, const Chain& C, int t) {
+  const float* q = C.ssq_in + (size_t)t * C.nssq;
+  float s = 0.0f;
+  for (int i = 0; i < C.nssq; ++i) s += q[i];
+  return 1.0f / sqrtf(s / (float)P.H + C.eps);
+}
+
 // Router chunk (c, g, tb): partial logits over hidden rows [64c, 64c + 64)
 // for experts [64g, 64g + 64) of tokens [4tb, 4tb + 4). Lane l of wave w owns
 // expert 64g + l and rows 64c + 16w .. + 16 (rows past H read zeros); float64
 // FMAs of exact bf16 products in row order per token, then the four waves'
 // partials are added in wave order through LDS.
-__device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c, int g, int tb, uint8_t* smem) {
+static_assert(kRouterTok * kRowsRouter <= kWG, "a router chunk's inputs are one per thread");
+__device__ void item_router_chunk(const Plan& P, const Args& A, const Chain& C, int item, int c, int g, int tb,
+                                  uint8_t* smem) {
   constexpr int RW = kRowsRouter / 4;  // rows per wave
   float* xs = reinterpret_cast<float*>(smem);                                     // [4][64]
   double* part = reinterpret_cast<double*>(smem + kRouterTok * kRowsRouter * 4);  // [4][4][64]
@@ -270,9 +282,31 @@ __device__ void item_router_chunk(const Plan& P, const Args& A, int item, int c,
   }
   double* rl = wsp<double>(A, P.o_rl);
   const int tg = tb * kRouterTok, nt = min(kRouterTok, B - tg);
-  for (int i = tid; i < nt * kRowsRouter; i += kWG) {
-    const int t = i / kRowsRouter, h = i % kRowsRouter;
-    xs[i] = h0 + h < H ? bf(A.x[(size_t)(tg + t) * H + h0 + h]) : 0.0f;
+  if (P.flags & F_NORM_IN) {
+    // x = bf16(y * inv_rms) of the previous layer's output; items of expert
+    // group 0 also write it for the expert kernel. A thread's y value
+    // (nt * 64 <= kWG) loads together with the partial sums behind inv_rms.
+    float* sinv = reinterpret_cast<float*>(part + 4 * kRouterTok * 64);  // [4]
+    const int t = tid / kRowsRouter, h = tid % kRowsRouter;
+    const bool in = t < nt && h0 + h < H;
+    const size_t o = (size_t)(tg + t) * H + h0 + h;
+    const float yv = in ? C.y_in[o] : 0.0f;
+    if (tid < nt) sinv[tid] = norm_inv(P, C, tg + tid);
+    __syncthreads();
+    if (t < nt) {
+      float v = 0.0f;
+      if (in) {
+        const uint32_t b = rne_bf16(yv * sinv[t]);
+        v = bf(b);
+        if (g == 0) C.x_norm[o] = (uint16_t)b;
+      }
+      xs[tid] = v;
+    }
+  } else {
+    for (int i = tid; i < nt * kRowsRouter; i += kWG) {
+      const int t = i / kRowsRouter, h = i % kRowsRouter;
+      xs[i] = h0 + h < H ? bf(A.x[(size_t)(tg + t) * H + h0 + h]) : 0.0f;
+    }
   }
   __syncthreads();
   trace_mark(0);
@@ -1150,7 +1184,7 @@ __device__ __forceinline__ float4 fma4(float w, float4 v, float4 a) {
 // z item j: basis pj, 64 columns of z, and four consecutive K-splits of H,
 // one per wave (split 4q + w); the waves' partial U^T x are added in wave
 // order through LDS and item j stores one partial, zp[pj][q][t][col].
-__device__ void item_z(const Plan& P, const Args& A, int j, uint8_t* smem) {
+__device__ void item_z(const Plan& P, const Args& A, const Chain& C, int j, uint8_t* smem) {
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   const int ncol = (P.r + 63) / 64;
   const int q = j % P.nq_z, rem = j / P.nq_z;
@@ -1165,6 +1199,7 @@ __device__ void item_z(const Plan& P, const Args& A, int j, uint8_t* smem) {
   const int ld = (KS + P.nch_z - 1) / P.nch_z * 4 + 1;
   uint4* ops = reinterpret_cast<uint4*>(smem) + w * kTokPass * ld;
   float* red = reinterpret_cast<float*>(smem + (size_t)4 * kTokPass * ld * 16);  // [4][64][16]
+  float* zinv = red + 4 * 64 * 16;                                                // [16] (F_NORM_IN)
   float* zp = wsp<float>(A, P.o_zp);
   const int B = P.B, H = P.H, r = P.r;
   const WsAccess ws(A, P);
@@ -1172,10 +1207,27 @@ __device__ void item_z(const Plan& P, const Args& A, int j, uint8_t* smem) {
   for (int tg = 0; tg < B; tg += kTokPass) {
     const int nt = min(kTokPass, B - tg);
     if (active) pipe.prime(U, r, c0, r, H, ks0, ks1);
+    if ((P.flags & F_NORM_IN) && tid < nt) zinv[tid] = norm_inv(P, C, tg + tid);
     __syncthreads();
-    if (active)  // this wave's own region: lanes stride by 64
-      stage_bf16(ops, ld, nt, (ks1 - ks0) * 4,
-                 [&](int t) { return A.x + (size_t)(tg + t) * H + ks0 * 32; }, l, 64);
+    if (active) {  // this wave's own region: lanes stride by 64
+      if (P.flags & F_NORM_IN) {
+        // x = bf16(y * inv_rms), as the router chunks form it
+        const int n8 = (ks1 - ks0) * 4;
+        for (int i = l; i < nt * n8; i += 64) {
+          const int t = i / n8, j8 = i % n8;
+          const float4* yr = reinterpret_cast<const float4*>(C.y_in + (size_t)(tg + t) * H + ks0 * 32 + 8 * j8);
+          const float4 a = yr[0], b = yr[1];
+          const float iv = zinv[t];
+          ops[t * ld + j8] = make_uint4(rne_bf16(a.x * iv) | (rne_bf16(a.y * iv) << 16),
+                                        rne_bf16(a.z * iv) | (rne_bf16(a.w * iv) << 16),
+                                        rne_bf16(b.x * iv) | (rne_bf16(b.y * iv) << 16),
+                                        rne_bf16(b.z * iv) | (rne_bf16(b.w * iv) << 16));
+        }
+      } else {
+        stage_bf16(ops, ld, nt, (ks1 - ks0) * 4,
+                   [&](int t) { return A.x + (size_t)(tg + t) * H + ks0 * 32; }, l, 64);
+      }
+    }
     __syncthreads();
     f32x4 acc[4];
     zero_acc(acc);
@@ -1640,7 +1692,8 @@ __device__ void item_down_dense(const Plan& P, const Args& A, const RouteTab& RT
 // split the ranks of B^T u, so each wave's share of B fits its prime before
 // the wait; the waves' accumulators are summed through LDS.
 template <bool LRD, bool SK>
-__device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, int jc, uint8_t* smem) {
+__device__ void item_combine(const Plan& P, const Args& A, const Chain& C, const RouteTab& RT, int jc,
+                             uint8_t* smem) {
   constexpr int NQ4 = SK ? 4 : 1;  // tiles per 256-column group
   constexpr int CW = 64 / NQ4;     // float4 column quads per token row of a tile
   const int cgq = jc % (P.ncgh * NQ4), tq = jc / (P.ncgh * NQ4);
@@ -1659,8 +1712,8 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
   const int* s_slot = RT.tok_slot + t0 * k;  // (t, j) -> slot of the tile's tokens
   const float* s_w_slot = RT.slot_w;
   const int* s_e_slot = RT.slot_e;
-  float4* red = reinterpret_cast<float4*>(smem);                      // [256]
-  float* dnb = reinterpret_cast<float*>(red + kWG);                   // [nt][256] VQ down sums
+  float* ssq = reinterpret_cast<float*>(smem);                        // [16 tokens][64] sums of y^2
+  float* dnb = ssq + kWG * 4;                                         // [nt][256] VQ down sums
   uint4* us = reinterpret_cast<uint4*>(dnb + kTokPass * kColsPerGroup);
   const int ntk = nt * k;
   const int nq = LRD ? KSR * 8 : 8, ld = KSR * 8 + 1;  // (no u rows without LRD)
@@ -1710,7 +1763,8 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
     const bool isu = LRD && unit < nu * cu;
     const int uu = isu ? unit : unit - nu * cu;
     // chunk-major: neighbouring threads read neighbouring quads of one row
-    const int it = isu ? uu % nu : uu % nd, c = isu ? uu / nu : uu / nd;
+    const int nuu = max(nu, 1);  // (no low-rank terms: isu is never set)
+    const int it = isu ? uu % nuu : uu % nd, c = isu ? uu / nuu : uu / nd;
     const int t = isu ? it / nq : it / CW, q = isu ? it % nq : 0;
     const int col = cbase + 4 * (it % CW);
     // the column's (or rank quad's) byte offset within a term's row; a
@@ -1745,6 +1799,9 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
       reinterpret_cast<float4*>(dnb)[(item - nu) / CW * 64 + (item - nu) % CW] = acc;
   }
   trace_mark(3);
+  const bool want_ssq = (P.flags & F_SSQ_OUT) != 0;
+  if (want_ssq)
+    for (int i = tid; i < kTokPass * 64; i += kWG) ssq[i] = 0.0f;
   __syncthreads();
   trace_mark(0);
   if (SK && r > 0) {
@@ -1770,6 +1827,7 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
         v[q] = sum;
       }
       *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + cbase + 4 * n) = make_float4(v[0], v[1], v[2], v[3]);
+      if (want_ssq) ssq[t * 64 + n] = v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
     }
   } else if (r > 0) {
     // y = VQ sums + B^T u, written from the accumulators: token rows 4g + i,
@@ -1785,16 +1843,29 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
       const int t = 4 * g + i;
       if (t < nt && cbase + c < H) {
         const float4 d = *reinterpret_cast<const float4*>(dnb + t * kColsPerGroup + c);
-        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + cbase + c) =
-            make_float4(d.x + acc[0][i], d.y + acc[1][i], d.z + acc[2][i], d.w + acc[3][i]);
+        const float4 v = make_float4(d.x + acc[0][i], d.y + acc[1][i], d.z + acc[2][i], d.w + acc[3][i]);
+        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + cbase + c) = v;
+        if (want_ssq) ssq[t * 64 + w * 16 + n] = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
       }
     }
   } else {
     for (int i = tid; i < nt * CW; i += kWG) {
       const int t = i / CW, col = cbase + 4 * (i % CW);
-      if (col < H)
-        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) =
-            reinterpret_cast<const float4*>(dnb)[t * 64 + i % CW];
+      if (col < H) {
+        const float4 v = reinterpret_cast<const float4*>(dnb)[t * 64 + i % CW];
+        *reinterpret_cast<float4*>(A.y + (size_t)(t0 + t) * H + col) = v;
+        if (want_ssq) ssq[t * 64 + i % CW] = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+      }
+    }
+  }
+  if (want_ssq) {
+    // this column tile's sum of y^2 per token, in thread-slot order, for the
+    // next layer's RMS normalisation
+    __syncthreads();
+    if (tid < nt) {
+      float sum = 0.0f;
+      for (int i = 0; i < 64; ++i) sum += ssq[tid * 64 + i];
+      C.ssq_out[(size_t)(t0 + tid) * C.nssq + cgq] = sum;
     }
   }
 }
@@ -1802,12 +1873,13 @@ __device__ void item_combine(const Plan& P, const Args& A, const RouteTab& RT, i
 // ===========================================================================
 // the two persistent kernels of a layer call
 // ===========================================================================
-// Brings the 7 64-byte lines of the kernel arguments (Plan, then Args) into
+// Brings the 9 64-byte lines of the kernel arguments (Plan, Args, Chain) into
 // the scalar cache with loads issued back to back and one wait, so the
 // fields read later hit instead of missing one line at a time. One asm
 // statement: the loads' destinations are clobbered until the wait.
-static_assert(sizeof(Plan) + sizeof(Args) > 6 * 64 && sizeof(Plan) + sizeof(Args) <= 7 * 64,
-              "kernel arguments span 7 lines; update warm_kernargs");
+static_assert(sizeof(Plan) + sizeof(Args) + sizeof(Chain) > 8 * 64 &&
+                  sizeof(Plan) + sizeof(Args) + sizeof(Chain) <= 9 * 64,
+              "kernel arguments span 9 lines; update warm_kernargs");
 __device__ __forceinline__ void warm_kernargs() {
 #if __HIP_DEVICE_COMPILE__
   asm volatile(
@@ -1818,8 +1890,10 @@ __device__ __forceinline__ void warm_kernargs() {
       "s_load_dword s94, %0, 0x100\n\t"
       "s_load_dword s95, %0, 0x140\n\t"
       "s_load_dword s96, %0, 0x180\n\t"
+      "s_load_dword s97, %0, 0x1c0\n\t"
+      "s_load_dword s98, %0, 0x200\n\t"
       "s_waitcnt lgkmcnt(0)" ::"s"(__builtin_amdgcn_kernarg_segment_ptr())
-      : "s90", "s91", "s92", "s93", "s94", "s95", "s96", "memory");
+      : "s90", "s91", "s92", "s93", "s94", "s95", "s96", "s97", "s98", "memory");
 #endif
 }
 
@@ -1832,9 +1906,30 @@ __device__ __forceinline__ void clear_ints(int* p, int n, int stride = 1) {
   for (int i = threadIdx.x; i < n; i += kWG) p[i * stride] = 0;
 }
 
+// Stacked decode step: a workgroup whose items are done reads its share
+// (part of parts) of
+// the next layer's routing-independent shared tensors (router weights, bases,
+// code books), so the next layer's route kernel finds them in the last-level
+// cache. One 4-byte load per 128-byte line; the loaded words only feed a
+// barrier vote (which, if it ever held, would count into the sink counter).
+__device__ void prefetch_next_layer(const Args& A, const Chain& C, int part, int parts) {
+  unsigned acc = 0;
+  for (int j = 0; j < kPrefetchTensors; ++j) {
+    const uint32_t n = C.pf_bytes[j];
+    if (!C.pf[j] || n == 0) continue;
+    const uint32_t lines = (n + 127) / 128;
+    const uint32_t l0 = (uint32_t)((uint64_t)lines * part / parts);
+    const uint32_t l1 = (uint32_t)((uint64_t)lines * (part + 1) / parts);
+    const rsrc_t rs = make_rsrc(C.pf[j], n);
+    for (uint32_t li = l0 + threadIdx.x; li < l1; li += kWG)
+      acc ^= __builtin_amdgcn_raw_buffer_load_b32(rs, li * 128, 0, 0);
+  }
+  if (__syncthreads_or(acc == 0x5EED5EEDu) && threadIdx.x == 0) atomicAdd(ctr(A, C_SINK), 1);
+}
+
 // Routing-independent work and the routing itself: router chunks, z units,
 // per-token select (the last one groups the slots), z reduce.
-__global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
+__global__ __launch_bounds__(kWG) void k_route(Plan P, Args A, Chain C) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   warm_kernargs();
   if (blockIdx.x == 0 && (P.flags & F_EXPERTS)) {
@@ -1848,13 +1943,13 @@ __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A) {
     __syncthreads();
     ItemTrace tr;
     const int nrt = P.nch_r * P.n_eg, jr = j % nrt;
-    item_router_chunk(P, A, j, jr % P.nch_r, jr / P.nch_r, j / nrt, smem);
+    item_router_chunk(P, A, C, j, jr % P.nch_r, jr / P.nch_r, j / nrt, smem);
     tr.done(A, P, j, 0);
   }
   for (; j < e_zc; j += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
-    item_z(P, A, j - e_rc, smem);
+    item_z(P, A, C, j - e_rc, smem);
     tr.done(A, P, j, 1);
   }
   for (; j < e_sel; j += gridDim.x) {
@@ -1886,7 +1981,7 @@ __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
 // XPRE (batch 1): the token's x and z rows are loaded at kernel start, while
 // the routing tables build, into an LDS area at the end of dynamic LDS.
 template <int D, int DNW, int MODE, bool CSK, bool XPRE>
-__global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A) {
+__global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A, Chain C) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   // the code book of the current item (zero-padded to 256 words), in
   // kBookCopies copies in the large-batch kernel
@@ -1998,8 +2093,15 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
   for (; jp < n_items; jp += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
-    item_combine<MODE == 0, CSK>(P, A, RT, jp - n_gu - n_dn, item_smem);
+    item_combine<MODE == 0, CSK>(P, A, C, RT, jp - n_gu - n_dn, item_smem);
     tr.done(A, P, P.n_pre + jp, 7);
+  }
+  // the next layer's shared tensors, read by the workgroups that run no
+  // combine (they finish while the combine tiles run)
+  if (P.flags & F_PREFETCH) {
+    const int G = gridDim.x, n_pf = G - min(P.n_cb, G);
+    const int rank = ((int)blockIdx.x - (n_gu + n_dn) % G - min(P.n_cb, G) + 2 * G) % G;
+    if (n_pf > 0 && rank < n_pf) prefetch_next_layer(A, C, rank, n_pf);
   }
 }
 
@@ -2089,9 +2191,9 @@ const void* expert_kernel(int d, int dnw, int mode, bool csk, bool xpre) {
       hipLaunchKernelGGL(kernel, dim3(grid), dim3(kWG), lds, st, __VA_ARGS__);                    \
   } while (0)
 
-hipError_t launch_route(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st, hipEvent_t ev0,
-                        hipEvent_t ev1) {
-  CARDAN_LAUNCH(k_route, grid, lds, st, ev0, ev1, P, A);
+hipError_t launch_route(const Plan& P, const Args& A, const Chain& C, int grid, size_t lds, hipStream_t st,
+                        hipEvent_t ev0, hipEvent_t ev1) {
+  CARDAN_LAUNCH(k_route, grid, lds, st, ev0, ev1, P, A, C);
   return hipGetLastError();
 }
 
@@ -2100,14 +2202,15 @@ hipError_t launch_route_reset(const Plan& P, const Args& A, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_expert(const Plan& P, const Args& A, int grid, size_t lds, hipStream_t st, hipEvent_t ev0,
-                         hipEvent_t ev1) {
+hipError_t launch_expert(const Plan& P, const Args& A, const Chain& C, int grid, size_t lds, hipStream_t st,
+                         hipEvent_t ev0, hipEvent_t ev1) {
   // the instantiation expert_kernel() names, launched with its own arguments
   const void* fn = expert_kernel(P.d, dn_width(P), expert_mode(P), (P.flags & F_CB_SPLITK) != 0,
                                  (P.flags & F_XPRE) != 0);
   Plan p = P;
   Args a = A;
-  void* args[] = {&p, &a};
+  Chain c = C;
+  void* args[] = {&p, &a, &c};
   if (ev0) return hipExtLaunchKernel(fn, dim3(grid), dim3(kWG), args, lds, st, ev0, ev1, 0);
   return hipLaunchKernel(fn, dim3(grid), dim3(kWG), args, lds, st);
 }

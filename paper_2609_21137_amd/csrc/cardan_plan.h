@@ -69,11 +69,17 @@ enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8,
        // (r = 0)
        F_DN_DENSE = 32, F_GU_DENSE = 64,
        F_CB_SPLITK = 128,  // set by the plan: combine tiles of 64 columns, ranks split over the waves
-       F_XPRE = 256 };     // set by the plan (batch 1): x and z staged once per workgroup
+       F_XPRE = 256,       // set by the plan (batch 1): x and z staged once per workgroup
+       // stacked decode step (Chain below): the layer's input is the previous
+       // layer's output y, RMS-normalised by the route kernel, which also
+       // writes it as bf16 x for the expert kernel
+       F_NORM_IN = 1024,
+       F_SSQ_OUT = 2048,   // combine tiles write per-token partial sums of y^2 for the next layer
+       F_PREFETCH = 4096 };  // idle expert-kernel workgroups touch the next layer's shared tensors
 
 // counters at the start of the workspace, one per 64-byte slot: the status
 // count of timed-out waits
-enum { C_ERR = 0, C_NUM };
+enum { C_ERR = 0, C_SINK = 1, C_NUM };  // C_SINK: where prefetch loads are folded into one store
 constexpr int kCtrStride = 16;      // ints between counters
 constexpr int kTickPad = 32;        // ints between the tile counters (one 128-byte line each)
 
@@ -207,5 +213,25 @@ struct Args {
   float* y;               // [B][H]
   uint8_t* ws;
 };
+
+// Stacked decode step: how a layer call chains to its neighbours (unused,
+// all zero, for a single layer).
+constexpr int kPrefetchTensors = 7;
+struct Chain {
+  const float* y_in;     // F_NORM_IN: previous layer's y [B][H]
+  const float* ssq_in;   // F_NORM_IN: its partial sums of squares [B][nssq]
+  uint16_t* x_norm;      // F_NORM_IN: the normalised input, written as bf16 [B][H]
+  float* ssq_out;        // F_SSQ_OUT: this layer's partial sums of squares [B][nssq]
+  float eps;             // RMS normalisation epsilon
+  int nssq;              // partial sums per token (the combine's column tiles)
+  const void* pf[kPrefetchTensors];        // F_PREFETCH: next layer's shared tensors
+  uint32_t pf_bytes[kPrefetchTensors];
+};
+
+// Combine column tiles per token row (each writes one partial sum of squares
+// under F_SSQ_OUT).
+__host__ __device__ inline int combine_col_tiles(const Plan& P) {
+  return P.ncgh * ((P.flags & F_CB_SPLITK) ? 4 : 1);
+}
 
 }  // namespace cardan

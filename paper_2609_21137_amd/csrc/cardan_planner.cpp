@@ -40,11 +40,11 @@ size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
 // Dynamic LDS of k_route for a plan.
 size_t lds_route(const Plan& P) {
   const int KSX = P.H / 32;
-  size_t need = (size_t)kRouterTok * kRowsRouter * 4 + (size_t)4 * kRouterTok * 64 * 8;  // router chunk
+  size_t need = (size_t)kRouterTok * kRowsRouter * 4 + (size_t)4 * kRouterTok * 64 * 8 + 16;  // router chunk
   need = std::max(need, (size_t)kMaxE * 8 + kMaxK * (8 + 8 + 4 + 4) + (size_t)kWG * 8);  // select
   need = std::max(need, (size_t)(kMaxB * kMaxK + 2 * kMaxE + 4) * 4);   // grouping
   if (P.flags & F_Z)
-    need = std::max(need, (size_t)4 * kTokPass * (ks_max(KSX, P.nch_z) * 4 + 1) * 16 + kZRed);
+    need = std::max(need, (size_t)4 * kTokPass * (ks_max(KSX, P.nch_z) * 4 + 1) * 16 + kZRed + kTokPass * 4);
   return round256(need);
 }
 

@@ -9,10 +9,10 @@
 namespace cardan {
 const void* route_kernel() { return nullptr; }
 const void* expert_kernel(int, int, int, bool, bool) { return nullptr; }
-hipError_t launch_route(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t) {
+hipError_t launch_route(const Plan&, const Args&, const Chain&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t) {
   return hipErrorInvalidDeviceFunction;
 }
-hipError_t launch_expert(const Plan&, const Args&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t) {
+hipError_t launch_expert(const Plan&, const Args&, const Chain&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t) {
   return hipErrorInvalidDeviceFunction;
 }
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t) { return hipErrorInvalidDeviceFunction; }

@@ -1,0 +1,123 @@
+"""The stacked decode step as one library call (cardan_moe_decode_step): the
+RMS normalisation between layers runs inside the next layer's routing
+kernel and the next layer's shared tensors are read ahead.
+
+Parity is teacher-forced per layer, as for the unfused chain: the oracle for
+layer l takes the step's own normalised input x_l (returned in x_norm), so a
+last-bit difference cannot flip a later top-k and hide as a large error.
+Per layer: top-k identical (after the oracle's margin check), affinities
+within 1e-5; the last layer's y within the 2e-2 bar and the 1e-4 headroom
+bar; every x_{l+1} within one bf16 step (relative) plus the headroom bar
+(normwise) of the oracle's RMSNorm of the oracle's y_l. A one-layer step equals cardan_moe_layer bit for bit; the step
+without x_norm equals the step with it; graph replays equal the eager call.
+"""
+
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.cardan_oracle as O
+from paper_2609_21137_amd import synth
+from paper_2609_21137_amd.configs import QWEN3_48L_B16, TINY
+
+pytestmark = pytest.mark.gpu
+
+EPS = 1e-6
+
+
+@pytest.fixture(scope="module")
+def C():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_21137_amd import cardan
+    return cardan
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.mark.parametrize("wname,n_layers", [("qwen3_b16", 3), ("tiny_b5", 4)])
+def test_decode_step_teacher_forced(C, wname, n_layers):
+    base = QWEN3_48L_B16 if wname == "qwen3_b16" else dataclasses.replace(TINY, B=5)
+    w = dataclasses.replace(base, layers=n_layers)
+    B, H = w.B, w.H
+    shape = C.shape_of(w)
+    _say(f"[decode-step] {wname}: {n_layers} layers H={H} I={w.I} E={w.E} B={B}")
+    Ls = [synth.workload_layer(w, li) for li in range(n_layers)]
+    DLs = [C.DeviceLayer.from_numpy(L) for L in Ls]
+    x0_bits = synth.workload_input(w, 0)
+    x0 = C.bf16_tensor(x0_bits)
+    ws = C.new_workspace(shape, B)
+    xn = torch.empty((n_layers - 1, B, H), dtype=torch.bfloat16, device="cuda")
+    y, idx, wt = C.moe_decode_step(shape, x0, DLs, EPS, ws=ws, x_norm=xn)
+    torch.cuda.synchronize()
+    assert C.workspace_status(ws) == 0
+    y_gpu = y.cpu().numpy().astype(np.float64)
+    idx_gpu, wt_gpu = idx.cpu().numpy(), wt.cpu().numpy()
+    xs = [x0_bits] + [C.bf16_bits(xn[l]) for l in range(n_layers - 1)]
+    for li in range(n_layers):
+        y_ref, idx_ref, a_ref, margin = O.moe_layer_factored(xs[li], Ls[li], w.top_k, w.d)
+        assert np.all(margin > 1e-9), (li, margin.min())
+        assert np.array_equal(idx_gpu[li], idx_ref), li
+        assert np.abs(wt_gpu[li] - a_ref).max() <= 1e-5, li
+        if li + 1 < n_layers:
+            # x_{l+1} against the oracle's RMSNorm of the oracle's y_l: one
+            # bf16 rounding (half a step relative, at most one step where the
+            # two sides round apart) plus y's own error carried through the
+            # normalisation, held to the 1e-4 headroom bar of the outputs
+            xn_ref = O.rmsnorm(y_ref, EPS)
+            x_gpu = O.bf16_to_f64(xs[li + 1])
+            dev = np.abs(x_gpu - xn_ref)
+            bound = 2.0 ** -8 * np.abs(xn_ref) + 1e-4 * np.abs(xn_ref).max()
+            _say(f"[decode-step] layer {li}: x_next max |dx| {dev.max():.3e} "
+                 f"(max |x| {np.abs(xn_ref).max():.3f}), margin {margin.min():.3e}")
+            assert np.all(dev <= bound), (li, (dev - bound).max())
+        else:
+            err = np.abs(y_gpu - y_ref).max() / np.abs(y_ref).max()
+            _say(f"[decode-step] last layer normalised max error {err:.3e}")
+            assert err <= 2e-2 and err <= 1e-4, err
+
+    # the same step without x_norm (internal buffers) gives the same outputs
+    ws2 = C.new_workspace(shape, B)
+    y2, idx2, wt2 = C.moe_decode_step(shape, x0, DLs, EPS, ws=ws2)
+    torch.cuda.synchronize()
+    assert torch.equal(y2, y) and torch.equal(idx2, idx) and torch.equal(wt2, wt)
+
+    # HIP graph replays reproduce the eager call bit for bit
+    yg = torch.empty_like(y)
+    ig = torch.empty_like(idx)
+    wg = torch.empty_like(wt)
+    xg = torch.empty_like(xn)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            C.moe_decode_step(shape, x0, DLs, EPS, ws=ws2, out=yg, x_norm=xg, idx=ig, w=wg)
+    torch.cuda.current_stream().wait_stream(s)
+    for rep in range(3):
+        for t in (yg, xg):
+            t.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert C.workspace_status(ws2) == 0
+        assert torch.equal(yg, y) and torch.equal(xg, xn), rep
+        assert torch.equal(ig, idx) and torch.equal(wg, wt), rep
+
+
+def test_one_layer_step_is_the_layer(C):
+    w = QWEN3_48L_B16
+    shape = C.shape_of(w)
+    L = synth.workload_layer(w, 0)
+    DL = C.DeviceLayer.from_numpy(L)
+    x = C.bf16_tensor(synth.workload_input(w, 0, step=3))
+    y1, i1, w1 = C.moe_decode_step(shape, x, [DL], EPS)
+    y0, i0, w0 = C.moe_layer(shape, x, DL)
+    torch.cuda.synchronize()
+    assert torch.equal(i1[0], i0) and torch.equal(w1[0], w0)
+    assert torch.equal(y1, y0)
