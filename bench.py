@@ -48,9 +48,11 @@ def parse():
     ap.add_argument("--workload", default="qwen3_30b_a3b_moe_layer_b1")
     ap.add_argument("--also", default="qwen3_30b_a3b_moe_layer_b16,wide_h4096_i1536_e64_top6_b4_skewed,"
                     "qwen3_48_layer_decode_step_b16,deepseek_v2_lite_moe_layer_b1,"
-                    "olmoe_1b_7b_moe_layer_b1,gemma4_26b_a4b_moe_layer_b1",
+                    "olmoe_1b_7b_moe_layer_b1,gemma4_26b_a4b_moe_layer_b1,"
+                    "nemotron3_nano_moe_layer_b1,nemotron3_nano_moe_layer_b16",
                     help="comma-separated extra workloads timed the same way (reported under 'also')")
-    ap.add_argument("--dense", default="qwen3_30b_a3b_moe_layer_b1,qwen3_30b_a3b_moe_layer_b16",
+    ap.add_argument("--dense", default="qwen3_30b_a3b_moe_layer_b1,qwen3_30b_a3b_moe_layer_b16,"
+                    "nemotron3_nano_moe_layer_b1,nemotron3_nano_moe_layer_b16",
                     help="workloads also timed with dense bf16 expert weights (the uncompressed "
                          "layer and the dense-down layer) on the same routing and inputs")
     ap.add_argument("--sweep", action="store_true",
@@ -88,19 +90,26 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def n_proj(w) -> int:
+    """Input-side projections per expert: gate and up, or up alone."""
+    return 1 if w.act == "relu2_up" else 2
+
+
 def compressed_bytes(w, n_active: int, z_sep: bool = False) -> dict:
     """Algorithmic bytes of one step: what the method must read at least once.
 
     Per active expert: gate and up codes (H*I/d bytes each) and coefficients
     V (r*I bf16 each); down codes (I*H/d) and A (I*r bf16). Shared: the basis
     U (one per projection when separate), the output basis B and three code
-    books. The router weights are counted separately.
+    books. Up-only experts have no gate codes, coefficients or code book.
+    The router weights are counted separately.
     """
-    per_gateup = 2 * (w.H * w.I // w.d) + 2 * (w.r * w.I * 2)
+    npj = n_proj(w)
+    per_gateup = npj * (w.H * w.I // w.d) + npj * (w.r * w.I * 2)
     per_down = (w.I * w.H // w.d) + (w.I * w.r * 2)
     basis_u = (2 if z_sep else 1) * w.H * w.r * 2
     basis_b = w.r * w.H * 2
-    codebooks = 3 * w.K * w.d * 2
+    codebooks = (npj + 1) * w.K * w.d * 2
     router = w.H * w.E * 2 + w.E * 4
     return {"compressed": n_active * (per_gateup + per_down) + basis_u + basis_b + codebooks,
             "expert_kernel": n_active * (per_gateup + per_down) + basis_b + codebooks,
@@ -115,7 +124,7 @@ def dense_bytes(w, n_active: int, form: str) -> dict:
     router = w.H * w.E * 2 + w.E * 4
     dn = w.I * w.H * 2
     if form == "dense":
-        expert = n_active * (2 * w.H * w.I * 2 + dn)
+        expert = n_active * (n_proj(w) * w.H * w.I * 2 + dn)
         return {"weights": expert, "expert_kernel": expert, "route_kernel": router}
     gu = 2 * (w.H * w.I // w.d) + 2 * (w.r * w.I * 2)
     expert = n_active * (gu + dn) + 2 * w.K * w.d * 2
@@ -141,11 +150,14 @@ def dense_weights(torch, w, n_layers, dense_cache, form):
     (``synth_device``; drawing 1.2 GB per layer on the host would dominate
     the run)."""
     from paper_2609_21137_amd import synth_device
-    key = (w.H, w.I, w.E, w.seed, form)
+    key = (w.H, w.I, w.E, w.seed, form, w.act)
     if key not in dense_cache:
         dense_cache.clear()
         torch.cuda.empty_cache()
-        names = ("W_gate", "W_up", "W_down") if form == "dense" else ("W_down",)
+        if form == "dense":
+            names = (("W_gate",) if n_proj(w) == 2 else ()) + ("W_up", "W_down")
+        else:
+            names = ("W_down",)
         dense_cache[key] = [synth_device.dense_tensors(w, li, names) for li in range(n_layers)]
     return dense_cache[key]
 
@@ -156,7 +168,7 @@ MALL_BYTES = 256 << 20
 def device_layers(C, torch, w, n_layers, layers_cache):
     """``n_layers`` independently seeded layers of workload ``w`` on the device."""
     from paper_2609_21137_amd import synth_device
-    key = (w.H, w.I, w.E, w.d, w.K, w.r, w.seed, w.hot_experts, w.hot_bias)
+    key = (w.H, w.I, w.E, w.d, w.K, w.r, w.seed, w.hot_experts, w.hot_bias, w.act)
     have = layers_cache.get(key, [])
     if len(have) < n_layers:
         if not have:
@@ -204,9 +216,11 @@ def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache, 
 
     # routing (hence the active-expert count) is fixed per (layer, input)
     # and the same in every form (the router weights are the layer's)
+    up_only = w.act == "relu2_up"
+    layer_call = C.moe_layer_relu2 if up_only else C.moe_layer
     n_act = []
     for j in range(n_inputs):
-        C.moe_layer(shape, xs[j], dls[j % n_layers], ws=ws, out=y, idx=idx, w=wt)
+        layer_call(shape, xs[j], dls[j % n_layers], ws=ws, out=y, idx=idx, w=wt)
         torch.cuda.synchronize()
         n_act.append(len(np.unique(idx.cpu().numpy())))
 
@@ -217,7 +231,7 @@ def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache, 
                  ctypes.c_void_p(wt.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(), stream)
     B = w.B
     if form == "compressed":
-        fn = lib.cardan_moe_layer
+        fn = lib.cardan_moe_layer_relu2 if up_only else lib.cardan_moe_layer
         ptrs = [(ctypes.c_void_p(xs[j].data_ptr()), structs[j % n_layers]) for j in range(n_inputs)]
 
         def call(xp, st):
@@ -232,10 +246,11 @@ def time_workload(C, torch, w, steps, warmup, n_layers, n_inputs, layers_cache, 
         def call(xp, st):
             return fn(ctypes.byref(shape), B, xp, ctypes.byref(st[0]), st[1], *args_tail)
     else:
-        fn = lib.cardan_dense_moe_layer
+        fn = lib.cardan_dense_moe_layer_relu2 if up_only else lib.cardan_dense_moe_layer
         mats = dense_weights(torch, w, n_layers, dense_cache, form)
         dstructs = [C.DenseLayer({"router_w": dls[li].tensors["router_w"],
-                                  "router_bias": dls[li].tensors["router_bias"], **mats[li]}).struct(shape)
+                                  "router_bias": dls[li].tensors["router_bias"], **mats[li]}).struct(
+                                      shape, up_only=up_only)
                     for li in range(n_layers)]
         ptrs = [(ctypes.c_void_p(xs[j].data_ptr()), dstructs[j % n_layers]) for j in range(n_inputs)]
 
@@ -640,7 +655,9 @@ def main():
     by_name = {main_sum["workload"]: main_sum, **{a["workload"]: a for a in also}}
     for name in [s for s in args.dense.split(",") if s]:
         ww = WORKLOADS[name]
-        for form, suffix in (("dense", "_dense_bf16"), ("dense_down", "_dense_down")):
+        # the dense-down form has gate and up projections (no up-only variant)
+        forms = (("dense", "_dense_bf16"),) + (() if ww.act == "relu2_up" else (("dense_down", "_dense_down"),))
+        for form, suffix in forms:
             print(f"[bench] {ww.name} ({form})", file=sys.stderr, flush=True)
             rr = time_workload(C, torch, ww, args.steps, args.warmup, args.layers, args.inputs, cache,
                                form=form, dense_cache=dense_cache)

@@ -166,6 +166,17 @@ int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
                      const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
                      void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* The whole layer with up-only experts and a squared-ReLU activation (the
+ * expert form of the paper's Nemotron-3 model, Table 2 "up" and the fidelity
+ * test of Sec. 5.7): routing and z = U_up^T x as cardan_moe_layer, then for
+ * every (token, selected expert) u = VQ gather sum + V_up^T z, p =
+ * max(u, 0)^2, the down output Q^T p + B^T (A^T p), and the weighted combine.
+ * The gate fields of `layer` (cb_gate, codes_gate, U_gate, V_gate) are not
+ * read and may be NULL. Outputs, workspace and errors as cardan_moe_layer. */
+int cardan_moe_layer_relu2(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                           const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* One decode step through n_layers stacked MoE layers (the 48-layer workload
  * of the paper's Qwen3 decoding, attention omitted): layer 0 reads x0
  * [B][H] bf16; layer l + 1 reads x_{l+1} = bf16_rne(y_l / sqrt(mean_h(y_l^2)
@@ -241,6 +252,13 @@ int cardan_moe_layer_dense_down(const cardan_shape* shape, int32_t B, const card
 int cardan_dense_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
                            const cardan_dense_layer* layer, float* y, int32_t* topk_idx,
                            float* topk_w, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The uncompressed layer with up-only squared-ReLU experts (Table 2, "up"):
+ * as cardan_dense_moe_layer with p = max(W_up[e]^T x, 0)^2; W_gate is not
+ * read (may be NULL). */
+int cardan_dense_moe_layer_relu2(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                                 const cardan_dense_layer* layer, float* y, int32_t* topk_idx,
+                                 float* topk_w, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* RMS normalisation between stacked layers: x_next[t][h] =
  * bf16_rne(y[t][h] / sqrt(mean_h y[t][h]^2 + eps)), no learned scale.

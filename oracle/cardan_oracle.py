@@ -26,7 +26,11 @@ Readings where the paper is silent (recorded with the rest in the design doc):
 * The down projection is compressed as ``Q_e + A_e B`` with ``B`` [r, H]
   shared on the output side (the workload definition; the paper itself keeps
   down in BF16, Sec. 3.1).
-* ``phi`` is SiLU gating: ``p = silu(g) * u``.
+* ``phi`` is SiLU gating: ``p = silu(g) * u`` (``act="silu_glu"``), or, for
+  the up-only experts of the paper's Nemotron-3 row (Table 2, projection
+  "up"; the squared-ReLU experts of its fidelity test, Sec. 5.7), the squared
+  ReLU of the up projection alone, ``p = max(u, 0)^2`` (``act="relu2_up"``;
+  the gate tensors are then absent and never read).
 * Top-k order is descending logit with exact ties going to the lower expert
   index; the bias is part of the logit; gating is a softmax over the k
   selected logits.
@@ -45,6 +49,9 @@ Functions:
 * ``moe_layer_dense_down`` -- compressed gate/up (Eq. (1)) with the down
                               projection kept as a dense bf16 matrix, the
                               paper's own setting (Sec. 3.1).
+
+The first four take ``act`` (``"silu_glu"`` or ``"relu2_up"``), the expert
+activation.
 
 All bf16 inputs arrive as raw uint16 bit patterns and are widened exactly.
 """
@@ -154,19 +161,27 @@ def decode_vq(codes, codebook, d: int) -> np.ndarray:
     return blocks.transpose(0, 2, 1).reshape(nb * d, n_out)
 
 
-def expert_matrices(layer: dict, e: int, d: int):
+def _rank(layer: dict) -> int:
+    """Rank r of the layer's shared basis (0 without a low-rank term)."""
+    U = layer.get("U_up")
+    return 0 if U is None else _f(U).shape[1]
+
+
+def expert_matrices(layer: dict, e: int, d: int, act: str = "silu_glu"):
     """Dense reconstructions of expert ``e``'s gate, up and down matrices.
 
     Gate/up follow Eq. (1): ``W = Q_B(J_e) + D C_e`` with ``D = U`` [H, r]
     and ``C_e = V_e`` [r, I], giving [H, I]. Down is ``Q_B(J^d_e) + A_e B``
     with ``A_e`` [I, r] private and ``B`` [r, H] shared, giving [I, H].
+    Up-only experts (``act="relu2_up"``) have no gate matrix (``None``).
     """
-    Wg = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d)
+    gated = act == "silu_glu"
+    Wg = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d) if gated else None
     Wu = decode_vq(layer["codes_up"][e], layer["cb_up"], d)
     Wd = decode_vq(layer["codes_down"][e], layer["cb_down"], d)
-    r = 0 if layer.get("U_gate") is None else _f(layer["U_gate"]).shape[1]
-    if r > 0:
-        Wg = Wg + _f(layer["U_gate"]) @ _f(layer["V_gate"][e])
+    if _rank(layer) > 0:
+        if gated:
+            Wg = Wg + _f(layer["U_gate"]) @ _f(layer["V_gate"][e])
         Wu = Wu + _f(layer["U_up"]) @ _f(layer["V_up"][e])
         Wd = Wd + _f(layer["A_down"][e]) @ _f(layer["B_down"])
     return Wg, Wu, Wd
@@ -178,6 +193,25 @@ def silu(g):
     return g / (1.0 + np.exp(-g))
 
 
+def relu2(u):
+    """Squared ReLU ``max(u, 0)^2``, the activation of up-only experts."""
+    u = np.asarray(u, dtype=np.float64)
+    return np.maximum(u, 0.0) ** 2
+
+
+ACTIVATIONS = ("silu_glu", "relu2_up")
+
+
+def activation(act: str, g, u):
+    """The expert activation phi (Sec. 2.1): ``silu(g) * u`` for gated
+    experts, ``max(u, 0)^2`` for up-only ones (``g`` unused, may be None)."""
+    if act == "silu_glu":
+        return silu(g) * u
+    if act == "relu2_up":
+        return relu2(u)
+    raise ValueError(f"unknown activation {act!r}")
+
+
 def shared_proj(x, U) -> np.ndarray:
     """Shared rank-r projection ``z = D^T h`` for every token (Sec. 4.2)."""
     return _f(x) @ _f(U)
@@ -186,12 +220,13 @@ def shared_proj(x, U) -> np.ndarray:
 # --------------------------------------------------------------------------
 # O1: the layer from dense reconstructions
 # --------------------------------------------------------------------------
-def expert_ffn(x, idx, a, layer: dict, d: int) -> np.ndarray:
+def expert_ffn(x, idx, a, layer: dict, d: int, act: str = "silu_glu") -> np.ndarray:
     """Expert computation plus the affinity-weighted sum for fixed routing.
 
     For token ``t`` and its j-th selected expert ``e``: ``g = Wg^T x_t``,
-    ``u = Wu^T x_t``, ``p = silu(g) * u``, ``y_e = Wd^T p``; the output is
-    ``sum_j a[t, j] * y_e`` summed in selection order (Sec. 2.1).
+    ``u = Wu^T x_t``, ``p = silu(g) * u`` (up-only: ``max(u, 0)^2``),
+    ``y_e = Wd^T p``; the output is ``sum_j a[t, j] * y_e`` summed in
+    selection order (Sec. 2.1).
     """
     xf = _f(x)
     idx = np.asarray(idx)
@@ -204,35 +239,36 @@ def expert_ffn(x, idx, a, layer: dict, d: int) -> np.ndarray:
         for j in range(idx.shape[1]):
             e = int(idx[t, j])
             if e not in cache:
-                cache[e] = expert_matrices(layer, e, d)
+                cache[e] = expert_matrices(layer, e, d, act)
             Wg, Wu, Wd = cache[e]
-            g = Wg.T @ xf[t]
+            g = None if Wg is None else Wg.T @ xf[t]
             u = Wu.T @ xf[t]
-            p = silu(g) * u
+            p = activation(act, g, u)
             y[t] += a[t, j] * (Wd.T @ p)
     return y
 
 
-def moe_layer(x, layer: dict, k: int, d: int):
+def moe_layer(x, layer: dict, k: int, d: int, act: str = "silu_glu"):
     """O1: route, then run the selected experts from dense reconstructions.
 
     Returns ``(y [B, H] f64, idx [B, k], a [B, k], margin [B])``.
     """
     idx, a, margin, _ = route(x, layer["router_w"], layer.get("router_bias"), k)
-    y = expert_ffn(x, idx, a, layer, d)
+    y = expert_ffn(x, idx, a, layer, d, act)
     return y, idx, a, margin
 
 
 # --------------------------------------------------------------------------
 # O3: Eq. (1) in factored form
 # --------------------------------------------------------------------------
-def expert_ffn_factored(x, idx, a, layer: dict, d: int, z=None) -> np.ndarray:
+def expert_ffn_factored(x, idx, a, layer: dict, d: int, z=None, act: str = "silu_glu") -> np.ndarray:
     """Same result as ``expert_ffn`` evaluated as in Eq. (1).
 
     Gate/up: ``o = Q_B(J_e)^T x + V_e^T (U^T x)`` with the shared projection
     ``U^T x`` computed once per token (Sec. 4.2); down:
     ``y_e = Q_B(J^d_e)^T p + B^T (A_e^T p)``. ``z`` optionally supplies the
-    shared projections as ``[2, B, r]`` (gate, up). Each selected expert's
+    shared projections as ``[2, B, r]`` (gate, up; up-only experts read the
+    up half alone). Each selected expert's
     VQ matrices are rebuilt once and applied to all of its tokens; the
     per-token expert outputs are then summed in selection order.
     """
@@ -241,21 +277,24 @@ def expert_ffn_factored(x, idx, a, layer: dict, d: int, z=None) -> np.ndarray:
     a = np.asarray(a, dtype=np.float64)
     B, H = xf.shape
     k = idx.shape[1]
-    has_lr = layer.get("U_gate") is not None and _f(layer["U_gate"]).shape[1] > 0
+    has_lr = _rank(layer) > 0
+    gated = act == "silu_glu"
     if has_lr and z is None:
-        z = np.stack([shared_proj(xf, layer["U_gate"]), shared_proj(xf, layer["U_up"])])
+        zg = shared_proj(xf, layer["U_gate"]) if gated else None
+        z = (zg, shared_proj(xf, layer["U_up"]))
     contrib = np.zeros((B, k, H))
     for e in sorted(set(int(v) for v in idx.ravel())):
-        Qg = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d)
+        Qg = decode_vq(layer["codes_gate"][e], layer["cb_gate"], d) if gated else None
         Qu = decode_vq(layer["codes_up"][e], layer["cb_up"], d)
         Qd = decode_vq(layer["codes_down"][e], layer["cb_down"], d)
         for t, j in zip(*np.nonzero(idx == e)):
-            g = Qg.T @ xf[t]
+            g = Qg.T @ xf[t] if gated else None
             u = Qu.T @ xf[t]
             if has_lr:
-                g = g + _f(layer["V_gate"][e]).T @ np.asarray(z[0][t], dtype=np.float64)
+                if gated:
+                    g = g + _f(layer["V_gate"][e]).T @ np.asarray(z[0][t], dtype=np.float64)
                 u = u + _f(layer["V_up"][e]).T @ np.asarray(z[1][t], dtype=np.float64)
-            p = silu(g) * u
+            p = activation(act, g, u)
             ye = Qd.T @ p
             if has_lr:
                 ye = ye + _f(layer["B_down"]).T @ (_f(layer["A_down"][e]).T @ p)
@@ -266,20 +305,21 @@ def expert_ffn_factored(x, idx, a, layer: dict, d: int, z=None) -> np.ndarray:
     return y
 
 
-def moe_layer_factored(x, layer: dict, k: int, d: int):
+def moe_layer_factored(x, layer: dict, k: int, d: int, act: str = "silu_glu"):
     """O3: route, then Eq. (1) in factored form. Same return as ``moe_layer``."""
     idx, a, margin, _ = route(x, layer["router_w"], layer.get("router_bias"), k)
-    return expert_ffn_factored(x, idx, a, layer, d), idx, a, margin
+    return expert_ffn_factored(x, idx, a, layer, d, act=act), idx, a, margin
 
 
 # --------------------------------------------------------------------------
 # dense-weight baselines
 # --------------------------------------------------------------------------
-def expert_ffn_dense(x, idx, a, W_gate, W_up, W_down) -> np.ndarray:
+def expert_ffn_dense(x, idx, a, W_gate, W_up, W_down, act: str = "silu_glu") -> np.ndarray:
     """Expert computation for fixed routing with dense expert matrices
     ``W_gate[e]``, ``W_up[e]`` [H, I] and ``W_down[e]`` [I, H] (Sec. 2.1):
     ``y_t = sum_j a[t, j] * W_down[e]^T (silu(W_gate[e]^T x_t) * W_up[e]^T x_t)``
-    in selection order."""
+    in selection order (up-only experts: ``max(W_up[e]^T x_t, 0)^2``,
+    ``W_gate`` unused)."""
     xf = _f(x)
     idx = np.asarray(idx)
     a = np.asarray(a, dtype=np.float64)
@@ -287,18 +327,18 @@ def expert_ffn_dense(x, idx, a, W_gate, W_up, W_down) -> np.ndarray:
     for t in range(xf.shape[0]):
         for j in range(idx.shape[1]):
             e = int(idx[t, j])
-            g = _f(W_gate[e]).T @ xf[t]
+            g = _f(W_gate[e]).T @ xf[t] if act == "silu_glu" else None
             u = _f(W_up[e]).T @ xf[t]
-            p = silu(g) * u
+            p = activation(act, g, u)
             y[t] += a[t, j] * (_f(W_down[e]).T @ p)
     return y
 
 
-def moe_layer_dense(x, router_w, router_bias, W_gate, W_up, W_down, k: int):
+def moe_layer_dense(x, router_w, router_bias, W_gate, W_up, W_down, k: int, act: str = "silu_glu"):
     """The uncompressed baseline layer: route, then dense experts.
     Returns ``(y [B, H] f64, idx [B, k], a [B, k], margin [B])``."""
     idx, a, margin, _ = route(x, router_w, router_bias, k)
-    return expert_ffn_dense(x, idx, a, W_gate, W_up, W_down), idx, a, margin
+    return expert_ffn_dense(x, idx, a, W_gate, W_up, W_down, act), idx, a, margin
 
 
 def moe_layer_dense_down(x, layer: dict, W_down, k: int, d: int):
@@ -323,7 +363,7 @@ def moe_layer_dense_down(x, layer: dict, W_down, k: int, d: int):
 # --------------------------------------------------------------------------
 # O2: scalar brute force (tiny shapes only)
 # --------------------------------------------------------------------------
-def moe_layer_scalar(x, layer: dict, k: int, d: int):
+def moe_layer_scalar(x, layer: dict, k: int, d: int, act: str = "silu_glu"):
     """O2: the whole layer with Python floats and explicit loops.
 
     Every weight is formed element by element from its definition,
@@ -334,27 +374,32 @@ def moe_layer_scalar(x, layer: dict, k: int, d: int):
     X = _f(x).tolist()
     Wr = _f(layer["router_w"]).tolist()
     bias = None if layer.get("router_bias") is None else _f(layer["router_bias"]).tolist()
-    cbg = _f(layer["cb_gate"]).tolist()
+    gated = act == "silu_glu"
+    if act not in ACTIVATIONS:
+        raise ValueError(f"unknown activation {act!r}")
+    cbg = _f(layer["cb_gate"]).tolist() if gated else None
     cbu = _f(layer["cb_up"]).tolist()
     cbd = _f(layer["cb_down"]).tolist()
-    Jg = np.asarray(layer["codes_gate"]).tolist()
+    Jg = np.asarray(layer["codes_gate"]).tolist() if gated else None
     Ju = np.asarray(layer["codes_up"]).tolist()
     Jd = np.asarray(layer["codes_down"]).tolist()
-    has_lr = layer.get("U_gate") is not None and _f(layer["U_gate"]).shape[1] > 0
+    has_lr = _rank(layer) > 0
+    Ug = Vg = None
     if has_lr:
-        Ug = _f(layer["U_gate"]).tolist()
+        if gated:
+            Ug = _f(layer["U_gate"]).tolist()
+            Vg = _f(layer["V_gate"]).tolist()
         Uu = _f(layer["U_up"]).tolist()
-        Vg = _f(layer["V_gate"]).tolist()
         Vu = _f(layer["V_up"]).tolist()
         Ad = _f(layer["A_down"]).tolist()
         Bd = _f(layer["B_down"]).tolist()
-        r = len(Ug[0])
+        r = len(Uu[0])
     else:
         r = 0
     B = len(X)
     H = len(X[0])
     E = len(Wr[0])
-    I = len(Jg[0][0])
+    I = len(Ju[0][0])
 
     def w_in_out(cb, J, U, V, e, i, j):
         val = cb[J[e][i // d][j]][i % d]
@@ -399,9 +444,13 @@ def moe_layer_scalar(x, layer: dict, k: int, d: int):
             u = [0.0] * I
             for c in range(I):
                 for i in range(H):
-                    g[c] += X[t][i] * w_in_out(cbg, Jg, Ug if r else None, Vg if r else None, e, i, c)
+                    if gated:
+                        g[c] += X[t][i] * w_in_out(cbg, Jg, Ug, Vg, e, i, c)
                     u[c] += X[t][i] * w_in_out(cbu, Ju, Uu if r else None, Vu if r else None, e, i, c)
-            p = [g[c] / (1.0 + math.exp(-g[c])) * u[c] for c in range(I)]
+            if gated:
+                p = [g[c] / (1.0 + math.exp(-g[c])) * u[c] for c in range(I)]
+            else:
+                p = [(u[c] if u[c] > 0.0 else 0.0) * (u[c] if u[c] > 0.0 else 0.0) for c in range(I)]
             for h in range(H):
                 s = 0.0
                 for i in range(I):

@@ -73,10 +73,12 @@ def _load():
         "cardan_vq_lr_expert_ffn": ([sp, i32, vp, vp, vp, vp, lp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_moe_layer": ([sp, i32, vp, lp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_moe_layer_noalloc": ([sp, i32, vp, lp, vp, vp, vp, vp], ctypes.c_int),
+        "cardan_moe_layer_relu2": ([sp, i32, vp, lp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_moe_decode_step": ([sp, i32, i32, vp, lp, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp],
                                    ctypes.c_int),
         "cardan_moe_layer_dense_down": ([sp, i32, vp, lp, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_dense_moe_layer": ([sp, i32, vp, dp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cardan_dense_moe_layer_relu2": ([sp, i32, vp, dp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cardan_rmsnorm_bf16": ([i32, i32, vp, ctypes.c_float, vp, vp], ctypes.c_int),
         "cardan_profile_begin": ([i32], ctypes.c_int),
         "cardan_profile_end": ([ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)], ctypes.c_int),
@@ -93,8 +95,9 @@ _lib = _load()
 EXPORTED = (
     "cardan_abi_version", "cardan_last_error", "cardan_workspace_bytes", "cardan_route_topk",
     "cardan_shared_proj", "cardan_vq_lr_expert_ffn", "cardan_moe_layer", "cardan_moe_layer_noalloc",
-    "cardan_moe_decode_step",
-    "cardan_moe_layer_dense_down", "cardan_dense_moe_layer", "cardan_rmsnorm_bf16",
+    "cardan_moe_decode_step", "cardan_moe_layer_relu2",
+    "cardan_moe_layer_dense_down", "cardan_dense_moe_layer", "cardan_dense_moe_layer_relu2",
+    "cardan_rmsnorm_bf16",
     "cardan_profile_begin", "cardan_profile_end",
 )
 
@@ -284,6 +287,24 @@ def moe_layer(shape: Shape, x, layer: DeviceLayer, ws=None, out=None, idx=None, 
     return y, idx, w
 
 
+def moe_layer_relu2(shape: Shape, x, layer: DeviceLayer, ws=None, out=None, idx=None, w=None):
+    """The whole layer with up-only squared-ReLU experts (the layer's gate
+    fields are not read). Returns ``(y float32 [B, H], topk_idx, topk_w)``."""
+    B = x.shape[0]
+    dev = x.device
+    y, idx, w = _outputs(shape, x, out, idx, w)
+    if ws is None:
+        ws = new_workspace(shape, B, dev)
+    st = layer.struct()
+    _check(_lib.cardan_moe_layer_relu2(
+        ctypes.byref(shape), B, _ptr(x, torch.bfloat16, "x", (B, shape.H)), ctypes.byref(st),
+        _ptr(y, torch.float32, "y", (B, shape.H)),
+        _ptr(idx, torch.int32, "topk_idx", (B, shape.top_k)),
+        _ptr(w, torch.float32, "topk_w", (B, shape.top_k)),
+        _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(dev)))
+    return y, idx, w
+
+
 def moe_decode_step(shape: Shape, x0, layers, eps: float = 1e-6, ws=None, out=None, x_norm=None,
                     idx=None, w=None):
     """``len(layers)`` stacked layers, each output RMS-normalised (bf16) into
@@ -362,7 +383,7 @@ class DenseLayer:
     and W_down [E, I, H] bf16."""
     tensors: dict
 
-    def struct(self, shape: Shape) -> DenseLayerStruct:
+    def struct(self, shape: Shape, up_only: bool = False) -> DenseLayerStruct:
         H, I, E = shape.H, shape.I, shape.E
         want = {"router_w": (torch.bfloat16, (H, E)), "router_bias": (torch.float32, (E,)),
                 "W_gate": (torch.bfloat16, (E, H, I)), "W_up": (torch.bfloat16, (E, H, I)),
@@ -370,21 +391,25 @@ class DenseLayer:
         vals = []
         for key in DENSE_LAYER_FIELDS:
             dt, shp = want[key]
-            p = _ptr(self.tensors.get(key), dt, key, shp, optional=key == "router_bias")
+            optional = key == "router_bias" or (up_only and key == "W_gate")
+            p = _ptr(self.tensors.get(key), dt, key, shp, optional=optional)
             vals.append(None if p is None else p.value)
         return DenseLayerStruct(*vals)
 
 
-def dense_moe_layer(shape: Shape, x, layer: DenseLayer, ws=None, out=None, idx=None, w=None):
-    """The uncompressed MoE layer (only H, I, E, top_k of ``shape`` are read).
+def dense_moe_layer(shape: Shape, x, layer: DenseLayer, ws=None, out=None, idx=None, w=None,
+                    relu2: bool = False):
+    """The uncompressed MoE layer (only H, I, E, top_k of ``shape`` are read);
+    ``relu2``: up-only squared-ReLU experts (``W_gate`` not read).
     Returns ``(y float32 [B, H], topk_idx, topk_w)``."""
     B = x.shape[0]
     dev = x.device
     y, idx, w = _outputs(shape, x, out, idx, w)
     if ws is None:
         ws = new_workspace(shape, B, dev)
-    st = layer.struct(shape)
-    _check(_lib.cardan_dense_moe_layer(
+    st = layer.struct(shape, up_only=relu2)
+    fn = _lib.cardan_dense_moe_layer_relu2 if relu2 else _lib.cardan_dense_moe_layer
+    _check(fn(
         ctypes.byref(shape), B, _ptr(x, torch.bfloat16, "x", (B, shape.H)), ctypes.byref(st),
         _ptr(y, torch.float32, "y", (B, shape.H)),
         _ptr(idx, torch.int32, "topk_idx", (B, shape.top_k)),

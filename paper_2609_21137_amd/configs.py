@@ -8,6 +8,7 @@ I=768, E=128, top-8) with the rank and code-book sizes fixed per workload.
 
 from __future__ import annotations
 
+import dataclasses
 from dataclasses import dataclass, field
 
 
@@ -27,6 +28,7 @@ class Workload:
     hot_experts: tuple = ()      # experts whose router logit gets +hot_bias
     hot_bias: float = 0.0
     rotate_layers: int = 0       # layers a benchmark rotates over (0: its default)
+    act: str = "silu_glu"        # expert activation: "silu_glu" (gate+up) or "relu2_up" (up only)
     description: str = field(default="", compare=False)
 
     @property
@@ -63,5 +65,15 @@ GEMMA4_B1 = Workload("gemma4_26b_a4b_moe_layer_b1", H=2816, I=704, E=128, top_k=
                      description="Gemma-4-26B-A4B-shaped MoE layer, d=8, K=256, r=384, batch 1")
 OTHER_MODELS_B1 = (DSV2_LITE_B1, OLMOE_B1, GEMMA4_B1)
 
+# the up-only model of the table: experts p = max(u, 0)^2 without a gate
+# projection; H = 2688 and I = 1856 are already multiples of the kernels'
+# 64 and 32 (no padding of either dimension)
+NEMOTRON3_B1 = Workload("nemotron3_nano_moe_layer_b1", H=2688, I=1856, E=128, top_k=6, d=8, K=256,
+                        r=512, B=1, seed=6, rotate_layers=2, act="relu2_up",
+                        description="Nemotron-3-Nano-shaped up-only squared-ReLU MoE layer, d=8, K=256, "
+                                    "r=512, batch 1")
+NEMOTRON3_B16 = dataclasses.replace(NEMOTRON3_B1, name="nemotron3_nano_moe_layer_b16", B=16,
+                                    description="Nemotron-3-Nano-shaped up-only layer, batch 16")
+
 WORKLOADS = {w.name: w for w in (TINY, QWEN3_B1, QWEN3_B16, WIDE_SKEW_B4, QWEN3_48L_B16,
-                                 *OTHER_MODELS_B1)}
+                                 *OTHER_MODELS_B1, NEMOTRON3_B1, NEMOTRON3_B16)}

@@ -129,24 +129,30 @@ StepBufs step_bufs(const Plan& P) {
     if (misaligned(p)) return fail(CARDAN_ERR_ALIGN, "%s is not 16-byte aligned", name); \
   } while (0)
 
-// need_down: the compressed down projection (code book, codes, A, B) is used
-int check_layer(const cardan_shape* s, const cardan_layer* L, bool need_router, bool need_down = true) {
+// need_down: the compressed down projection (code book, codes, A, B) is used;
+// need_gate: the gate projection is used (not for up-only experts)
+int check_layer(const cardan_shape* s, const cardan_layer* L, bool need_router, bool need_down = true,
+                bool need_gate = true) {
   if (!L) return fail(CARDAN_ERR_NULL_PTR, "layer is NULL");
   if (need_router) REQ(L->router_w, "router_w");
   if (L->router_bias && (reinterpret_cast<uintptr_t>(L->router_bias) & 3u))
     return fail(CARDAN_ERR_ALIGN, "router_bias is not 4-byte aligned");
-  REQ(L->cb_gate, "cb_gate");
+  if (need_gate) {
+    REQ(L->cb_gate, "cb_gate");
+    REQ(L->codes_gate, "codes_gate");
+  }
   REQ(L->cb_up, "cb_up");
-  REQ(L->codes_gate, "codes_gate");
   REQ(L->codes_up, "codes_up");
   if (need_down) {
     REQ(L->cb_down, "cb_down");
     REQ(L->codes_down, "codes_down");
   }
   if (s->r > 0) {
-    REQ(L->U_gate, "U_gate");
+    if (need_gate) {
+      REQ(L->U_gate, "U_gate");
+      REQ(L->V_gate, "V_gate");
+    }
     REQ(L->U_up, "U_up");
-    REQ(L->V_gate, "V_gate");
     REQ(L->V_up, "V_up");
     if (need_down) {
       REQ(L->A_down, "A_down");
@@ -318,12 +324,14 @@ int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out) {
   if (!out) return fail(CARDAN_ERR_NULL_PTR, "out is NULL");
   // the largest layout over batches 1..B, so one workspace serves any batch
   // up to B (split counts, hence layouts, depend on the batch)
-  // and every expert-weight form (compressed, dense down, all dense)
+  // and every expert-weight form (compressed, dense down, all dense) and
+  // activation (gated SiLU, up-only squared ReLU)
   size_t need = 0;
   const int all = F_ROUTE | F_Z | F_GROUP | F_EXPERTS;
   for (int b = 1; b <= B; ++b) {
     for (int form : {0, (int)F_DN_DENSE, F_DN_DENSE | F_GU_DENSE})
-      need = std::max(need, make_plan(shape, b, 1, all | form).total);
+      for (int act : {0, (int)F_UP_RELU2})
+        need = std::max(need, make_plan(shape, b, 1, all | form | act).total);
     need = std::max(need, step_bufs(make_plan(shape, b, 1, all | F_NORM_IN | F_SSQ_OUT)).total);
   }
   *out = need;
@@ -419,6 +427,37 @@ int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
   if ((rc = check_ws(P, ws, ws_bytes))) return rc;
   uint8_t* w = static_cast<uint8_t*>(ws);
   Args A = args_for(layer, w);
+  A.x = x;
+  A.topk_idx = topk_idx;
+  A.topk_w = topk_w;
+  A.z_out = reinterpret_cast<float*>(w + P.o_z);
+  A.y = y;
+  return run_layer(P, A, stream);
+}
+
+int cardan_moe_layer_relu2(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                           const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
+                           void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  int rc = check_shape(shape, B);
+  if (rc) return rc;
+  REQ(x, "x");
+  REQ(y, "y");
+  REQ(topk_idx, "topk_idx");
+  REQ(topk_w, "topk_w");
+  if ((rc = check_layer(shape, layer, true, true, false))) return rc;
+  const int flags = F_ROUTE | F_GROUP | F_EXPERTS | F_UP_RELU2 | (shape->r > 0 ? F_Z : 0);
+  const Plan P = make_plan(shape, B, 0, flags);
+  if ((rc = check_ws(P, ws, ws_bytes))) return rc;
+  // the kernels read only the up projection; the gate pointers alias it so
+  // that the one z basis (U_gate slot) is the up basis
+  cardan_layer L = *layer;
+  L.cb_gate = L.cb_up;
+  L.codes_gate = L.codes_up;
+  L.U_gate = L.U_up;
+  L.V_gate = L.V_up;
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  Args A = args_for(&L, w);
   A.x = x;
   A.topk_idx = topk_idx;
   A.topk_w = topk_w;
@@ -567,10 +606,13 @@ int cardan_moe_layer_dense_down(const cardan_shape* shape, int32_t B, const card
   return run_layer(P, A, stream);
 }
 
-int cardan_dense_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
-                           const cardan_dense_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
-                           void* ws, size_t ws_bytes, hipStream_t stream) {
-  g_err[0] = 0;
+}  // extern "C"
+
+namespace {
+// the uncompressed layer; relu2: up-only experts (W_gate not read)
+int dense_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x, const cardan_dense_layer* layer,
+                    float* y, int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes, hipStream_t stream,
+                    bool relu2) {
   if (!shape) return fail(CARDAN_ERR_NULL_PTR, "shape is NULL");
   cardan_shape s = *shape;  // only H, I, E and top_k describe a dense layer
   s.d = 8;
@@ -587,17 +629,17 @@ int cardan_dense_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf
   REQ(layer->router_w, "router_w");
   if (layer->router_bias && (reinterpret_cast<uintptr_t>(layer->router_bias) & 3u))
     return fail(CARDAN_ERR_ALIGN, "router_bias is not 4-byte aligned");
-  REQ(layer->W_gate, "W_gate");
+  if (!relu2) REQ(layer->W_gate, "W_gate");
   REQ(layer->W_up, "W_up");
   REQ(layer->W_down, "W_down");
-  const Plan P = make_plan(&s, B, 0, F_ROUTE | F_GROUP | F_EXPERTS | F_GU_DENSE | F_DN_DENSE);
+  const Plan P = make_plan(&s, B, 0, F_ROUTE | F_GROUP | F_EXPERTS | F_GU_DENSE | F_DN_DENSE | (relu2 ? F_UP_RELU2 : 0));
   if ((rc = check_ws(P, ws, ws_bytes))) return rc;
   // the kernels read the dense matrices through the code pointers
   cardan_layer L;
   memset(&L, 0, sizeof L);
   L.router_w = layer->router_w;
   L.router_bias = layer->router_bias;
-  L.codes_gate = reinterpret_cast<const uint8_t*>(layer->W_gate);
+  L.codes_gate = reinterpret_cast<const uint8_t*>(relu2 ? layer->W_up : layer->W_gate);
   L.codes_up = reinterpret_cast<const uint8_t*>(layer->W_up);
   L.codes_down = reinterpret_cast<const uint8_t*>(layer->W_down);
   Args A = args_for(&L, static_cast<uint8_t*>(ws));
@@ -606,6 +648,23 @@ int cardan_dense_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf
   A.topk_w = topk_w;
   A.y = y;
   return run_layer(P, A, stream);
+}
+}  // namespace
+
+extern "C" {
+
+int cardan_dense_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                           const cardan_dense_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
+                           void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  return dense_moe_layer(shape, B, x, layer, y, topk_idx, topk_w, ws, ws_bytes, stream, false);
+}
+
+int cardan_dense_moe_layer_relu2(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
+                                 const cardan_dense_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  return dense_moe_layer(shape, B, x, layer, y, topk_idx, topk_w, ws, ws_bytes, stream, true);
 }
 
 int cardan_rmsnorm_bf16(int32_t B, int32_t H, const float* y, float eps, cardan_bf16* x_next,

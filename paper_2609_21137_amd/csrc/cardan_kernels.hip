@@ -1122,15 +1122,18 @@ __device__ __forceinline__ void put_split_quad(uint4* row, int q, float4 v) {
   *lo = make_uint2(lw[0] | (lw[1] << 16), lw[2] | (lw[3] << 16));
 }
 
-// Down operand rows from the gate/up partial sums: p = silu(g) * u for token
-// rows [0, nt) (slots slot0 + t) on I columns col0 + [0, 4 nquad), each sum
+// Down operand rows from the gate/up partial sums: p = silu(g) * u (up-only
+// experts: p = max(u, 0)^2) for token rows [0, nt) (slots slot0 + t) on I columns col0 + [0, 4 nquad), each sum
 // over the ns splits in split order, staged as bf16 hi/lo quads. U units
 // (token, quad) per thread per round and NSC splits per load batch keep 16
 // loads in flight.
 template <int U, int NSC>
-__device__ __forceinline__ void stage_silu(const WsAccess& ws, const Plan& P, uint4* ops, int ld, int nt, int nquad,
-                                           int slot0, int col0) {
+__device__ __forceinline__ void stage_p(const WsAccess& ws, const Plan& P, uint4* ops, int ld, int nt, int nquad,
+                                        int slot0, int col0) {
   const int ns = P.ns, I = P.I, n = nt * nquad;
+  // up-only experts: the gate partials are never written, and their loads
+  // take the out-of-range offset (zeros, no memory access)
+  const bool relu2 = (P.flags & F_UP_RELU2) != 0;
   for (int i0 = threadIdx.x; i0 < n; i0 += U * kWG) {
     float4 g[U], u[U];
     uint32_t base[U];
@@ -1149,7 +1152,8 @@ __device__ __forceinline__ void stage_silu(const WsAccess& ws, const Plan& P, ui
         for (int pj = 0; pj < 2; ++pj)
 #pragma unroll
           for (int sc = 0; sc < NSC; ++sc)
-            v[uu][pj][sc] = ws.f4(s0 + sc < ns ? base[uu] + (uint32_t)((pj * ns + s0 + sc) * I * 4) : kOob);
+            v[uu][pj][sc] = ws.f4(s0 + sc < ns && (pj || !relu2) ? base[uu] + (uint32_t)((pj * ns + s0 + sc) * I * 4)
+                                                                 : kOob);
 #pragma unroll
       for (int uu = 0; uu < U; ++uu)
 #pragma unroll
@@ -1165,9 +1169,15 @@ __device__ __forceinline__ void stage_silu(const WsAccess& ws, const Plan& P, ui
       const int i = i0 + uu * kWG;
       if (i >= n) continue;
       const float4 x = g[uu], y = u[uu];
-      put_split_quad(ops + (i / nquad) * ld, i % nquad,
-                     make_float4(x.x / (1.0f + expf(-x.x)) * y.x, x.y / (1.0f + expf(-x.y)) * y.y,
-                                 x.z / (1.0f + expf(-x.z)) * y.z, x.w / (1.0f + expf(-x.w)) * y.w));
+      float4 p;
+      if (relu2) {
+        const float4 c = make_float4(fmaxf(y.x, 0.f), fmaxf(y.y, 0.f), fmaxf(y.z, 0.f), fmaxf(y.w, 0.f));
+        p = make_float4(c.x * c.x, c.y * c.y, c.z * c.z, c.w * c.w);
+      } else {
+        p = make_float4(x.x / (1.0f + expf(-x.x)) * y.x, x.y / (1.0f + expf(-x.y)) * y.y,
+                        x.z / (1.0f + expf(-x.z)) * y.z, x.w / (1.0f + expf(-x.w)) * y.w);
+      }
+      put_split_quad(ops + (i / nquad) * ld, i % nquad, p);
     }
   }
 }
@@ -1458,8 +1468,8 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
     trace_mark(2);
   }
 
-  // counts the tile done for (a, cg); the down tiles form p = silu(g) * u
-  // from the 2 ns partial sums of their columns
+  // counts the tile done for (a, cg); the down tiles form p from the
+  // n_proj ns partial sums of their columns
   publish(wsp<int>(A, P.o_gu_tick) + (a * P.ncg + cg) * kTickPad);
 }
 
@@ -1476,7 +1486,7 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
   // every gate/up tile of the column groups holding inputs [32 ks0, 32 ks1)
   const int cg0 = ks0 * 32 / kColsPerGroup, ncgw = (ks1 * 32 - 1) / kColsPerGroup - cg0 + 1;
   const int* tick = wsp<const int>(A, P.o_gu_tick) + (a * P.ncg + cg0) * kTickPad;
-  wait_all(A, ncgw, [&](int i) { return ld_dev(tick + i * kTickPad) >= 2 * P.ns; });
+  wait_all(A, ncgw, [&](int i) { return ld_dev(tick + i * kTickPad) >= n_proj(P) * P.ns; });
   const int ld = (ks1 - ks0) * 8 + 1;
   uint4* ps = reinterpret_cast<uint4*>(smem);
   const WsAccess ws(A, P);
@@ -1487,13 +1497,13 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
     stage();
     const int nquad = (ks1 - ks0) * 8, slot0 = R.s0 + tg, col0 = ks0 * 32;
     if (P.ns <= 1)
-      stage_silu<8, 1>(ws, P, ps, ld, nt, nquad, slot0, col0);
+      stage_p<8, 1>(ws, P, ps, ld, nt, nquad, slot0, col0);
     else if (P.ns <= 2)
-      stage_silu<4, 2>(ws, P, ps, ld, nt, nquad, slot0, col0);
+      stage_p<4, 2>(ws, P, ps, ld, nt, nquad, slot0, col0);
     else if (P.ns <= 4)
-      stage_silu<2, 4>(ws, P, ps, ld, nt, nquad, slot0, col0);
+      stage_p<2, 4>(ws, P, ps, ld, nt, nquad, slot0, col0);
     else
-      stage_silu<1, 8>(ws, P, ps, ld, nt, nquad, slot0, col0);
+      stage_p<1, 8>(ws, P, ps, ld, nt, nquad, slot0, col0);
     __syncthreads();
     trace_mark(0);
     f32x4 acc[4];
@@ -1510,7 +1520,7 @@ __device__ __forceinline__ void down_body_wide(const Plan& P, const Args& A, con
   // every gate/up tile of the column groups holding inputs [32 ks0, 32 ks1)
   const int cg0 = ks0 * 32 / kColsPerGroup, ncgw = (ks1 * 32 - 1) / kColsPerGroup - cg0 + 1;
   const int* tick = wsp<const int>(A, P.o_gu_tick) + (a * P.ncg + cg0) * kTickPad;
-  wait_all(A, ncgw, [&](int i) { return ld_dev(tick + i * kTickPad) >= 2 * P.ns; });
+  wait_all(A, ncgw, [&](int i) { return ld_dev(tick + i * kTickPad) >= n_proj(P) * P.ns; });
   const int ld = (ks1 - ks0) * 8 + 1;
   uint4* ps = reinterpret_cast<uint4*>(smem);
   const WsAccess ws(A, P);
@@ -1521,13 +1531,13 @@ __device__ __forceinline__ void down_body_wide(const Plan& P, const Args& A, con
     stage();
     const int nquad = (ks1 - ks0) * 8, slot0 = R.s0 + tg, col0 = ks0 * 32;
     if (P.ns <= 1)
-      stage_silu<8, 1>(ws, P, ps, ld, nt, nquad, slot0, col0);
+      stage_p<8, 1>(ws, P, ps, ld, nt, nquad, slot0, col0);
     else if (P.ns <= 2)
-      stage_silu<4, 2>(ws, P, ps, ld, nt, nquad, slot0, col0);
+      stage_p<4, 2>(ws, P, ps, ld, nt, nquad, slot0, col0);
     else if (P.ns <= 4)
-      stage_silu<2, 4>(ws, P, ps, ld, nt, nquad, slot0, col0);
+      stage_p<2, 4>(ws, P, ps, ld, nt, nquad, slot0, col0);
     else
-      stage_silu<1, 8>(ws, P, ps, ld, nt, nquad, slot0, col0);
+      stage_p<1, 8>(ws, P, ps, ld, nt, nquad, slot0, col0);
     __syncthreads();
     trace_mark(0);
     f32x4 acc[NACC];
@@ -1622,7 +1632,7 @@ __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, i
 
 // Dense gate/up tile (a, pj, cg, s): 256 output columns of W_pj[e] [H][I]
 // over split s of the H inputs, partial sums into the same slots as the
-// compressed tile, so the down tiles take p = silu(g) * u unchanged.
+// compressed tile, so the down tiles form p unchanged.
 __device__ void item_gateup_dense(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg,
                                   int s, uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);

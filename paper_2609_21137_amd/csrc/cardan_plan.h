@@ -17,8 +17,9 @@
 //   select          per token: logits, top-k, gating
 //   z reduce        256 outputs of z = U^T x each
 //   gate/up tiles   (active expert a, gate|up, 256 columns, split of the
-//                   joint axis [H inputs | r ranks]), partial sums; the last
-//                   tile of (a, columns) forms p = silu(g) * u
+//                   joint axis [H inputs | r ranks]), partial sums; the down
+//                   tiles form p = silu(g) * u from them (up-only experts: up
+//                   tiles alone, p = relu(u)^2)
 //   down tiles      (a, 256 output columns of [H | r], split of I); the last
 //                   low-rank tile of an expert sums its splits into u_e
 //   combine tiles   (256 output columns, group of tpc tokens)
@@ -75,7 +76,10 @@ enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8,
        // writes it as bf16 x for the expert kernel
        F_NORM_IN = 1024,
        F_SSQ_OUT = 2048,   // combine tiles write per-token partial sums of y^2 for the next layer
-       F_PREFETCH = 4096 };  // idle expert-kernel workgroups touch the next layer's shared tensors
+       F_PREFETCH = 4096,  // idle expert-kernel workgroups touch the next layer's shared tensors
+       // up-only experts with a squared-ReLU activation, p = max(u, 0)^2: no
+       // gate tiles; the layer's gate pointers are not read
+       F_UP_RELU2 = 8192 };
 
 // counters at the start of the workspace, one per 64-byte slot: the status
 // count of timed-out waits
@@ -134,7 +138,9 @@ inline __host__ __device__ size_t combine_lds(const Plan& P) {
 __host__ __device__ inline int expert_mode(const Plan& P) {
   return (P.flags & F_GU_DENSE) ? 2 : (P.flags & F_DN_DENSE) ? 1 : 0;
 }
-__host__ __device__ inline int gateup_tiles_per_expert(const Plan& P) { return 2 * P.ncg * P.ns; }
+// projections with gate/up tiles: gate and up, or up alone
+__host__ __device__ inline int n_proj(const Plan& P) { return (P.flags & F_UP_RELU2) ? 1 : 2; }
+__host__ __device__ inline int gateup_tiles_per_expert(const Plan& P) { return n_proj(P) * P.ncg * P.ns; }
 __host__ __device__ inline int dn_width(const Plan& P) { return (P.flags & F_DN_WIDE) ? 2 : 1; }
 __host__ __device__ inline int down_tiles_per_expert(const Plan& P) {
   return (P.ncgh + dn_width(P) - 1) / dn_width(P) * P.nsd + P.ncgr * P.nsdl;
@@ -163,12 +169,13 @@ __host__ __device__ inline void joint_split(int s, int ns, int ns_v, int KSX, in
 // coefficient tiles the second, each class in its natural (expert, gate|up,
 // column group, split) order; once one class runs out the other fills every
 // position. Gate/up tiles wait for nothing, so any order is deadlock-free.
+// Up-only experts have up tiles alone (pj = 1).
 struct GateUpTile {
   int a, pj, cg, s;
 };
 __host__ __device__ inline GateUpTile gateup_at(const Plan& P, int p, int nact, int s_vq, int G) {
-  const int half = G >> 1;
-  const int n_v = nact * 2 * P.ncg * s_vq, n_l = nact * 2 * P.ncg * (P.ns - s_vq);
+  const int half = G >> 1, np = n_proj(P);
+  const int n_v = nact * np * P.ncg * s_vq, n_l = nact * np * P.ncg * (P.ns - s_vq);
   const int r = p / G, w = p - r * G;
   const int v = r * half + (w < half ? w : half);  // code-preferring positions before p
   const int l = p - v;                             // coefficient-preferring positions before p
@@ -188,7 +195,7 @@ __host__ __device__ inline GateUpTile gateup_at(const Plan& P, int p, int nact, 
   i /= nsc;
   const int cg = i % P.ncg;
   i /= P.ncg;
-  return {i >> 1, i & 1, cg, s};
+  return np == 2 ? GateUpTile{i >> 1, i & 1, cg, s} : GateUpTile{i, 1, cg, s};
 }
 
 // Dynamic LDS limit of either kernel; a plan needing more is rejected.

@@ -96,7 +96,8 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // min(r, 256) I * 2. Dense bf16 weights: 256 H * 2 per gate/up and
   // 256 I * 2 per down (expert, 256 columns).
   const double exp_act = fmax(1.0, P.E * (1.0 - pow(1.0 - (double)P.k / P.E, (double)B)));
-  const double gu_expert = mode == 2 ? 2.0 * P.H * P.I * 2 : 2.0 * P.H * P.I / P.d + 2.0 * P.I * P.r * 2;
+  const double npj = n_proj(P);  // gate and up, or up alone
+  const double gu_expert = mode == 2 ? npj * P.H * P.I * 2 : npj * P.H * P.I / P.d + npj * P.I * P.r * 2;
   const double dn_expert = mode >= 1 ? (double)P.I * P.H * 2 : (double)P.H * P.I / P.d + (double)P.I * P.r * 2;
   const double per_expert = gu_expert + dn_expert;
   // A VQ down K-step costs twice a gate/up one (p enters as hi + lo), so its
@@ -127,7 +128,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
     }
     P.nsd = mode >= 1 ? splits(256.0 * P.I * 2, KSD) : splits(2.0 * 256.0 * P.I / P.d, KSD);
     P.nsdl = P.r > 0 ? splits((double)std::min(P.r, kColsPerGroup) * P.I * 2, KSD) : 1;
-    const double items = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
+    const double items = exp_act * (npj * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
     if (items <= 512.0 || tile >= tile_max) break;
     tile *= 1.05;
   }
@@ -145,7 +146,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
     for (int mult = 1; mult <= 4 && !done; mult *= 2) {
       const int nv = std::max(P.ns_v, ceil_div(KSX, pd * mult));
       for (const int nl : {nl_fine, nl_keep}) {
-        const double items = exp_act * (2.0 * P.ncg * (nv + nl) + P.ncgh * P.nsd + P.ncgr * P.nsdl);
+        const double items = exp_act * (npj * P.ncg * (nv + nl) + P.ncgh * P.nsd + P.ncgr * P.nsdl);
         if (items <= 1.25 * 512.0) {
           P.ns_v = nv;
           P.ns = nv + nl;
@@ -179,7 +180,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // VQ down tiles over two column groups, so that each K-step's activation
   // reads serve twice the columns and the down tiles take half the
   // workgroup slots (fewer rounds, longer tiles)
-  const double items_all = exp_act * (2.0 * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
+  const double items_all = exp_act * (npj * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
   if (mode == 0 && items_all > 2 * 512.0 && P.ncgh > 1 && P.d == 8) P.flags |= F_DN_WIDE;
 
   // Small batches at ranks above 128: B^T u streams more of B than a

@@ -14,7 +14,9 @@ Recipe (one independent PCG64 stream per tensor, keyed by
 * Codes uniform over ``0..K-1``, one uint8 per block, row-major
   ``[in/d, out]`` per expert.
 * Shared basis ``U[H, r] ~ N(0, 1/H)`` (variance), one matrix used for both
-  gate and up; private ``V_e[r, I] ~ N(0, 0.01)`` (std).
+  gate and up; private ``V_e[r, I] ~ N(0, 0.01)`` (std). Up-only layers
+  (squared-ReLU experts) draw no gate tensors; their up basis has its own
+  stream.
 * Down: private ``A_e[I, r] ~ N(0, 0.01)`` (std), shared ``B[r, H] ~ N(0, 1/H)``
   (variance).
 * Dense bf16 expert matrices (the uncompressed baseline and the dense-down
@@ -64,12 +66,15 @@ def _normal_bf16(rng: np.random.Generator, shape, std: float) -> np.ndarray:
 
 
 def make_layer(H: int, I: int, E: int, d: int, K: int, r: int, seed: int, layer: int = 0,
-               hot_experts=(), hot_bias: float = 0.0, separate_up_basis: bool = False) -> dict:
+               hot_experts=(), hot_bias: float = 0.0, separate_up_basis: bool = False,
+               up_only: bool = False) -> dict:
     """All weights of one layer as numpy arrays in their storage formats.
 
     Keys match the C struct ``cardan_layer``. ``U_up`` is the same array as
     ``U_gate`` unless ``separate_up_basis`` is set (then it gets its own
-    stream). With ``r == 0`` the low-rank arrays are ``None``.
+    stream). With ``r == 0`` the low-rank arrays are ``None``. ``up_only``
+    (experts without a gate projection): the gate arrays are ``None`` and
+    ``U_up`` has its own stream; the other arrays are the same draws.
     """
     if H % d or I % d:
         raise ValueError("H and I must be multiples of d")
@@ -79,17 +84,18 @@ def make_layer(H: int, I: int, E: int, d: int, K: int, r: int, seed: int, layer:
     for e in hot_experts:
         bias[e] += hot_bias
     L["router_bias"] = bias.astype(np.float32)
-    L["cb_gate"] = _normal_bf16(_rng(seed, layer, _T_CBG), (K, d), 0.02)
+    L["cb_gate"] = None if up_only else _normal_bf16(_rng(seed, layer, _T_CBG), (K, d), 0.02)
     L["cb_up"] = _normal_bf16(_rng(seed, layer, _T_CBU), (K, d), 0.02)
     L["cb_down"] = _normal_bf16(_rng(seed, layer, _T_CBD), (K, d), 0.02)
-    L["codes_gate"] = _rng(seed, layer, _T_JG).integers(0, K, size=(E, H // d, I), dtype=np.uint8)
+    L["codes_gate"] = (None if up_only else
+                       _rng(seed, layer, _T_JG).integers(0, K, size=(E, H // d, I), dtype=np.uint8))
     L["codes_up"] = _rng(seed, layer, _T_JU).integers(0, K, size=(E, H // d, I), dtype=np.uint8)
     L["codes_down"] = _rng(seed, layer, _T_JD).integers(0, K, size=(E, I // d, H), dtype=np.uint8)
     if r > 0:
-        L["U_gate"] = _normal_bf16(_rng(seed, layer, _T_U), (H, r), H ** -0.5)
+        L["U_gate"] = None if up_only else _normal_bf16(_rng(seed, layer, _T_U), (H, r), H ** -0.5)
         L["U_up"] = (_normal_bf16(_rng(seed, layer, _T_UU), (H, r), H ** -0.5)
-                     if separate_up_basis else L["U_gate"])
-        L["V_gate"] = _normal_bf16(_rng(seed, layer, _T_VG), (E, r, I), 0.01)
+                     if separate_up_basis or up_only else L["U_gate"])
+        L["V_gate"] = None if up_only else _normal_bf16(_rng(seed, layer, _T_VG), (E, r, I), 0.01)
         L["V_up"] = _normal_bf16(_rng(seed, layer, _T_VU), (E, r, I), 0.01)
         L["A_down"] = _normal_bf16(_rng(seed, layer, _T_A), (E, I, r), 0.01)
         L["B_down"] = _normal_bf16(_rng(seed, layer, _T_B), (r, H), H ** -0.5)
@@ -130,7 +136,7 @@ def make_input(H: int, B: int, seed: int, layer: int = 0, step: int = 0) -> np.n
 def workload_layer(w: Workload, layer: int = 0, **kw) -> dict:
     """``make_layer`` for a named workload."""
     return make_layer(w.H, w.I, w.E, w.d, w.K, w.r, w.seed, layer,
-                      hot_experts=w.hot_experts, hot_bias=w.hot_bias, **kw)
+                      hot_experts=w.hot_experts, hot_bias=w.hot_bias, up_only=w.act == "relu2_up", **kw)
 
 
 def workload_input(w: Workload, layer: int = 0, step: int = 0, B: int | None = None) -> np.ndarray:

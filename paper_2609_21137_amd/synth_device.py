@@ -18,7 +18,7 @@ from .configs import Workload
 
 # stream ids of the tensors (distinct from one another per (seed, layer))
 _IDS = {"router_w": 2, "cb_gate": 3, "cb_up": 4, "cb_down": 5, "codes_gate": 6, "codes_up": 7,
-        "codes_down": 8, "U_gate": 9, "V_gate": 11, "V_up": 12, "A_down": 13, "B_down": 14,
+        "codes_down": 8, "U_gate": 9, "U_up": 10, "V_gate": 11, "V_up": 12, "A_down": 13, "B_down": 14,
         "W_gate": 15, "W_up": 16, "W_down": 17}
 
 
@@ -39,8 +39,10 @@ def _codes(shape, K: int, g: torch.Generator) -> torch.Tensor:
 
 def layer_tensors(w: Workload, layer: int) -> dict:
     """One compressed layer's device tensors, keyed like ``cardan_layer``
-    (``U_up`` is the same tensor as ``U_gate``; ``None`` where r == 0)."""
+    (``U_up`` is the same tensor as ``U_gate``; ``None`` where r == 0; up-only
+    layers have no gate tensors and their own ``U_up``)."""
     H, I, E, d, K, r = w.H, w.I, w.E, w.d, w.K, w.r
+    up_only = w.act == "relu2_up"
     T = {"router_w": _normal_bf16((H, E), H ** -0.5, _gen(w.seed, layer, "router_w"))}
     bias = 1e-3 * torch.arange(E, dtype=torch.float64)
     for e in w.hot_experts:
@@ -48,13 +50,15 @@ def layer_tensors(w: Workload, layer: int) -> dict:
     T["router_bias"] = bias.to(torch.float32).cuda()
     for cb in ("cb_gate", "cb_up", "cb_down"):
         T[cb] = _normal_bf16((K, d), 0.02, _gen(w.seed, layer, cb))
-    T["codes_gate"] = _codes((E, H // d, I), K, _gen(w.seed, layer, "codes_gate"))
+    T["codes_gate"] = None if up_only else _codes((E, H // d, I), K, _gen(w.seed, layer, "codes_gate"))
     T["codes_up"] = _codes((E, H // d, I), K, _gen(w.seed, layer, "codes_up"))
     T["codes_down"] = _codes((E, I // d, H), K, _gen(w.seed, layer, "codes_down"))
+    if up_only:
+        T["cb_gate"] = None
     if r > 0:
-        T["U_gate"] = _normal_bf16((H, r), H ** -0.5, _gen(w.seed, layer, "U_gate"))
-        T["U_up"] = T["U_gate"]
-        T["V_gate"] = _normal_bf16((E, r, I), 0.01, _gen(w.seed, layer, "V_gate"))
+        T["U_gate"] = None if up_only else _normal_bf16((H, r), H ** -0.5, _gen(w.seed, layer, "U_gate"))
+        T["U_up"] = _normal_bf16((H, r), H ** -0.5, _gen(w.seed, layer, "U_up")) if up_only else T["U_gate"]
+        T["V_gate"] = None if up_only else _normal_bf16((E, r, I), 0.01, _gen(w.seed, layer, "V_gate"))
         T["V_up"] = _normal_bf16((E, r, I), 0.01, _gen(w.seed, layer, "V_up"))
         T["A_down"] = _normal_bf16((E, I, r), 0.01, _gen(w.seed, layer, "A_down"))
         T["B_down"] = _normal_bf16((r, H), H ** -0.5, _gen(w.seed, layer, "B_down"))

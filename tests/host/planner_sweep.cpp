@@ -110,10 +110,10 @@ static void check_plan(const cardan_shape& s, int B, int z_sep, int flags, Count
       for (int p = 0; p < n; ++p) {
         const GateUpTile t = gateup_at(P, p, nact, P.ns_v, G);
         const bool ok = t.a >= 0 && t.a < nact && (t.pj == 0 || t.pj == 1) && t.cg >= 0 && t.cg < P.ncg &&
-                        t.s >= 0 && t.s < P.ns;
+                        t.s >= 0 && t.s < P.ns && (t.pj == 1 || !(P.flags & F_UP_RELU2));
         CHECK(ok);
         if (!ok) continue;
-        const int id = ((t.a * 2 + t.pj) * P.ncg + t.cg) * P.ns + t.s;
+        const int np = n_proj(P), id = ((t.a * np + (np == 2 ? t.pj : 0)) * P.ncg + t.cg) * P.ns + t.s;
         CHECK(!seen[id]);
         seen[id] = 1;
       }
@@ -130,7 +130,7 @@ int main(int argc, char** argv) {
   std::vector<cardan_shape> shapes = {
       {256, 128, 8, 2, 4, 16, 8},      {2048, 768, 128, 8, 8, 256, 128}, {4096, 1536, 64, 6, 8, 256, 256},
       {2048, 1408, 64, 6, 8, 256, 384}, {2048, 1024, 64, 8, 4, 256, 256}, {2816, 704, 128, 8, 8, 256, 384},
-      {2688, 1856, 128, 6, 8, 256, 128}, {64, 32, 1, 1, 2, 1, 0},        {8192, 4096, 1024, 32, 8, 256, 512}};
+      {2688, 1856, 128, 6, 8, 256, 128}, {2688, 1856, 128, 6, 8, 256, 512}, {64, 32, 1, 1, 2, 1, 0},        {8192, 4096, 1024, 32, 8, 256, 512}};
   for (int i = 0; i < n_random; ++i) {
     cardan_shape s;
     s.d = pick({2, 4, 8});
@@ -156,7 +156,10 @@ int main(int argc, char** argv) {
       check_plan(s, B, 1, F_ROUTE, &ref);
       check_plan(s, B, 1, F_Z, &ref);
       check_plan(s, B, 1, F_GROUP | F_EXPERTS, &ref);
-      plans += 5;
+      // up-only squared-ReLU experts, compressed and dense
+      check_plan(s, B, 0, all | F_UP_RELU2, &ref);
+      check_plan(s, B, 0, F_ROUTE | F_GROUP | F_EXPERTS | F_DN_DENSE | F_GU_DENSE | F_UP_RELU2, &ref);
+      plans += 7;
     }
   }
   printf("%ld plans checked, %d failures\n", plans, g_fail);

@@ -350,13 +350,134 @@ def pin_dense_down_reduces_to_compressed():
     assert np.abs(y1).max() > 1e-3  # a non-trivial output
 
 
+# --------------------------------------------------------------------------
+# up-only experts with a squared-ReLU activation (Table 2, projection "up")
+# --------------------------------------------------------------------------
+def dense_relu2_moe_torch(x, Wr, bias, Wu, Wd, k):
+    """Plain dense MoE with up-only experts: router, top-k, softmax over the
+    top-k, ``relu(h W_up)^2 W_down`` per expert, affinity-weighted sum
+    (torch float64)."""
+    x = torch.as_tensor(x, dtype=torch.float64)
+    logits = x @ torch.as_tensor(Wr, dtype=torch.float64) + torch.as_tensor(bias, dtype=torch.float64)
+    vals, idx = torch.topk(logits, k, dim=1)
+    a = torch.softmax(vals, dim=1)
+    Wu = torch.as_tensor(Wu, dtype=torch.float64)
+    Wd = torch.as_tensor(Wd, dtype=torch.float64)
+    y = torch.zeros_like(x)
+    for t in range(x.shape[0]):
+        for j in range(k):
+            e = int(idx[t, j])
+            p = torch.square(torch.relu(x[t] @ Wu[e]))
+            y[t] += a[t, j] * (p @ Wd[e])
+    return y.numpy(), idx.numpy(), a.numpy()
+
+
+def _up_only(L):
+    """The layer without its gate tensors (what an up-only model stores)."""
+    L = dict(L)
+    for key in ("cb_gate", "codes_gate", "U_gate", "V_gate"):
+        L[key] = None
+    return L
+
+
+def pin_relu2_closed_form():
+    u = np.array([-2.0, -0.5, 0.0, 0.5, 3.0])
+    assert O.relu2(u).tolist() == [0.0, 0.0, 0.0, 0.25, 9.0]
+    assert O.activation("relu2_up", None, u).tolist() == [0.0, 0.0, 0.0, 0.25, 9.0]
+    # the gated form multiplies by u, the up-only form never reads g
+    g = np.array([1.0])
+    assert abs(O.activation("silu_glu", g, np.array([2.0]))[0] - 2.0 / (1.0 + math.exp(-1.0))) < 1e-15
+
+
+def pin_relu2_onehot_is_dense_moe():
+    """r = 0 and code book = identity (K = d): the up-only layer equals a
+    dense up-only MoE on the 0/1 matrices W[i, j] = [i % d == J[i // d, j]]
+    (torch's relu and square); x ~ N(0, 1) gives u of both signs."""
+    H, I, E, k, d, B = 16, 8, 5, 2, 4, 3
+    L = _up_only(_rand_layer(H, I, E, d, d, 0, seed=17))
+    eye = _bf(np.eye(d))
+    L["cb_up"] = L["cb_down"] = eye
+    x = synth.make_input(H, B, seed=17)
+
+    def onehot(J, n_in):
+        rows = np.arange(n_in)
+        return (rows[:, None] % d == J[rows // d, :]).astype(np.float64)
+
+    Wu = np.stack([onehot(L["codes_up"][e], H) for e in range(E)])
+    Wd = np.stack([onehot(L["codes_down"][e], I) for e in range(E)])
+    xf = O.bf16_to_f64(x)
+    y_ref, idx_ref, a_ref = dense_relu2_moe_torch(xf, O.bf16_to_f64(L["router_w"]),
+                                                  L["router_bias"].astype(np.float64), Wu, Wd, k)
+    u_all = np.einsum("th,ehi->tei", xf, Wu)
+    assert (u_all > 0).any() and (u_all < 0).any()
+    for fn in (O.moe_layer, O.moe_layer_factored, O.moe_layer_scalar):
+        y, idx, a, _ = fn(x, L, k, d, "relu2_up")
+        assert np.array_equal(idx, idx_ref), fn.__name__
+        assert np.allclose(a, a_ref, rtol=0, atol=1e-14), fn.__name__
+        assert np.allclose(y, y_ref, rtol=1e-12, atol=1e-12), fn.__name__
+
+
+def pin_relu2_o1_equals_scalar_and_factored():
+    """Up-only layers with the low-rank terms: O1 (dense reconstruction), O2
+    (scalar loops) and O3 (factored) agree on tiny shapes; a gated layer's
+    gate tensors, where present, change nothing."""
+    for n, (H, I, E, k, d, K, r, B) in enumerate(TINY_SHAPES):
+        full = _scale_codebooks(_rand_layer(H, I, E, d, K, r, seed=300 + n), 25.0)
+        L = _up_only(full)
+        x = synth.make_input(H, B, seed=300 + n)
+        y1, i1, a1, _ = O.moe_layer(x, L, k, d, "relu2_up")
+        y2, i2, a2, _ = O.moe_layer_scalar(x, L, k, d, "relu2_up")
+        y3, i3, a3, _ = O.moe_layer_factored(x, L, k, d, "relu2_up")
+        y4, _, _, _ = O.moe_layer_factored(x, full, k, d, "relu2_up")
+        assert np.array_equal(i1, i2) and np.array_equal(i1, i3)
+        scale = max(np.abs(y2).max(), 1e-30)
+        assert np.abs(y1 - y2).max() <= 1e-12 * scale, (n, np.abs(y1 - y2).max(), scale)
+        assert np.abs(y1 - y3).max() <= 1e-12 * scale
+        assert np.array_equal(y3, y4)
+        assert scale > 1e-6  # a non-trivial output
+
+
+def pin_relu2_dense_baseline_against_torch():
+    H, I, E, k, B = 16, 12, 6, 3, 4
+    W = synth.make_dense_weights(H, I, E, seed=19, which=("up", "down"))
+    Wr = _bf(np.random.default_rng(19).standard_normal((H, E)) * 0.5)
+    bias = np.linspace(0.0, 1e-2, E).astype(np.float32)
+    x = synth.make_input(H, B, seed=19)
+    Wu, Wd = (O.bf16_to_f64(W[n]) * 20.0 for n in ("W_up", "W_down"))
+    Wu_b, Wd_b = _bf(Wu), _bf(Wd)
+    y, idx, a, _ = O.moe_layer_dense(x, Wr, bias, None, Wu_b, Wd_b, k, "relu2_up")
+    y_ref, idx_ref, a_ref = dense_relu2_moe_torch(O.bf16_to_f64(x), O.bf16_to_f64(Wr), bias.astype(np.float64),
+                                                  O.bf16_to_f64(Wu_b), O.bf16_to_f64(Wd_b), k)
+    assert np.array_equal(idx, idx_ref)
+    assert np.allclose(a, a_ref, rtol=0, atol=1e-14)
+    assert np.allclose(y, y_ref, rtol=1e-12, atol=1e-12)
+    assert np.abs(y).max() > 1e-3
+
+
+def pin_relu2_reduces_to_dense_relu2():
+    """With r = 0 the decoded up-only layer equals the dense up-only baseline
+    on the decoded matrices bit for bit."""
+    H, I, E, k, d, K, B = 16, 16, 5, 2, 4, 16, 3
+    L = _up_only(_scale_codebooks(_rand_layer(H, I, E, d, K, 0, seed=21), 10.0))
+    x = synth.make_input(H, B, seed=21)
+    dec = lambda key, cb: np.stack([_bf(O.decode_vq(L[key][e], L[cb], d)) for e in range(E)])
+    Wu, Wd = dec("codes_up", "cb_up"), dec("codes_down", "cb_down")
+    y1, idx1, a1, _ = O.moe_layer(x, L, k, d, "relu2_up")
+    y2, idx2, a2, _ = O.moe_layer_dense(x, L["router_w"], L["router_bias"], None, Wu, Wd, k, "relu2_up")
+    assert np.array_equal(idx1, idx2) and np.array_equal(a1, a2)
+    assert np.array_equal(y1, y2)
+    assert np.abs(y1).max() > 1e-3
+
+
 PINS = [
     pin_worked_example, pin_o1_equals_scalar_bruteforce, pin_o1_equals_factored,
     pin_onehot_codebook_is_dense_moe, pin_value_table_d1_is_dense_moe,
     pin_zero_codebooks_is_lowrank_moe, pin_expert_permutation_invariance,
     pin_batch_rows_independent, pin_topk_rules, pin_decode_layout, pin_silu_and_rmsnorm,
     pin_bf16_widening, pin_storage_rate_tables, pin_dense_baseline_against_torch,
-    pin_dense_down_reduces_to_compressed,
+    pin_dense_down_reduces_to_compressed, pin_relu2_closed_form, pin_relu2_onehot_is_dense_moe,
+    pin_relu2_o1_equals_scalar_and_factored, pin_relu2_dense_baseline_against_torch,
+    pin_relu2_reduces_to_dense_relu2,
 ]
 
 
@@ -381,23 +502,23 @@ def _mut_decode_blocks_across_columns(codes, codebook, d):
     return blocks.reshape(J.shape[0] * d, J.shape[1])   # element order scrambled
 
 
-def _mut_drop_gate_lr(layer, e, d):
-    Wg, Wu, Wd = _ORIG["expert_matrices"](layer, e, d)
+def _mut_drop_gate_lr(layer, e, d, act="silu_glu"):
+    Wg, Wu, Wd = _ORIG["expert_matrices"](layer, e, d, act)
     if layer.get("U_gate") is not None and O.bf16_to_f64(layer["U_gate"]).shape[1] > 0:
         Wg = Wg - O.bf16_to_f64(layer["U_gate"]) @ O.bf16_to_f64(layer["V_gate"][e])
     return Wg, Wu, Wd
 
 
-def _mut_drop_down_lr(layer, e, d):
-    Wg, Wu, Wd = _ORIG["expert_matrices"](layer, e, d)
-    if layer.get("U_gate") is not None and O.bf16_to_f64(layer["U_gate"]).shape[1] > 0:
+def _mut_drop_down_lr(layer, e, d, act="silu_glu"):
+    Wg, Wu, Wd = _ORIG["expert_matrices"](layer, e, d, act)
+    if layer.get("U_up") is not None and O.bf16_to_f64(layer["U_up"]).shape[1] > 0:
         Wd = Wd - O.bf16_to_f64(layer["A_down"][e]) @ O.bf16_to_f64(layer["B_down"])
     return Wg, Wu, Wd
 
 
-def _mut_swap_gate_up(layer, e, d):
-    Wg, Wu, Wd = _ORIG["expert_matrices"](layer, e, d)
-    return Wu, Wg, Wd
+def _mut_swap_gate_up(layer, e, d, act="silu_glu"):
+    Wg, Wu, Wd = _ORIG["expert_matrices"](layer, e, d, act)
+    return (Wu, Wg, Wd) if Wg is not None else (Wg, Wu, Wd)
 
 
 def _mut_silu_sign(g):
@@ -429,15 +550,17 @@ def _mut_no_bias(x, router_w, router_bias=None):
     return _ORIG["router_logits"](x, router_w, None)
 
 
-def _mut_unweighted(x, idx, a, layer, d):
-    return _ORIG["expert_ffn"](x, idx, np.ones_like(np.asarray(a, dtype=np.float64)), layer, d)
+def _mut_unweighted(x, idx, a, layer, d, act="silu_glu"):
+    return _ORIG["expert_ffn"](x, idx, np.ones_like(np.asarray(a, dtype=np.float64)), layer, d, act)
 
 
 def _mut_storage_no_basis(d, K, r, H, I, E, b_index=None, b_coef=16, b_codebook=16, b_basis=16):
     return _ORIG["storage_bits_per_weight"](d, K, r, H, I, E, b_index, b_coef, b_codebook, 0)
 
 
-def _mut_dense_no_silu(x, idx, a, W_gate, W_up, W_down):
+def _mut_dense_no_silu(x, idx, a, W_gate, W_up, W_down, act="silu_glu"):
+    if act != "silu_glu":
+        return _ORIG["expert_ffn_dense"](x, idx, a, W_gate, W_up, W_down, act)
     xf = O.bf16_to_f64(x)
     y = np.zeros_like(xf)
     for t in range(xf.shape[0]):
@@ -453,6 +576,27 @@ def _mut_rmsnorm_eps_outside(y, eps=1e-6):
     return y / (np.sqrt(np.mean(y * y, axis=1, keepdims=True)) + eps)
 
 
+def _mut_relu2_unsquared(u):
+    return np.maximum(np.asarray(u, dtype=np.float64), 0.0)
+
+
+def _mut_relu2_no_relu(u):
+    return np.asarray(u, dtype=np.float64) ** 2
+
+
+def _mut_relu2_reads_gate(act, g, u):
+    # up-only experts given the gated form's SiLU of u times u
+    if act == "relu2_up":
+        return O.silu(u) * u
+    return _ORIG["activation"](act, g, u)
+
+
+def _mut_dense_relu2_transposed_up(x, idx, a, W_gate, W_up, W_down, act="silu_glu"):
+    if act == "relu2_up":  # input rows of W_up taken in reverse order
+        W_up = np.ascontiguousarray(np.asarray(W_up)[:, ::-1, :])
+    return _ORIG["expert_ffn_dense"](x, idx, a, W_gate, W_up, W_down, act)
+
+
 def _mut_dense_down_transposed(x, layer, W_down, k, d):
     Wt = np.ascontiguousarray(np.swapaxes(np.asarray(W_down), 1, 2))
     return _ORIG["moe_layer_dense_down"](x, layer, Wt, k, d)
@@ -460,7 +604,8 @@ def _mut_dense_down_transposed(x, layer, W_down, k, d):
 
 _ORIG = {name: getattr(O, name) for name in
          ("decode_vq", "expert_matrices", "silu", "gating", "select_topk", "router_logits",
-          "expert_ffn", "storage_bits_per_weight", "moe_layer_dense_down")}
+          "expert_ffn", "storage_bits_per_weight", "moe_layer_dense_down", "activation",
+          "expert_ffn_dense")}
 
 MUTATIONS = {
     "decode_element_order_reversed": ("decode_vq", _mut_decode_reversed),
@@ -477,6 +622,10 @@ MUTATIONS = {
     "dense_baseline_silu_dropped": ("expert_ffn_dense", _mut_dense_no_silu),
     "dense_down_transposed": ("moe_layer_dense_down", _mut_dense_down_transposed),
     "rmsnorm_eps_outside_sqrt": ("rmsnorm", _mut_rmsnorm_eps_outside),
+    "relu2_not_squared": ("relu2", _mut_relu2_unsquared),
+    "relu2_negative_half_kept": ("relu2", _mut_relu2_no_relu),
+    "up_only_given_silu_gating": ("activation", _mut_relu2_reads_gate),
+    "dense_relu2_up_rows_reversed": ("expert_ffn_dense", _mut_dense_relu2_transposed_up),
 }
 
 
