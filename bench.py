@@ -59,6 +59,10 @@ def parse():
                     help="instead of the benchmark line: time the Qwen3-shaped layer at batch 1 and "
                          "16 over block lengths d in {2, 4, 8} and ranks r in {0, 128, 256, 384, 512} "
                          "(the selections-versus-bytes trade-off) and print one JSON line")
+    ap.add_argument("--gateup-ab", default="",
+                    help="instead of the benchmark line: time these workloads (name or name@batch, "
+                         "comma-separated) with code-word and with projection-code-book gate/up tiles "
+                         "and print one JSON line")
     ap.add_argument("--layers", type=int, default=8, help="independently seeded layers rotated")
     ap.add_argument("--inputs", type=int, default=64,
                     help="distinct seeded inputs rotated (a multiple of --layers), so that the "
@@ -519,6 +523,35 @@ def summarize(w, r, src_hash, name=None):
     }
 
 
+def gateup_ab(C, torch, args):
+    """Code-word against projection-code-book gate/up tiles (CARDAN_GATEUP)
+    on the same layers and inputs, per workload; one JSON line."""
+    import dataclasses
+
+    from paper_2609_21137_amd.configs import WORKLOADS
+    names = [n for n in args.gateup_ab.split(",") if n]
+    rows = []
+    cache = {}
+    for name in names:
+        base, _, b = name.partition("@")
+        w = WORKLOADS[base]
+        if b:
+            w = dataclasses.replace(w, B=int(b), name=f"{base}_b{b}")
+        row = {"workload": w.name, "B": w.B, "d": w.d}
+        for form in ("codeword", "tbook", "codeword", "tbook"):  # twice, interleaved
+            os.environ["CARDAN_GATEUP"] = form
+            print(f"[gateup-ab] {w.name} {form}", file=sys.stderr, flush=True)
+            rr = time_workload(C, torch, w, args.steps, args.warmup, w.rotate_layers or 2, args.inputs, cache)
+            sm = summarize(w, rr, kernel_source_hash())
+            row.setdefault(form, []).append({"us_per_layer_median": sm["us_per_layer_median"],
+                                             "us_per_layer_ci95": sm["us_per_layer_ci95"],
+                                             "kernel_us": sm["kernel_us"]})
+        rows.append(row)
+    os.environ.pop("CARDAN_GATEUP", None)
+    print(json.dumps({"gateup_ab": "code-word vs projection-code-book gate/up tiles", "steps": args.steps,
+                      "rows": rows, "kernel_source_hash": kernel_source_hash()}))
+
+
 def sweep(C, torch, args):
     """Compressed layer latency over (d, r) at the Qwen3 shape, batches 1 and
     16, each point over two rotated layers (the touched experts of a rotation
@@ -621,6 +654,9 @@ def main():
         sys.exit(1)
     if args.calibrate_copy_mb:
         calibrate_copy(torch, args.calibrate_copy_mb)
+        return
+    if args.gateup_ab:
+        gateup_ab(C, torch, args)
         return
     if args.sweep:
         sweep(C, torch, args)

@@ -5,6 +5,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -95,6 +96,16 @@ int resident_grid(const void* fn, size_t lds, hipError_t* err) {
     have = cache[i].dev == dev && cache[i].fn == fn && cache[i].lds == lds;
   if (!have && n_cache < 64) cache[n_cache++] = {dev, fn, lds, g};
   return g;
+}
+
+// Gate/up form of a whole-layer call: the environment variable CARDAN_GATEUP
+// = "tbook" requests the projection-code-book tiles, "codeword" the
+// code-word tiles; otherwise the default below. The planner drops F_TBOOK
+// where it does not apply.
+int gateup_form(const cardan_shape*, int) {
+  const char* v = getenv("CARDAN_GATEUP");
+  if (v && strcmp(v, "tbook") == 0) return F_TBOOK;
+  return 0;
 }
 
 int check_ws(const Plan& P, const void* ws, size_t ws_bytes) {
@@ -325,13 +336,15 @@ int cardan_workspace_bytes(const cardan_shape* shape, int32_t B, size_t* out) {
   // the largest layout over batches 1..B, so one workspace serves any batch
   // up to B (split counts, hence layouts, depend on the batch)
   // and every expert-weight form (compressed, dense down, all dense) and
-  // activation (gated SiLU, up-only squared ReLU)
+  // activation (gated SiLU, up-only squared ReLU) and gate/up form (code
+  // words, projection code book)
   size_t need = 0;
   const int all = F_ROUTE | F_Z | F_GROUP | F_EXPERTS;
   for (int b = 1; b <= B; ++b) {
     for (int form : {0, (int)F_DN_DENSE, F_DN_DENSE | F_GU_DENSE})
       for (int act : {0, (int)F_UP_RELU2})
-        need = std::max(need, make_plan(shape, b, 1, all | form | act).total);
+        for (int gu : {0, (int)F_TBOOK})
+          need = std::max(need, make_plan(shape, b, 1, all | form | act | gu).total);
     need = std::max(need, step_bufs(make_plan(shape, b, 1, all | F_NORM_IN | F_SSQ_OUT)).total);
   }
   *out = need;
@@ -422,7 +435,7 @@ int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
   REQ(topk_w, "topk_w");
   if ((rc = check_layer(shape, layer, true))) return rc;
   const int z_sep = shape->r > 0 && layer->U_up != layer->U_gate;
-  const int flags = F_ROUTE | F_GROUP | F_EXPERTS | (shape->r > 0 ? F_Z : 0);
+  const int flags = F_ROUTE | F_GROUP | F_EXPERTS | (shape->r > 0 ? F_Z : 0) | gateup_form(shape, B);
   const Plan P = make_plan(shape, B, z_sep, flags);
   if ((rc = check_ws(P, ws, ws_bytes))) return rc;
   uint8_t* w = static_cast<uint8_t*>(ws);
@@ -446,7 +459,7 @@ int cardan_moe_layer_relu2(const cardan_shape* shape, int32_t B, const cardan_bf
   REQ(topk_idx, "topk_idx");
   REQ(topk_w, "topk_w");
   if ((rc = check_layer(shape, layer, true, true, false))) return rc;
-  const int flags = F_ROUTE | F_GROUP | F_EXPERTS | F_UP_RELU2 | (shape->r > 0 ? F_Z : 0);
+  const int flags = F_ROUTE | F_GROUP | F_EXPERTS | F_UP_RELU2 | (shape->r > 0 ? F_Z : 0) | gateup_form(shape, B);
   const Plan P = make_plan(shape, B, 0, flags);
   if ((rc = check_ws(P, ws, ws_bytes))) return rc;
   // the kernels read only the up projection; the gate pointers alias it so

@@ -743,6 +743,56 @@ __device__ __forceinline__ float z_sum(const Plan& P, const Args& A, int src, in
   return s;
 }
 
+// Projection-code-book item j (F_TBOOK; Sec. 4.2): token t, input-side
+// projection pj, blocks [b0, b0 + nb) of x: thread k holds code word k of the
+// projection's book and writes T[t][pj][b][k] = sum_i x[t][b*d + i] cb[k][i]
+// (float32, i ascending) for each block, 1 KB per block across the threads,
+// four blocks per round (their LDS reads issued together). Read by the next
+// kernel of the call (the stream orders it).
+template <int D>
+__device__ void tbook_rows(const Plan& P, const Args& A, int t, int pj, int b0, int nb, const float* xs) {
+  const int K = P.K, nblk = P.H / D, k = threadIdx.x;
+  if (k >= K) return;
+  const uint16_t* cb = (pj ? A.L.cb_up : A.L.cb_gate) + (size_t)k * D;
+  float c[D];
+#pragma unroll
+  for (int i = 0; i < D; ++i) c[i] = bf(cb[i]);
+  // buffer stores: the compiler cannot take them for writes to xs
+  const rsrc_t trs = make_rsrc(wsp<float>(A, tbook_offset(P)), (uint32_t)tbook_bytes(P));
+  const uint32_t o = (uint32_t)(((((size_t)t * 2 + pj) * nblk + b0) * K + k) * 4);
+  for (int bb0 = 0; bb0 < nb; bb0 += 4) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float* xb = xs + min(bb0 + u, nb - 1) * D;
+      float acc = 0.0f;
+#pragma unroll
+      for (int i = 0; i < D; ++i) acc = fmaf(xb[i], c[i], acc);
+      v[u] = acc;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (bb0 + u < nb)
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[u]), trs, o + (uint32_t)(bb0 + u) * K * 4, 0, 0);
+  }
+}
+
+__device__ void item_tbook(const Plan& P, const Args& A, int j, uint8_t* smem) {
+  const int d = P.d, nblk = P.H / d, ng = tbook_groups(P), np = n_proj(P);
+  const int g = j % ng, rest = j / ng;
+  const int pj = np == 2 ? rest % 2 : 1, t = rest / np;
+  const int b0 = g * kTBookBlocks, nb = min(kTBookBlocks, nblk - b0);
+  float* xs = reinterpret_cast<float*>(smem);  // [nb * d]
+  for (int i = threadIdx.x; i < nb * d; i += kWG) xs[i] = bf(A.x[(size_t)t * P.H + b0 * d + i]);
+  __syncthreads();
+  if (d == 8)
+    tbook_rows<8>(P, A, t, pj, b0, nb, xs);
+  else if (d == 4)
+    tbook_rows<4>(P, A, t, pj, b0, nb, xs);
+  else
+    tbook_rows<2>(P, A, t, pj, b0, nb, xs);
+}
+
 __device__ void item_z_reduce(const Plan& P, const Args& A, int i) {
   const int* zcf = wsp<const int>(A, P.o_zc_flag);
   wait_all(A, P.n_zc, [&](int f) { return ld_dev(zcf + f * kTickPad) != 0; });
@@ -806,6 +856,9 @@ struct WsAccess {
   __device__ __forceinline__ void st4(uint32_t o, float4 v) const {
     typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, o, 0, kSc1);
+  }
+  __device__ __forceinline__ void st1(uint32_t o, float v) const {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rs, o, 0, kSc1);
   }
 };
 
@@ -1318,6 +1371,62 @@ __device__ __forceinline__ void book_store_copies(uint4* cb, uint4 v) {
 // requested at once when every tile starts; large batches).
 // XP (batch 1): the token's x row and z rows were staged into LDS (xpre,
 // zpre) by the workgroup at kernel start, so the tile stages nothing.
+// Gate/up code tile (a, pj, cg, s < ns_v) on the projection code book
+// (F_TBOOK; Sec. 4.2), for an expert of at most kTBookTok tokens: thread j
+// owns column cg * 256 + j and sums T[tok][pj][b][J_e[b][col]] over the
+// split's blocks b (ascending) from T rows staged in LDS; the sum goes to the
+// same partial-sum slot as the code-word tile's. Its codes (one byte per
+// block) load before the T rows.
+template <int D>
+__device__ void item_gateup_t(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg, int s,
+                              uint8_t* smem) {
+  const Routing R = expert_of(P, RT, a);
+  const int H = P.H, I = P.I, K = P.K, nblk = H / D;
+  constexpr int BPS = 32 / D;  // blocks per K-step
+  int ks0, ks1;
+  joint_split(s, P.ns, P.ns_v, H / 32, (P.r + 31) / 32, ks0, ks1);
+  const int b0 = ks0 * BPS, nb = min(ks1 - ks0, kTBookTileBlocks / BPS) * BPS;
+  const int col = cg * kColsPerGroup + threadIdx.x;
+  const rsrc_t crs = make_rsrc((pj ? A.L.codes_up : A.L.codes_gate) + (size_t)R.e * nblk * I, (uint32_t)nblk * I);
+  const rsrc_t trs = make_rsrc(wsp<const float>(A, tbook_offset(P)), (uint32_t)tbook_bytes(P));
+  float* Ts = reinterpret_cast<float*>(smem);  // [nb][K]
+  float* gu = wsp<float>(A, P.o_gu);
+  const WsAccess ws(A, P);
+  constexpr int kT4 = kTBookTileBlocks * 256 / 4 / kWG;  // float4 T loads per thread (K <= 256)
+  const int n4 = nb * K / 4;
+  for (int t = 0; t < R.ne; ++t) {
+    // the T rows first, then the codes: loads return in order, so staging
+    // the T rows does not wait for the codes' HBM latency
+    const int tok = RT.slot_tok[R.s0 + t];
+    const uint32_t row = (uint32_t)((((size_t)tok * 2 + pj) * nblk + b0) * K * 4);
+    float4 tv[kT4];
+#pragma unroll
+    for (int u = 0; u < kT4; ++u) {
+      const int i = threadIdx.x + u * kWG;
+      tv[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(trs, i < n4 ? row + 16u * i : kOob, 0, 0));
+    }
+    uint32_t code[kTBookTileBlocks];
+#pragma unroll
+    for (int bb = 0; bb < kTBookTileBlocks; ++bb)
+      code[bb] = __builtin_amdgcn_raw_buffer_load_b8(
+          crs, bb < nb && col < I ? (uint32_t)((b0 + bb) * I + col) : kOob, 0, 0);
+#pragma unroll
+    for (int u = 0; u < kT4; ++u) {
+      const int i = threadIdx.x + u * kWG;
+      if (i < n4) reinterpret_cast<float4*>(Ts)[i] = tv[u];
+    }
+    __syncthreads();
+    float acc = 0.0f;
+#pragma unroll
+    for (int bb = 0; bb < kTBookTileBlocks; ++bb)
+      if (bb < nb) acc += Ts[bb * K + (int)code[bb]];
+    if (col < I)
+      ws.st1(ws.off(gu + (((size_t)(R.s0 + t) * 2 + pj) * P.ns + s) * I + col), acc);
+    __syncthreads();
+  }
+  publish(wsp<int>(A, P.o_gu_tick) + (a * P.ncg + cg) * kTickPad);
+}
+
 template <int D, bool LATE, int NC, bool XP, int PDC>
 __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, int a, int pj, int cg, int s,
                             bool lr_first, uint4* cbs, uint8_t* smem, const uint4* xpre, const uint4* zpre) {
@@ -1968,11 +2077,16 @@ __global__ __launch_bounds__(kWG) void k_route(Plan P, Args A, Chain C) {
     item_select(P, A, j - e_zc, smem);
     tr.done(A, P, j, 2);
   }
-  for (; j < P.n_pre; j += gridDim.x) {
+  const int e_zr = P.n_pre - P.n_tb;
+  for (; j < e_zr; j += gridDim.x) {
     __syncthreads();
     ItemTrace tr;
     item_z_reduce(P, A, j - e_sel);
     tr.done(A, P, j, 3);
+  }
+  for (; j < P.n_pre; j += gridDim.x) {
+    __syncthreads();
+    item_tbook(P, A, j - e_zr, smem);
   }
 }
 
@@ -2076,11 +2190,21 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     // first in the second half of the grid, so the two workgroups sharing a
     // CU overlap LDS-bound and HBM-bound phases
     const bool lr_first = (int)(jp % gridDim.x) >= (int)(gridDim.x >> 1);
-    if constexpr (MODE == 2)
+    if constexpr (MODE == 2) {
       item_gateup_dense(P, A, RT, t.a, t.pj, t.cg, t.s, item_smem);
-    else
+    } else {
+      // projection-code-book tiles only in the narrow compressed kernels for
+      // d = 4 and 8 (their registers stay out of the others)
+      if constexpr (MODE == 0 && DNW == 1 && D != 2) {
+        if ((P.flags & F_TBOOK) && t.s < P.ns_v && expert_of(P, RT, t.a).ne <= kTBookTok) {
+          item_gateup_t<D>(P, A, RT, t.a, t.pj, t.cg, t.s, item_smem);
+          tr.done(A, P, P.n_pre + jp, 4);
+          continue;
+        }
+      }
       item_gateup<D, DNW == 2, NC, XPRE, DNW == 2 ? kPdGateUpWide : kPdGateUp>(P, A, RT, t.a, t.pj, t.cg, t.s,
                                                                           lr_first, cbs, item_smem, xpre, zpre);
+    }
     tr.done(A, P, P.n_pre + jp, 4);
   }
   for (; jp < n_gu + n_dn; jp += gridDim.x) {

@@ -59,6 +59,10 @@ constexpr int kXpreBytes = (kXpreXGroups + 2 * kXpreZRow) * 16;
 constexpr int kZRed = 4 * 64 * 16 * 4;       // z item: [4 waves][64 lanes][16] float sums
 constexpr int kPdDenseW = 2;       // K-steps in flight per wave of a dense bf16 expert-weight tile
                                    // (measured faster than 3 at batch 1 and 16)
+constexpr int kTBookBlocks = 64;       // blocks of x per projection-code-book item of k_route
+constexpr int kTBookTok = 1;           // tokens of an expert a T-path gate/up tile takes
+constexpr int kTBookTileBlocks = 48;   // blocks of a T-path tile (its T rows fill <= 48 KB of LDS at K = 256)
+constexpr size_t kTBookMaxBytes = 64ull << 20;  // largest table the planner accepts
 
 
 // flags of one call
@@ -79,7 +83,12 @@ enum { F_ROUTE = 1, F_Z = 2, F_GROUP = 4, F_EXPERTS = 8,
        F_PREFETCH = 4096,  // idle expert-kernel workgroups touch the next layer's shared tensors
        // up-only experts with a squared-ReLU activation, p = max(u, 0)^2: no
        // gate tiles; the layer's gate pointers are not read
-       F_UP_RELU2 = 8192 };
+       F_UP_RELU2 = 8192,
+       // projection code book (Sec. 4.2): k_route builds, per token and
+       // input-side projection, T[b][k] = x[b*d .. b*d+d) . cb[k] (float32);
+       // a gate/up code tile whose expert has at most kTBookTok tokens sums
+       // T[b][J[b][j]] over its blocks instead of decoding code words on MFMA
+       F_TBOOK = 16384 };
 
 // counters at the start of the workspace, one per 64-byte slot: the status
 // count of timed-out waits
@@ -110,6 +119,7 @@ struct Plan {
   // item counts of this call
   int n_rc, n_zc, n_sel, n_zr, n_pre;
   int n_rc_flags, n_zc_flags;  // flag slots (shape-wide maxima of n_rc, n_zc)
+  int n_tb;       // projection-code-book items of k_route (F_TBOOK), the last of its items
   // workspace byte offsets
   size_t o_ctr, o_rc_flag, o_zc_flag, o_gu_tick, o_dn_done;  // counters
   size_t o_rl, o_zp, o_z, o_gu, o_dn, o_uap, total;
@@ -132,6 +142,18 @@ inline __host__ __device__ size_t combine_lds(const Plan& P) {
   const size_t cu = P.r > 0 ? ((size_t)P.k * P.nsdl + kCombineChunk - 1) / kCombineChunk : 0;
   const size_t cd = ((size_t)P.k * P.nsd + kCombineChunk - 1) / kCombineChunk;
   return combine_part_offset(P) + (size_t)P.tpc * (nq * cu + 64 * cd) * 16;
+}
+
+// Projection code book T (F_TBOOK): float32 [B][2][H/d][K] (gate, up) after
+// the low-rank partial sums, the last region of the workspace.
+__host__ __device__ inline size_t tbook_offset(const Plan& P) {
+  return (P.o_uap + (size_t)P.nsdl * P.S * P.r * 4 + 255) & ~(size_t)255;
+}
+__host__ __device__ inline size_t tbook_bytes(const Plan& P) {
+  return (size_t)P.B * 2 * (P.H / P.d) * P.K * 4;
+}
+__host__ __device__ inline int tbook_groups(const Plan& P) {
+  return (P.H / P.d + kTBookBlocks - 1) / kTBookBlocks;
 }
 
 // expert-weight form of a call: 0 compressed, 1 dense down, 2 all dense

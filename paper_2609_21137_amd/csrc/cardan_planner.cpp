@@ -56,6 +56,8 @@ size_t lds_expert(const Plan& P) {
   const int ksd = std::max(ks_max(KSD, P.nsd), ks_max(KSD, P.nsdl));
   need = std::max(need, (size_t)P.nt_max * (ksd * 8 + 1) * 16 + kWG * 2 * 16);
   need = std::max(need, combine_lds(P) + ((P.flags & F_CB_SPLITK) ? kSplitKRed : 0));
+  // T-path gate/up tiles: the T rows of their blocks for one token
+  if (P.flags & F_TBOOK) need = std::max(need, (size_t)ks_max(KSX, P.ns_v) * (32 / P.d) * P.K * 4);
   return round256(need);
 }
 
@@ -168,6 +170,24 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
       ++P.ns;
     }
   }
+  // Projection code book: only for whole-layer calls on compressed weights
+  // with d = 4 or 8, K % 4 == 0 (16-byte T rows) and a table of at most
+  // kTBookMaxBytes, in the narrow expert kernel (no F_DN_WIDE); its code splits hold at most the
+  // K-steps whose T rows fit kTBookTileBlocks blocks of 1 KB (K = 256), and
+  // the low-rank steps get splits of their own (a T-path tile has no MFMA
+  // accumulators to add them to)
+  if ((P.flags & F_TBOOK) &&
+      (mode != 0 || !(P.flags & F_ROUTE) || (P.flags & F_NORM_IN) || P.d == 2 || P.K % 4 ||
+       tbook_bytes(P) > kTBookMaxBytes))
+    P.flags &= ~F_TBOOK;
+  if (P.flags & F_TBOOK) {
+    const int bps = 32 / P.d;
+    const int nbt = std::min(kTBookTileBlocks, (int)(48 * 1024 / ((size_t)P.K * 4)));
+    const int ks_t = std::max(1, nbt / bps);
+    const int nl = KSZ > 0 ? std::max(1, P.ns - P.ns_v) : 0;
+    P.ns_v = std::min(KSX, std::max(P.ns_v, ceil_div(KSX, ks_t)));
+    P.ns = P.ns_v + nl;
+  }
   auto down_fits = [&](int n) {
     return (size_t)P.nt_max * (ks_max(KSD, n) * 8 + 1) * 16 + kWG * 2 * 16 <= kLdsBudget;
   };
@@ -181,7 +201,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   // reads serve twice the columns and the down tiles take half the
   // workgroup slots (fewer rounds, longer tiles)
   const double items_all = exp_act * (npj * P.ncg * P.ns + P.ncgh * P.nsd + P.ncgr * P.nsdl);
-  if (mode == 0 && items_all > 2 * 512.0 && P.ncgh > 1 && P.d == 8) P.flags |= F_DN_WIDE;
+  if (mode == 0 && items_all > 2 * 512.0 && P.ncgh > 1 && P.d == 8 && !(P.flags & F_TBOOK)) P.flags |= F_DN_WIDE;
 
   // Small batches at ranks above 128: B^T u streams more of B than a
   // combine tile primes before its wait, so the tiles shrink to 64 columns
@@ -197,7 +217,8 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.n_zc = (flags & F_Z) ? z_items : 0;
   P.n_sel = (flags & F_ROUTE) ? B : 0;
   P.n_zr = (flags & F_Z) ? ceil_div(2 * B * P.r, kWG) : 0;
-  P.n_pre = P.n_rc + P.n_zc + P.n_sel + P.n_zr;
+  P.n_tb = (P.flags & F_TBOOK) ? B * n_proj(P) * tbook_groups(P) : 0;
+  P.n_pre = P.n_rc + P.n_zc + P.n_sel + P.n_zr + P.n_tb;
 
   // Counters first, at offsets that depend only on H, I and E (not on B,
   // r or the expert-weight form): a call leaves its expert ticks set until
@@ -217,6 +238,7 @@ Plan make_plan(const cardan_shape* s, int B, int z_sep, int flags) {
   P.o_gu = o; o = align256(o + (size_t)P.S * 2 * P.ns * P.I * 4);
   P.o_dn = o; o = align256(o + (size_t)P.nsd * P.S * P.H * 4);
   P.o_uap = o; o = align256(o + (size_t)P.nsdl * P.S * P.r * 4);
+  if (P.flags & F_TBOOK) o = tbook_offset(P) + tbook_bytes(P);
   P.total = o;
   P.lds_route = lds_route(P);
   // routing tables: active-expert records and four per-slot arrays

@@ -94,6 +94,26 @@ static void check_plan(const cardan_shape& s, int B, int z_sep, int flags, Count
   CHECK(P.lds_expert > P.lds_routing);
   if (P.flags & F_XPRE) CHECK(B == 1 && mode == 0 && P.H <= 8 * kXpreXGroups);
   if (P.flags & F_DN_WIDE) CHECK(mode == 0 && P.d == 8);
+  // projection code book: code splits whose T rows fit the tile's LDS area,
+  // low-rank steps in splits of their own, the table last in the workspace
+  if (P.flags & F_TBOOK) {
+    const int bps = 32 / P.d;
+    CHECK(mode == 0 && P.K % 4 == 0 && (P.flags & F_ROUTE) && !(P.flags & F_NORM_IN));
+    CHECK(P.d != 2 && !(P.flags & F_DN_WIDE));
+    CHECK(tbook_offset(P) >= P.o_uap + (size_t)P.nsdl * P.S * P.r * 4);
+    CHECK(P.total == tbook_offset(P) + tbook_bytes(P) && tbook_bytes(P) <= kTBookMaxBytes);
+    CHECK(P.n_tb == B * n_proj(P) * tbook_groups(P));
+    CHECK(P.n_pre == P.n_rc + P.n_zc + P.n_sel + P.n_zr + P.n_tb);
+    for (int sp = 0; sp < P.ns_v; ++sp) {
+      int k0, k1;
+      joint_split(sp, P.ns, P.ns_v, KSX, KSZ, k0, k1);
+      CHECK(k1 <= KSX && (k1 - k0) * bps <= kTBookTileBlocks);
+      CHECK((size_t)(k1 - k0) * bps * P.K * 4 <=
+            P.lds_expert - P.lds_routing - ((P.flags & F_XPRE) ? kXpreBytes : 0));
+    }
+  } else {
+    CHECK(P.n_tb == 0);
+  }
   // item counts fit the kernels' int arithmetic
   const double items = (double)P.max_act * (gateup_tiles_per_expert(P) + down_tiles_per_expert(P)) + P.n_cb;
   CHECK(items < 2.0e9);
@@ -159,7 +179,10 @@ int main(int argc, char** argv) {
       // up-only squared-ReLU experts, compressed and dense
       check_plan(s, B, 0, all | F_UP_RELU2, &ref);
       check_plan(s, B, 0, F_ROUTE | F_GROUP | F_EXPERTS | F_DN_DENSE | F_GU_DENSE | F_UP_RELU2, &ref);
-      plans += 7;
+      // projection-code-book gate/up tiles (gated and up-only)
+      check_plan(s, B, 0, all | F_TBOOK, &ref);
+      check_plan(s, B, 1, all | F_TBOOK | F_UP_RELU2, &ref);
+      plans += 9;
     }
   }
   printf("%ld plans checked, %d failures\n", plans, g_fail);
