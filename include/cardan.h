@@ -161,7 +161,13 @@ int cardan_vq_lr_expert_ffn(const cardan_shape* shape, int32_t B, const cardan_b
  * Sec. 4.2): route + top-k + gating as cardan_route_topk, z = U^T x as
  * cardan_shared_proj, then the grouped expert computation and weighted
  * combine of cardan_vq_lr_expert_ffn. Writes y [B][H] float32 and the
- * routing topk_idx [B][top_k] int32, topk_w [B][top_k] float32. */
+ * routing topk_idx [B][top_k] int32, topk_w [B][top_k] float32.
+ * Gate/up form: the VQ part is decoded from code words on the matrix cores;
+ * with the environment variable CARDAN_GATEUP=tbook (read at every call of
+ * this entry point and of cardan_moe_layer_relu2) one-token experts sum the
+ * per-token projection code book T[b][k] = x_b . cb_k of Sec. 4.2 instead
+ * (d = 4 or 8, K a multiple of 4, at most 64 MiB of T; otherwise the code
+ * words). Both give the same result up to float32 rounding. */
 int cardan_moe_layer(const cardan_shape* shape, int32_t B, const cardan_bf16* x,
                      const cardan_layer* layer, float* y, int32_t* topk_idx, float* topk_w,
                      void* ws, size_t ws_bytes, hipStream_t stream);
