@@ -17,7 +17,7 @@
 
 namespace cardan {
 const void* route_kernel();
-const void* expert_kernel(int d, int dnw, int mode, bool csk, bool xpre);
+const void* expert_kernel(const Plan& P);
 hipError_t launch_route(const Plan&, const Args&, const Chain&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_expert(const Plan&, const Args&, const Chain&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t);
 hipError_t launch_route_reset(const Plan&, const Args&, hipStream_t);
@@ -245,9 +245,7 @@ int run_layer(const Plan& P, const Args& A, hipStream_t stream, const Chain* cha
     }
   }
   if (P.flags & F_EXPERTS) {
-    const int cap = resident_grid(expert_kernel(P.d, dn_width(P), expert_mode(P), (P.flags & F_CB_SPLITK) != 0,
-                                                (P.flags & F_XPRE) != 0),
-                                  P.lds_expert, &err);
+    const int cap = resident_grid(expert_kernel(P), P.lds_expert, &err);
     if (cap <= 0) return hip_fail(err, "occupancy query");
     Timed tm(stream, CARDAN_KERNEL_EXPERT);
     err = launch_expert(P, A, C, cap, P.lds_expert, stream, tm.ev0, tm.ev1);

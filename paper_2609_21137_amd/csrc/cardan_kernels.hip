@@ -259,16 +259,17 @@ __device__ __forceinline__ float norm_inv(const Plan& P, const Chain& C, int t) 
   return 1.0f / sqrtf(s / (float)P.H + C.eps);
 }
 
-// Router chunk (c, g, tb): partial logits over hidden rows [64c, 64c + 64)
-// for experts [64g, 64g + 64) of tokens [4tb, 4tb + 4). Lane l of wave w owns
-// expert 64g + l and rows 64c + 16w .. + 16 (rows past H read zeros); float64
-// FMAs of exact bf16 products in row order per token, then the four waves'
-// partials are added in wave order through LDS.
-static_assert(kRouterTok * kRowsRouter <= kWG, "a router chunk's inputs are one per thread");
+// Router chunk (c, g, tb): partial logits over hidden rows [R c, R c + R)
+// (R = kRowsRouter) for experts [64g, 64g + 64) of tokens [4tb, 4tb + 4).
+// Lane l of wave w owns expert 64g + l and rows R c + (R/4) w .. + R/4 (rows
+// past H read zeros; all of its weights are loaded up front); float64 FMAs of
+// exact bf16 products in row order per token, in groups of 16 rows, then the
+// four waves' partials are added in wave order through LDS.
 __device__ void item_router_chunk(const Plan& P, const Args& A, const Chain& C, int item, int c, int g, int tb,
                                   uint8_t* smem) {
   constexpr int RW = kRowsRouter / 4;  // rows per wave
-  float* xs = reinterpret_cast<float*>(smem);                                     // [4][64]
+  static_assert(RW % 16 == 0, "rows per wave in groups of 16");
+  float* xs = reinterpret_cast<float*>(smem);                                     // [4][R]
   double* part = reinterpret_cast<double*>(smem + kRouterTok * kRowsRouter * 4);  // [4][4][64]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int E = P.E, H = P.H, B = P.B, h0 = c * kRowsRouter;
@@ -284,23 +285,30 @@ __device__ void item_router_chunk(const Plan& P, const Args& A, const Chain& C, 
   const int tg = tb * kRouterTok, nt = min(kRouterTok, B - tg);
   if (P.flags & F_NORM_IN) {
     // x = bf16(y * inv_rms) of the previous layer's output; items of expert
-    // group 0 also write it for the expert kernel. A thread's y value
-    // (nt * 64 <= kWG) loads together with the partial sums behind inv_rms.
+    // group 0 also write it for the expert kernel. The y values load
+    // together with the partial sums behind inv_rms.
+    constexpr int NI = (kRouterTok * kRowsRouter + kWG - 1) / kWG;  // inputs per thread
     float* sinv = reinterpret_cast<float*>(part + 4 * kRouterTok * 64);  // [4]
-    const int t = tid / kRowsRouter, h = tid % kRowsRouter;
-    const bool in = t < nt && h0 + h < H;
-    const size_t o = (size_t)(tg + t) * H + h0 + h;
-    const float yv = in ? C.y_in[o] : 0.0f;
+    float yv[NI];
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+      const int i = tid + u * kWG, t = i / kRowsRouter, h = i % kRowsRouter;
+      yv[u] = t < nt && h0 + h < H ? C.y_in[(size_t)(tg + t) * H + h0 + h] : 0.0f;
+    }
     if (tid < nt) sinv[tid] = norm_inv(P, C, tg + tid);
     __syncthreads();
-    if (t < nt) {
-      float v = 0.0f;
-      if (in) {
-        const uint32_t b = rne_bf16(yv * sinv[t]);
-        v = bf(b);
-        if (g == 0) C.x_norm[o] = (uint16_t)b;
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+      const int i = tid + u * kWG, t = i / kRowsRouter, h = i % kRowsRouter;
+      if (t < nt) {
+        float v = 0.0f;
+        if (h0 + h < H) {
+          const uint32_t b = rne_bf16(yv[u] * sinv[t]);
+          v = bf(b);
+          if (g == 0) C.x_norm[(size_t)(tg + t) * H + h0 + h] = (uint16_t)b;
+        }
+        xs[i] = v;
       }
-      xs[tid] = v;
     }
   } else {
     for (int i = tid; i < nt * kRowsRouter; i += kWG) {
@@ -310,9 +318,6 @@ __device__ void item_router_chunk(const Plan& P, const Args& A, const Chain& C, 
   }
   __syncthreads();
   trace_mark(0);
-  double wd[RW];
-#pragma unroll
-  for (int i = 0; i < RW; ++i) wd[i] = (double)bf(wv[i]);
   for (int t = 0; t < nt; ++t) {
     // the wave's inputs of token t: the same LDS words for every lane
     const float4* xr = reinterpret_cast<const float4*>(xs + t * kRowsRouter + RW * w);
@@ -320,10 +325,10 @@ __device__ void item_router_chunk(const Plan& P, const Args& A, const Chain& C, 
 #pragma unroll
     for (int q = 0; q < RW / 4; ++q) {
       const float4 xq = xr[q];
-      a0 = fma(wd[4 * q + 0], (double)xq.x, a0);
-      a1 = fma(wd[4 * q + 1], (double)xq.y, a1);
-      a2 = fma(wd[4 * q + 2], (double)xq.z, a2);
-      a3 = fma(wd[4 * q + 3], (double)xq.w, a3);
+      a0 = fma((double)bf(wv[4 * q + 0]), (double)xq.x, a0);
+      a1 = fma((double)bf(wv[4 * q + 1]), (double)xq.y, a1);
+      a2 = fma((double)bf(wv[4 * q + 2]), (double)xq.z, a2);
+      a3 = fma((double)bf(wv[4 * q + 3]), (double)xq.w, a3);
     }
     part[(w * kRouterTok + t) * 64 + lane] = (a0 + a1) + (a2 + a3);
   }
@@ -1180,13 +1185,10 @@ __device__ __forceinline__ void put_split_quad(uint4* row, int q, float4 v) {
 // over the ns splits in split order, staged as bf16 hi/lo quads. U units
 // (token, quad) per thread per round and NSC splits per load batch keep 16
 // loads in flight.
-template <int U, int NSC>
+template <int U, int NSC, bool RELU2>
 __device__ __forceinline__ void stage_p(const WsAccess& ws, const Plan& P, uint4* ops, int ld, int nt, int nquad,
                                         int slot0, int col0) {
   const int ns = P.ns, I = P.I, n = nt * nquad;
-  // up-only experts: the gate partials are never written, and their loads
-  // take the out-of-range offset (zeros, no memory access)
-  const bool relu2 = (P.flags & F_UP_RELU2) != 0;
   for (int i0 = threadIdx.x; i0 < n; i0 += U * kWG) {
     float4 g[U], u[U];
     uint32_t base[U];
@@ -1205,8 +1207,10 @@ __device__ __forceinline__ void stage_p(const WsAccess& ws, const Plan& P, uint4
         for (int pj = 0; pj < 2; ++pj)
 #pragma unroll
           for (int sc = 0; sc < NSC; ++sc)
-            v[uu][pj][sc] = ws.f4(s0 + sc < ns && (pj || !relu2) ? base[uu] + (uint32_t)((pj * ns + s0 + sc) * I * 4)
-                                                                 : kOob);
+            // up-only experts: no gate partials, whose loads take the
+            // out-of-range offset (zeros, no memory access)
+            v[uu][pj][sc] = ws.f4(s0 + sc < ns && (pj || !RELU2) ? base[uu] + (uint32_t)((pj * ns + s0 + sc) * I * 4)
+                                                                  : kOob);
 #pragma unroll
       for (int uu = 0; uu < U; ++uu)
 #pragma unroll
@@ -1223,7 +1227,7 @@ __device__ __forceinline__ void stage_p(const WsAccess& ws, const Plan& P, uint4
       if (i >= n) continue;
       const float4 x = g[uu], y = u[uu];
       float4 p;
-      if (relu2) {
+      if constexpr (RELU2) {
         const float4 c = make_float4(fmaxf(y.x, 0.f), fmaxf(y.y, 0.f), fmaxf(y.z, 0.f), fmaxf(y.w, 0.f));
         p = make_float4(c.x * c.x, c.y * c.y, c.z * c.z, c.w * c.w);
       } else {
@@ -1587,7 +1591,21 @@ __device__ void item_gateup(const Plan& P, const Args& A, const RouteTab& RT, in
 // columns of r (A_e^T p -> uap[s], nsdl splits: the coefficient bytes of a
 // K-step are 16x the code bytes). Weight loads are issued before waiting
 // for the expert's p.
-template <typename Prime, typename Stage, typename Run, typename Dst>
+// stage_p with U and NSC for 16 loads in flight at the plan's split count
+template <bool RELU2>
+__device__ __forceinline__ void stage_p_ns(const WsAccess& ws, const Plan& P, uint4* ps, int ld, int nt, int nquad,
+                                           int slot0, int col0) {
+  if (P.ns <= 1)
+    stage_p<8, 1, RELU2>(ws, P, ps, ld, nt, nquad, slot0, col0);
+  else if (P.ns <= 2)
+    stage_p<4, 2, RELU2>(ws, P, ps, ld, nt, nquad, slot0, col0);
+  else if (P.ns <= 4)
+    stage_p<2, 4, RELU2>(ws, P, ps, ld, nt, nquad, slot0, col0);
+  else
+    stage_p<1, 8, RELU2>(ws, P, ps, ld, nt, nquad, slot0, col0);
+}
+
+template <bool RELU2, typename Prime, typename Stage, typename Run, typename Dst>
 __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Routing& R, int a, int ks0, int ks1,
                                           int c0, int n_out, Prime prime, Stage stage, Run run, Dst dst,
                                           uint8_t* smem) {
@@ -1605,14 +1623,7 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
     __syncthreads();
     stage();
     const int nquad = (ks1 - ks0) * 8, slot0 = R.s0 + tg, col0 = ks0 * 32;
-    if (P.ns <= 1)
-      stage_p<8, 1>(ws, P, ps, ld, nt, nquad, slot0, col0);
-    else if (P.ns <= 2)
-      stage_p<4, 2>(ws, P, ps, ld, nt, nquad, slot0, col0);
-    else if (P.ns <= 4)
-      stage_p<2, 4>(ws, P, ps, ld, nt, nquad, slot0, col0);
-    else
-      stage_p<1, 8>(ws, P, ps, ld, nt, nquad, slot0, col0);
+    stage_p_ns<RELU2>(ws, P, ps, ld, nt, nquad, slot0, col0);
     __syncthreads();
     trace_mark(0);
     f32x4 acc[4];
@@ -1622,7 +1633,7 @@ __device__ __forceinline__ void down_body(const Plan& P, const Args& A, const Ro
   }
 }
 
-template <int NACC, typename Prime, typename Stage, typename Run, typename Finish>
+template <bool RELU2, int NACC, typename Prime, typename Stage, typename Run, typename Finish>
 __device__ __forceinline__ void down_body_wide(const Plan& P, const Args& A, const Routing& R, int a, int ks0, int ks1,
                                           Prime prime, Stage stage, Run run, Finish finish, uint8_t* smem) {
   prime();
@@ -1639,14 +1650,7 @@ __device__ __forceinline__ void down_body_wide(const Plan& P, const Args& A, con
     __syncthreads();
     stage();
     const int nquad = (ks1 - ks0) * 8, slot0 = R.s0 + tg, col0 = ks0 * 32;
-    if (P.ns <= 1)
-      stage_p<8, 1>(ws, P, ps, ld, nt, nquad, slot0, col0);
-    else if (P.ns <= 2)
-      stage_p<4, 2>(ws, P, ps, ld, nt, nquad, slot0, col0);
-    else if (P.ns <= 4)
-      stage_p<2, 4>(ws, P, ps, ld, nt, nquad, slot0, col0);
-    else
-      stage_p<1, 8>(ws, P, ps, ld, nt, nquad, slot0, col0);
+    stage_p_ns<RELU2>(ws, P, ps, ld, nt, nquad, slot0, col0);
     __syncthreads();
     trace_mark(0);
     f32x4 acc[NACC];
@@ -1657,7 +1661,7 @@ __device__ __forceinline__ void down_body_wide(const Plan& P, const Args& A, con
   }
 }
 
-template <int D>
+template <int D, bool RELU2>
 __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgx, int s,
                              uint4* cbs, uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);
@@ -1669,7 +1673,7 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
   // d = 2 holds four code rows per K-step: half the steps in flight (same registers as d = 4)
   VqPipe<D, 2, D == 2 ? kPdVq / 2 : kPdVq> pipe;
   uint4 bk;
-  down_body(P, A, R, a, ks0, ks1, c0, H,
+  down_body<RELU2>(P, A, R, a, ks0, ks1, c0, H,
             [&]() {
               bk = book_load<D>(A.L.cb_down, P.K);
               __builtin_amdgcn_sched_barrier(0);
@@ -1683,7 +1687,7 @@ __device__ void item_down_vq(const Plan& P, const Args& A, const RouteTab& RT, i
 
 // VQ down tile over two column groups (cgx, cgx + 1): as item_down_vq, each
 // wave on 64 columns of both groups.
-template <int D>
+template <int D, bool RELU2>
 __device__ void item_down_vq2(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgx, int s,
                               uint4* cbs, uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);
@@ -1694,7 +1698,7 @@ __device__ void item_down_vq2(const Plan& P, const Args& A, const RouteTab& RT, 
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
   VqPipe2<D, kPdVq, kBookCopies> pipe;
   uint4 bk;
-  down_body_wide<8>(P, A, R, a, ks0, ks1,
+  down_body_wide<RELU2, 8>(P, A, R, a, ks0, ks1,
                [&]() {
                  bk = book_load<D>(A.L.cb_down, P.K);
                  __builtin_amdgcn_sched_barrier(0);
@@ -1720,6 +1724,7 @@ __device__ void item_down_vq2(const Plan& P, const Args& A, const RouteTab& RT, 
 // Low-rank down tile (a, cgr, s): partial A_e^T p over split s of I. The
 // last of the expert's ncgr * nsdl tiles sums the splits into u_e[slot]
 // (r values per slot) and flags the expert's low-rank part done.
+template <bool RELU2>
 __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgr, int s,
                              uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);
@@ -1729,7 +1734,7 @@ __device__ void item_down_lr(const Plan& P, const Args& A, const RouteTab& RT, i
   const uint16_t* Ae = A.L.A_down + (size_t)R.e * I * r;
   float* uap = wsp<float>(A, P.o_uap);
   DensePipe<2, kPdDense> pipe;
-  down_body(P, A, R, a, ks0, ks1, c0, r, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); }, [&]() {},
+  down_body<RELU2>(P, A, R, a, ks0, ks1, c0, r, [&]() { pipe.prime(Ae, r, c0, r, I, ks0, ks1); }, [&]() {},
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(ps, ld, ks0, nt, acc); },
             [&](int slot) { return uap + ((size_t)s * S + slot) * r; }, smem);
   // the combine sums the nsdl partials of u_e itself
@@ -1786,6 +1791,7 @@ __device__ void item_gateup_dense(const Plan& P, const Args& A, const RouteTab& 
 
 // Dense down tile (a, cgx, s): 256 output columns of W_down[e] [I][H] over
 // split s of I, partial sums into dn[s] as the VQ down tile.
+template <bool RELU2>
 __device__ void item_down_dense(const Plan& P, const Args& A, const RouteTab& RT, int a, int cgx, int s,
                                 uint8_t* smem) {
   const Routing R = expert_of(P, RT, a);
@@ -1795,7 +1801,7 @@ __device__ void item_down_dense(const Plan& P, const Args& A, const RouteTab& RT
   const uint16_t* W = reinterpret_cast<const uint16_t*>(A.L.codes_down) + (size_t)R.e * I * H;
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
   DensePipe<2, kPdDenseW> pipe;
-  down_body(P, A, R, a, ks0, ks1, c0, H, [&]() { pipe.prime(W, H, c0, H, I, ks0, ks1); }, [&]() {},
+  down_body<RELU2>(P, A, R, a, ks0, ks1, c0, H, [&]() { pipe.prime(W, H, c0, H, I, ks0, ks1); }, [&]() {},
             [&](const uint4* ps, int ld, int nt, f32x4* acc) { pipe.run(ps, ld, ks0, nt, acc); },
             [&](int slot) { return dn + (size_t)slot * H; }, smem);
   publish(wsp<int>(A, P.o_dn_done) + (R.e * (P.ncgh + 1) + cgx) * kTickPad);
@@ -2104,8 +2110,12 @@ __global__ __launch_bounds__(kWG) void k_route_reset(Plan P, Args A) {
 // CSK: combine tiles split over the ranks of B^T u (large r, small batches).
 // XPRE (batch 1): the token's x and z rows are loaded at kernel start, while
 // the routing tables build, into an LDS area at the end of dynamic LDS.
-template <int D, int DNW, int MODE, bool CSK, bool XPRE>
+// VAR: kVarRelu2 (up-only squared-ReLU experts) and kVarTBook (projection-
+// code-book gate/up tiles) bits, each a separate instantiation so that the
+// gated code-word kernels carry no code of either.
+template <int D, int DNW, int MODE, bool CSK, bool XPRE, int VAR>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k_expert(Plan P, Args A, Chain C) {
+  constexpr bool RELU2 = (VAR & kVarRelu2) != 0, TBOOK = (VAR & kVarTBook) != 0;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   // the code book of the current item (zero-padded to 256 words), in
   // kBookCopies copies in the large-batch kernel
@@ -2193,9 +2203,9 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     if constexpr (MODE == 2) {
       item_gateup_dense(P, A, RT, t.a, t.pj, t.cg, t.s, item_smem);
     } else {
-      // projection-code-book tiles only in the narrow compressed kernels for
-      // d = 4 and 8 (their registers stay out of the others)
-      if constexpr (MODE == 0 && DNW == 1 && D != 2) {
+      // projection-code-book tiles (their own instantiations: the code-word
+      // kernels carry none of their code)
+      if constexpr (TBOOK) {
         if ((P.flags & F_TBOOK) && t.s < P.ns_v && expert_of(P, RT, t.a).ne <= kTBookTok) {
           item_gateup_t<D>(P, A, RT, t.a, t.pj, t.cg, t.s, item_smem);
           tr.done(A, P, P.n_pre + jp, 4);
@@ -2213,14 +2223,14 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void k
     const int j = jp - n_gu, a = j / tdn, rem = j % tdn;
     if (rem < nvq) {
       if constexpr (MODE != 0)
-        item_down_dense(P, A, RT, a, rem / P.nsd, rem % P.nsd, item_smem);
+        item_down_dense<RELU2>(P, A, RT, a, rem / P.nsd, rem % P.nsd, item_smem);
       else if constexpr (DNW == 2)
-        item_down_vq2<D>(P, A, RT, a, rem / P.nsd * 2, rem % P.nsd, cbs, item_smem);
+        item_down_vq2<D, RELU2>(P, A, RT, a, rem / P.nsd * 2, rem % P.nsd, cbs, item_smem);
       else
-        item_down_vq<D>(P, A, RT, a, rem / P.nsd, rem % P.nsd, cbs, item_smem);
+        item_down_vq<D, RELU2>(P, A, RT, a, rem / P.nsd, rem % P.nsd, cbs, item_smem);
       tr.done(A, P, P.n_pre + jp, 5);
     } else {
-      item_down_lr(P, A, RT, a, (rem - nvq) / P.nsdl, (rem - nvq) % P.nsdl, item_smem);
+      item_down_lr<RELU2>(P, A, RT, a, (rem - nvq) / P.nsdl, (rem - nvq) % P.nsdl, item_smem);
       tr.done(A, P, P.n_pre + jp, 6);
     }
   }
@@ -2295,23 +2305,42 @@ __global__ __launch_bounds__(kWG) void k_rmsnorm(int H, const float* __restrict_
 // ---------------------------------------------------------------------------
 const void* route_kernel() { return reinterpret_cast<const void*>(&k_route); }
 
-template <int D, int DNW, int MODE, bool CSK, bool XPRE>
+template <int D, int DNW, int MODE, bool CSK, bool XPRE, int VAR>
 const void* kx() {
-  return reinterpret_cast<const void*>(&k_expert<D, DNW, MODE, CSK, XPRE>);
+  return reinterpret_cast<const void*>(&k_expert<D, DNW, MODE, CSK, XPRE, VAR>);
 }
 
-template <int D>
+template <int D, int VAR>
 const void* kx_compressed(bool csk, bool xpre) {
-  return csk ? (xpre ? kx<D, 1, 0, true, true>() : kx<D, 1, 0, true, false>())
-             : (xpre ? kx<D, 1, 0, false, true>() : kx<D, 1, 0, false, false>());
+  return csk ? (xpre ? kx<D, 1, 0, true, true, VAR>() : kx<D, 1, 0, true, false, VAR>())
+             : (xpre ? kx<D, 1, 0, false, true, VAR>() : kx<D, 1, 0, false, false, VAR>());
 }
 
-const void* expert_kernel(int d, int dnw, int mode, bool csk, bool xpre) {
-  if (mode == 2) return kx<8, 1, 2, false, false>();
+template <int VAR>
+const void* kx_by_d(int d, bool csk, bool xpre) {
+  return d == 8 ? kx_compressed<8, VAR>(csk, xpre) : d == 4 ? kx_compressed<4, VAR>(csk, xpre)
+                                                            : kx_compressed<2, VAR>(csk, xpre);
+}
+
+// The instantiation a plan runs: the dense forms and the wide large-batch
+// kernel per activation; the narrow compressed kernels per (d, csk, xpre)
+// and activation, with projection-code-book tiles (d = 4, 8; never wide)
+// where the plan has them.
+const void* expert_kernel(const Plan& P) {
+  const bool relu2 = (P.flags & F_UP_RELU2) != 0, tb = (P.flags & F_TBOOK) != 0;
+  const bool csk = (P.flags & F_CB_SPLITK) != 0, xpre = (P.flags & F_XPRE) != 0;
+  const int mode = expert_mode(P), d = P.d;
+  if (mode == 2) return relu2 ? kx<8, 1, 2, false, false, kVarRelu2>() : kx<8, 1, 2, false, false, 0>();
   if (mode == 1)
-    return d == 8 ? kx<8, 1, 1, false, false>() : d == 4 ? kx<4, 1, 1, false, false>() : kx<2, 1, 1, false, false>();
-  if (d == 8 && dnw == 2) return kx<8, 2, 0, false, false>();
-  return d == 8 ? kx_compressed<8>(csk, xpre) : d == 4 ? kx_compressed<4>(csk, xpre) : kx_compressed<2>(csk, xpre);
+    return d == 8 ? kx<8, 1, 1, false, false, 0>() : d == 4 ? kx<4, 1, 1, false, false, 0>()
+                                                             : kx<2, 1, 1, false, false, 0>();
+  if (d == 8 && dn_width(P) == 2) return relu2 ? kx<8, 2, 0, false, false, kVarRelu2>() : kx<8, 2, 0, false, false, 0>();
+  if (tb && d != 2) {
+    constexpr int T = kVarTBook, TR = kVarTBook | kVarRelu2;
+    if (d == 8) return relu2 ? kx_compressed<8, TR>(csk, xpre) : kx_compressed<8, T>(csk, xpre);
+    return relu2 ? kx_compressed<4, TR>(csk, xpre) : kx_compressed<4, T>(csk, xpre);
+  }
+  return relu2 ? kx_by_d<kVarRelu2>(d, csk, xpre) : kx_by_d<0>(d, csk, xpre);
 }
 
 // With a start/stop event pair the launch records them as part of the
@@ -2339,8 +2368,7 @@ hipError_t launch_route_reset(const Plan& P, const Args& A, hipStream_t st) {
 hipError_t launch_expert(const Plan& P, const Args& A, const Chain& C, int grid, size_t lds, hipStream_t st,
                          hipEvent_t ev0, hipEvent_t ev1) {
   // the instantiation expert_kernel() names, launched with its own arguments
-  const void* fn = expert_kernel(P.d, dn_width(P), expert_mode(P), (P.flags & F_CB_SPLITK) != 0,
-                                 (P.flags & F_XPRE) != 0);
+  const void* fn = expert_kernel(P);
   Plan p = P;
   Args a = A;
   Chain c = C;

@@ -59,6 +59,7 @@ constexpr int kXpreBytes = (kXpreXGroups + 2 * kXpreZRow) * 16;
 constexpr int kZRed = 4 * 64 * 16 * 4;       // z item: [4 waves][64 lanes][16] float sums
 constexpr int kPdDenseW = 2;       // K-steps in flight per wave of a dense bf16 expert-weight tile
                                    // (measured faster than 3 at batch 1 and 16)
+constexpr int kVarRelu2 = 1, kVarTBook = 2;  // k_expert variant bits (activation, gate/up form)
 constexpr int kTBookBlocks = 64;       // blocks of x per projection-code-book item of k_route
 constexpr int kTBookTok = 1;           // tokens of an expert a T-path gate/up tile takes
 constexpr int kTBookTileBlocks = 48;   // blocks of a T-path tile (its T rows fill <= 48 KB of LDS at K = 256)

@@ -8,7 +8,7 @@
 
 namespace cardan {
 const void* route_kernel() { return nullptr; }
-const void* expert_kernel(int, int, int, bool, bool) { return nullptr; }
+const void* expert_kernel(const Plan&) { return nullptr; }
 hipError_t launch_route(const Plan&, const Args&, const Chain&, int, size_t, hipStream_t, hipEvent_t, hipEvent_t) {
   return hipErrorInvalidDeviceFunction;
 }
