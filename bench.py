@@ -77,6 +77,9 @@ def parse():
                          "'k_expert<8, 1, 2>' for the dense layer's expert kernel)")
     ap.add_argument("--pmc-name", default=None,
                     help="--summarize-pmc: record name (default: --workload)")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="CSV",
+                    help="print the mean per dispatch of every (kernel, counter) pair in rocprofv3 "
+                         "--pmc counter CSVs as one JSON line, then exit")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
@@ -603,6 +606,24 @@ def _pmc_means(path):
     return {k: (len(v), sum(v) / len(v)) for k, v in acc.items()}
 
 
+def summarize_counters(paths):
+    """Mean value per dispatch of each counter of each cardan kernel in
+    rocprofv3 --pmc counter CSVs (several counters per run)."""
+    import csv
+    acc = {}
+    for path in paths:
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if "cardan" not in row["Kernel_Name"]:
+                    continue
+                key = (row["Kernel_Name"], row["Counter_Name"])
+                acc.setdefault(key, []).append(float(row["Counter_Value"]))
+    out = {}
+    for (k, c), v in sorted(acc.items()):
+        out.setdefault(k, {"dispatches": len(v)})[c] = round(sum(v) / len(v), 3)
+    print(json.dumps({"kernel_source_hash": kernel_source_hash(), "per_dispatch_mean": out}))
+
+
 def summarize_pmc(args):
     """HBM bytes per k_expert launch: FETCH_SIZE and WRITE_SIZE per dispatch,
     each scaled by what the same counter reads for a plain copy of known size."""
@@ -625,7 +646,8 @@ def summarize_pmc(args):
         "hbm_write_bytes_per_launch": round(write[name][1] * 1024 * w_scale),
     }
     rec["hbm_bytes_per_launch"] = rec["hbm_read_bytes_per_launch"] + rec["hbm_write_bytes_per_launch"]
-    out = os.path.join(ROOT, "profiles", f"k_expert_{wl}_pmc.json")
+    kshort = "k_route" if "k_route" in name else "k_expert"
+    out = os.path.join(ROOT, "profiles", f"{kshort}_{wl}_pmc.json")
     with open(out, "w") as f:
         json.dump(rec, f, indent=1)
         f.write("\n")
@@ -634,6 +656,9 @@ def summarize_pmc(args):
 
 def main():
     args = parse()
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
+        return
     if args.summarize_pmc:
         if not args.calibrate_copy_mb:
             print("--summarize-pmc needs --calibrate-copy-mb (the calibration copy size)",
