@@ -1696,7 +1696,7 @@ __device__ void item_down_vq2(const Plan& P, const Args& A, const RouteTab& RT, 
   const int c0 = cgx * kColsPerGroup + (threadIdx.x >> 6) * 64;
   const uint8_t* codes = A.L.codes_down + (size_t)R.e * (I / D) * H;
   float* dn = wsp<float>(A, P.o_dn) + (size_t)s * S * H;
-  VqPipe2<D, kPdVq, kBookCopies> pipe;
+  VqPipe2<D, kPdVqWide, kBookCopies> pipe;
   uint4 bk;
   down_body_wide<RELU2, 8>(P, A, R, a, ks0, ks1,
                [&]() {

@@ -42,6 +42,8 @@ constexpr int kColsPerGroup = 256;  // output columns per expert tile (4 waves x
 constexpr int kTokPass = 16;        // token slots per MFMA pass (N of 16x16x32)
 constexpr int kMaxE = 1024, kMaxK = 32, kMaxR = 512, kMaxB = 64;
 constexpr int kPdVq = 16;     // code K-steps in flight per wave (4 B per lane each)
+constexpr int kPdVqWide = 8;  // the same in the down tiles of two column groups (large batches; 8 KB of
+                              // codes per wave: measured faster than 12 and 16 steps at batch 16)
 constexpr int kPdGateUp = 8;  // the same for gate/up tiles: half the bytes requested at once when
                               // every tile starts together, the rest as the first steps complete
 constexpr int kPdGateUpWide = 16;  // gate/up code steps in flight in the large-batch kernel: 4 KB of
