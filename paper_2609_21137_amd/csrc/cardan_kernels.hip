@@ -216,6 +216,18 @@ __device__ __forceinline__ double wave_sum(double x) {
   return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
 
+// Sum of a float over the wave, in every lane (the same fixed tree; all
+// lanes active).
+__device__ __forceinline__ float wave_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x111, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x112, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x114, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x118, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x142, 0xA, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x143, 0xC, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
 // x of lane 0 (all lanes active).
 __device__ __forceinline__ double lane0(double x) {
   const long long v = __double_as_longlong(x);
@@ -1984,13 +1996,14 @@ __device__ void item_combine(const Plan& P, const Args& A, const Chain& C, const
     }
   }
   if (want_ssq) {
-    // this column tile's sum of y^2 per token, in thread-slot order, for the
-    // next layer's RMS normalisation
+    // this column tile's sum of y^2 per token (its 64 thread-slot partials
+    // summed by one wave in a fixed tree), for the next layer's RMS
+    // normalisation
     __syncthreads();
-    if (tid < nt) {
-      float sum = 0.0f;
-      for (int i = 0; i < 64; ++i) sum += ssq[tid * 64 + i];
-      C.ssq_out[(size_t)(t0 + tid) * C.nssq + cgq] = sum;
+    const int l = tid & 63;
+    for (int t = w; t < nt; t += 4) {
+      const float sum = wave_sum(ssq[t * 64 + l]);
+      if (l == 0) C.ssq_out[(size_t)(t0 + t) * C.nssq + cgq] = sum;
     }
   }
 }
