@@ -175,6 +175,33 @@ def test_given_routing_with_invalid_and_duplicate_entries(C, case):
     assert err <= HEADROOM, err
 
 
+@pytest.mark.parametrize("B", [40, 64])
+def test_given_routing_block_builders(C, B):
+    """Caller routing with repeats and invalid indices through the
+    block-wide routing-table builder at B * k = 240 and 384 selections (more
+    than one per thread)."""
+    H, I, E, k, d, K, r = 256, 128, 16, 6, 8, 64, 8
+    w = TINY.__class__(f"routing_b{B}", H=H, I=I, E=E, top_k=k, d=d, K=K, r=r, B=B, seed=0)
+    L = synth.make_layer(H, I, E, d, K, r, seed=17)
+    shape = C.shape_of(w)
+    DL = C.DeviceLayer.from_numpy(L)
+    rng = np.random.default_rng(B)
+    idx = rng.integers(0, E, size=(B, k)).astype(np.int32)
+    idx[rng.random(idx.shape) < 0.08] = -1
+    idx[rng.random(idx.shape) < 0.04] = E + 2
+    idx[::5, 1] = idx[::5, 0]  # an expert twice within a token
+    wts = rng.random(idx.shape).astype(np.float32)
+    x_bits = synth.make_input(H, B, seed=9)
+    x = C.bf16_tensor(x_bits)
+    z = C.shared_proj(shape, x, DL.tensors["U_gate"])
+    y = C.vq_lr_expert_ffn(shape, x, torch.from_numpy(idx).cuda(), torch.from_numpy(wts).cuda(), z, DL)
+    torch.cuda.synchronize()
+    ok = (idx >= 0) & (idx < E)
+    y_ref = O.expert_ffn(x_bits, np.where(ok, idx, 0), np.where(ok, wts, 0.0).astype(np.float64), L, d)
+    err = np.abs(y.cpu().numpy() - y_ref).max() / np.abs(y_ref).max()
+    assert err <= HEADROOM, err
+
+
 def test_component_isolation(C):
     """Zero code books (pure low rank) and r = 0 (pure VQ)."""
     w = TINY
