@@ -511,11 +511,16 @@ int cardan_moe_decode_step(const cardan_shape* shape, int32_t B, int32_t n_layer
   uint16_t* xbuf[2] = {reinterpret_cast<uint16_t*>(w + sb.o_x),
                        reinterpret_cast<uint16_t*>(w + sb.o_x) + (size_t)B * shape->H};
   const size_t BH = (size_t)B * shape->H, Bk = (size_t)B * shape->top_k;
+  // Reading the next layer's shared tensors ahead (idle expert-kernel
+  // workgroups) measured slower than not doing it, so it is off unless the
+  // environment variable CARDAN_PREFETCH is "1".
+  const char* pf_env = getenv("CARDAN_PREFETCH");
+  const bool prefetch = pf_env && strcmp(pf_env, "1") == 0;
   for (int l = 0; l < n_layers; ++l) {
     const cardan_layer& L = layers[l];
     const bool last = l == n_layers - 1;
     const int z_sep = shape->r > 0 && L.U_up != L.U_gate;
-    const int flags = base | (l > 0 ? F_NORM_IN : 0) | (last ? 0 : F_SSQ_OUT | F_PREFETCH);
+    const int flags = base | (l > 0 ? F_NORM_IN : 0) | (last ? 0 : F_SSQ_OUT | (prefetch ? F_PREFETCH : 0));
     const Plan P = make_plan(shape, B, z_sep, flags);
     uint16_t* xin = l == 0 ? nullptr : (x_norm ? x_norm + (size_t)(l - 1) * BH : xbuf[l % 2]);
     Args A = args_for(&L, w);

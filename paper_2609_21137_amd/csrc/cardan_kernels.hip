@@ -2052,14 +2052,26 @@ __device__ __forceinline__ void clear_ints(int* p, int n, int stride = 1) {
 // barrier vote (which, if it ever held, would count into the sink counter).
 __device__ void prefetch_next_layer(const Args& A, const Chain& C, int part, int parts) {
   unsigned acc = 0;
+  // each thread's first line of every tensor, all loads issued together
+  // (an absent tensor or a thread past its share reads the out-of-range
+  // offset: no memory access)
+#pragma unroll
   for (int j = 0; j < kPrefetchTensors; ++j) {
-    const uint32_t n = C.pf_bytes[j];
-    if (!C.pf[j] || n == 0) continue;
+    const uint32_t n = C.pf[j] ? C.pf_bytes[j] : 0u;
+    const uint32_t lines = (n + 127) / 128;
+    const uint32_t l0 = (uint32_t)((uint64_t)lines * part / parts);
+    const uint32_t l1 = (uint32_t)((uint64_t)lines * (part + 1) / parts);
+    const uint32_t li = l0 + threadIdx.x;
+    acc ^= __builtin_amdgcn_raw_buffer_load_b32(make_rsrc(C.pf[j], n), li < l1 ? li * 128 : kOob, 0, 0);
+  }
+  // shares of more lines than threads (few idle workgroups)
+  for (int j = 0; j < kPrefetchTensors; ++j) {
+    const uint32_t n = C.pf[j] ? C.pf_bytes[j] : 0u;
     const uint32_t lines = (n + 127) / 128;
     const uint32_t l0 = (uint32_t)((uint64_t)lines * part / parts);
     const uint32_t l1 = (uint32_t)((uint64_t)lines * (part + 1) / parts);
     const rsrc_t rs = make_rsrc(C.pf[j], n);
-    for (uint32_t li = l0 + threadIdx.x; li < l1; li += kWG)
+    for (uint32_t li = l0 + threadIdx.x + kWG; li < l1; li += kWG)
       acc ^= __builtin_amdgcn_raw_buffer_load_b32(rs, li * 128, 0, 0);
   }
   if (__syncthreads_or(acc == 0x5EED5EEDu) && threadIdx.x == 0) atomicAdd(ctr(A, C_SINK), 1);

@@ -9,10 +9,13 @@ Per layer: top-k identical (after the oracle's margin check), affinities
 within 1e-5; the last layer's y within the 2e-2 bar and the 1e-4 headroom
 bar; every x_{l+1} within one bf16 step (relative) plus the headroom bar
 (normwise) of the oracle's RMSNorm of the oracle's y_l. A one-layer step equals cardan_moe_layer bit for bit; the step
-without x_norm equals the step with it; graph replays equal the eager call.
+without x_norm equals the step with it, and with the next layer's shared
+tensors read ahead (CARDAN_PREFETCH=1) too; graph replays equal the eager
+call.
 """
 
 import dataclasses
+import os
 import sys
 
 import numpy as np
@@ -87,6 +90,16 @@ def test_decode_step_teacher_forced(C, wname, n_layers):
     y2, idx2, wt2 = C.moe_decode_step(shape, x0, DLs, EPS, ws=ws2)
     torch.cuda.synchronize()
     assert torch.equal(y2, y) and torch.equal(idx2, idx) and torch.equal(wt2, wt)
+
+    # reading the next layer's shared tensors ahead (opt-in) changes nothing
+    os.environ["CARDAN_PREFETCH"] = "1"
+    try:
+        y3, idx3, wt3 = C.moe_decode_step(shape, x0, DLs, EPS, ws=ws2)
+        torch.cuda.synchronize()
+    finally:
+        del os.environ["CARDAN_PREFETCH"]
+    assert C.workspace_status(ws2) == 0
+    assert torch.equal(y3, y) and torch.equal(idx3, idx) and torch.equal(wt3, wt)
 
     # HIP graph replays reproduce the eager call bit for bit
     yg = torch.empty_like(y)
