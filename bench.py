@@ -344,8 +344,8 @@ def time_decode_step(C, torch, w, steps, warmup, layers_cache):
     (bf16) into the next layer's input. Two forms of the same step, each
     captured once as a HIP graph and replayed (eager launches are the
     fallback): the library's decode step (cardan_moe_decode_step: the
-    normalisation inside the next layer's routing kernel, the next layer's
-    shared tensors read ahead; two kernels per layer) and the unfused chain
+    normalisation inside the next layer's routing kernel; two kernels per
+    layer) and the unfused chain
     (cardan_moe_layer, then cardan_rmsnorm_bf16: three kernels per layer).
     Per-step latency: an event pair around every replay."""
     import ctypes
@@ -435,8 +435,7 @@ def time_decode_step(C, torch, w, steps, warmup, layers_cache):
     _, wall_u, med_u, lo_u, hi_u = measure(unfused)
     bytes_step = sum(compressed_bytes(w, a)["compressed"] for a in n_act)
     return {"workload": w.name, "B": B, "layers": L, "distinct_layers": len(dls), "mode": mode,
-            "form": "cardan_moe_decode_step (normalisation fused into the next routing kernel, "
-                    "next-layer prefetch)",
+            "form": "cardan_moe_decode_step (normalisation fused into the next routing kernel)",
             "ms_per_step": round(1e3 * wall / steps, 4),
             "ms_per_step_median": round(med, 4), "ms_per_step_ci95": [round(lo, 4), round(hi, 4)],
             "us_per_layer": round(1e6 * wall / steps / L, 3),
