@@ -194,9 +194,11 @@ int cardan_moe_layer_relu2(const cardan_shape* shape, int32_t B, const cardan_bf
  * the normalised inputs of layers 1..n_layers-1 as [n_layers - 1][B][H] bf16.
  * The normalisation runs inside the next layer's routing kernel (the layer's
  * combine writes per-token partial sums of y^2), so a layer costs two kernel
- * launches; the expert kernel's idle workgroups read the next layer's router
- * weights, bases and code books ahead of its routing kernel (the paper's
- * overlap of routing-independent reads, Sec. 4.1). ws: at least
+ * launches. With the environment variable CARDAN_PREFETCH set to "1" the
+ * expert kernel's idle workgroups also read the next layer's router weights,
+ * bases and code books ahead of its routing kernel (the paper's overlap of
+ * routing-independent reads, Sec. 4.1); it changes no output and is off by
+ * default because it measured slower. ws: at least
  * cardan_workspace_bytes(shape, B) bytes; one workspace serves every layer.
  * 1 <= n_layers <= 4096, eps finite and >= 0. */
 int cardan_moe_decode_step(const cardan_shape* shape, int32_t B, int32_t n_layers, const cardan_bf16* x0,
